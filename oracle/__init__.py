@@ -1,0 +1,44 @@
+"""CPU oracle for the FarSkip MoE block forward -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product path (the HIP library and its Python
+binding) never imports, calls or links anything here, and this package
+imports nothing from the product path.
+
+What it computes is the plain definition of one FarSkip MoE block on one
+expert-parallel rank's share (Section 2.1: the MoE layer, Dispatch and
+Combine; Section 3: the FarSkip residual, Eq. 7 with the outdated input of
+Eq. 8a for the MoE and the partial input of Eq. 8b for the next layer).
+Floating point is fp64 on values decoded exactly from the fp32/bf16 inputs.
+Routing decisions are taken from fp32 logits summed in the documented fixed
+order (``logits_routing_f32``), because the kernel takes them in fp32.
+
+Parity status per function (what pins it is in tests/test_oracle_pins.py):
+  logits_f64, logits_routing_f32 ... pinned (exact integer cases, error bound)
+  route ............................ pinned (brute force over subsets)
+  dispatch_plan, pack .............. pinned (stable argsort, bijection)
+  receive_rows ..................... pinned (per-source decomposition)
+  swiglu ........................... pinned (closed forms)
+  combine, moe_block ............... pinned (dense masked brute force)
+  farskip_pair, regular_pair ....... pinned (zero-output equality, conservation)
+"""
+
+from .moe import (  # noqa: F401
+    ROUTER_SLICE,
+    logits_f64,
+    logits_routing_f32,
+    route,
+    dispatch_plan,
+    pack,
+    receive_rows,
+    silu,
+    swiglu,
+    shared_ffn,
+    combine,
+    moe_block,
+    moe_tokens_direct,
+    farskip_pair,
+    regular_pair,
+    residual_add,
+    dense_linear,
+)

@@ -1,0 +1,375 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Every check here compares the oracle with something other than itself: a
+hand-derived value, a closed form, an exact integer result, a library routine
+(stable argsort, bincount, scipy softmax), brute force over subsets, or an
+invariant of the FarSkip residual (Section 3, Eqs. 6-8).  The paper prints no
+worked numeric example for the block, so there is no printed fixture.
+"""
+
+import itertools
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+def bf16_values(a):
+    """Round fp32 values to bf16-representable fp32 values (RNE)."""
+    u = np.asarray(a, np.float32).view(np.uint32).astype(np.uint64)
+    u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32)
+
+
+# ---------------------------------------------------------------- O1 logits
+def test_routing_logits_exact_on_integers():
+    # Small integers: every partial sum is an integer below 2^24, so the fp32
+    # order-fixed sum must equal the exact integer matmul, for a d that is not
+    # a multiple of the slice length (ragged last slice).
+    g = rng(0)
+    x = g.integers(-8, 9, size=(5, 700)).astype(np.float32)
+    w = g.integers(-8, 9, size=(7, 700)).astype(np.float32)
+    exact = x.astype(np.int64) @ w.astype(np.int64).T
+    z = oracle.logits_routing_f32(x, w)
+    assert np.array_equal(z.astype(np.int64), exact)
+    assert np.array_equal(oracle.logits_f64(x, w), exact.astype(np.float64))
+
+
+def test_routing_logits_order_hand_value():
+    # d = 512 = two slices.  Slice 0 holds 2^24 followed by 255 ones: every
+    # fp32 add of 1 to 2^24 rounds back to 2^24 (tie to even), so slice 0
+    # sums to 2^24.  Slice 1 holds 256 ones and sums to 256 exactly.  The
+    # final add gives 2^24 + 256, which is representable.  The exact sum
+    # would be 2^24 + 511.
+    x = np.ones((1, 512), np.float32)
+    w = np.ones((1, 512), np.float32)
+    w[0, 0] = 2.0 ** 24
+    z = oracle.logits_routing_f32(x, w)
+    assert z[0, 0] == np.float32(16777472.0)
+    assert oracle.logits_f64(x, w)[0, 0] == 16777216.0 + 511.0
+
+
+def test_routing_logits_error_bound():
+    # Recursive-summation error bound: each product rounds once and passes
+    # through at most (slice - 1) + n_slices additions.
+    g = rng(1)
+    d = 2048 + 192
+    x = bf16_values(g.standard_normal((16, d)))
+    w = bf16_values(0.02 * g.standard_normal((24, d)))
+    z32 = oracle.logits_routing_f32(x, w).astype(np.float64)
+    z64 = oracle.logits_f64(x, w)
+    n_add = oracle.ROUTER_SLICE + math.ceil(d / oracle.ROUTER_SLICE) + 1
+    u = 2.0 ** -24
+    bound = 1.01 * n_add * u * (np.abs(x.astype(np.float64)) @ np.abs(w.astype(np.float64)).T)
+    assert np.all(np.abs(z32 - z64) <= bound)
+
+
+# ---------------------------------------------------------------- O2-O6 route
+def test_route_sigmoid_hand_example():
+    # z = [0, ln 3, -ln 3, ln 7] -> sigmoid = [1/2, 3/4, 1/4, 7/8].
+    z = np.array([[0.0, math.log(3), -math.log(3), math.log(7)]])
+    ids, w, near, _ = oracle.route(z, "sigmoid", 2, norm_topk=False)
+    assert ids.tolist() == [[3, 1]]
+    assert np.allclose(w, [[7 / 8, 3 / 4]], rtol=0, atol=1e-15)
+    ids, w, near, _ = oracle.route(z, "sigmoid", 2, norm_topk=True, routed_scale=2.5)
+    assert np.allclose(w, [[2.5 * 7 / 13, 2.5 * 6 / 13]], rtol=0, atol=1e-15)
+    assert not near.any()
+
+
+def test_route_bias_changes_selection_not_weights():
+    z = np.array([[2.0, 1.0, 0.0, -1.0]])
+    bias = np.array([0.0, 0.0, 0.0, 5.0])
+    ids, w, _, _ = oracle.route(z, "sigmoid", 1, bias=bias)
+    assert ids.tolist() == [[3]]
+    assert w[0, 0] == pytest.approx(1.0 / (1.0 + math.exp(1.0)), abs=1e-15)
+
+
+def test_route_softmax_weights_and_ties():
+    g = rng(2)
+    z = g.standard_normal((9, 6)).astype(np.float32)
+    # k = E, no renormalisation: weights are the softmax over all experts,
+    # checked against scipy's softmax.
+    ids, w, near, _ = oracle.route(z, "softmax", 6)
+    p = scipy.special.softmax(z.astype(np.float64), axis=1)
+    assert np.allclose(np.take_along_axis(p, ids.astype(np.int64), axis=1), w, atol=1e-15)
+    assert np.allclose(w.sum(1), 1.0, atol=1e-14)
+    assert not near.any()
+    # equal logits: the lower expert index wins and comes first
+    zt = np.array([[0.5, 1.0, 1.0, 1.0, -2.0]], np.float32)
+    ids, _, _, _ = oracle.route(zt, "softmax", 2)
+    assert ids.tolist() == [[1, 2]]
+
+
+def _brute_route(keys, k, G, tg):
+    """Selection by exhaustive search: the kept groups are the tg-subset of
+    groups with the largest total group score, where a group's score is the
+    largest sum over pairs of its keys; the selected experts are the k-subset
+    of allowed experts with the largest key sum; slot order by key."""
+    E = len(keys)
+    gsz = E // G
+    if G > 1:
+        def gscore(gi):
+            ks = keys[gi * gsz:(gi + 1) * gsz]
+            return max(a + b for a, b in itertools.combinations(ks, 2)) if gsz >= 2 else ks[0]
+        gs = [gscore(gi) for gi in range(G)]
+        best = max(itertools.combinations(range(G), tg), key=lambda c: sum(gs[i] for i in c))
+        allowed = [e for e in range(E) if e // gsz in best]
+    else:
+        allowed = list(range(E))
+    sel = max(itertools.combinations(allowed, k), key=lambda c: sum(keys[e] for e in c))
+    return sorted(sel, key=lambda e: -keys[e])
+
+
+@pytest.mark.parametrize("score,G,tg,k", [("softmax", 1, 1, 3), ("sigmoid", 1, 1, 2),
+                                          ("sigmoid", 4, 2, 3), ("softmax", 3, 1, 2),
+                                          ("sigmoid", 2, 1, 1)])
+def test_route_matches_brute_force(score, G, tg, k):
+    g = rng(3)
+    E = 12
+    bias = 0.3 * g.standard_normal(E) if score == "sigmoid" else None
+    for _ in range(40):
+        z = g.standard_normal((1, E))
+        ids, _, near, _ = oracle.route(z, score, k, G, tg, bias=bias)
+        keys = z[0] if score == "softmax" else 1 / (1 + np.exp(-z[0])) + bias
+        assert ids[0].tolist() == _brute_route(list(keys), k, G, tg)
+        assert not near.any()
+
+
+def test_route_flags_near_ties():
+    z = np.array([[0.3, 0.3 + 1e-9, -1.0]])
+    _, _, near, margin = oracle.route(z, "sigmoid", 1)
+    assert near[0] and margin[0] < 1e-6
+    _, _, near, _ = oracle.route(np.array([[0.3, 0.9, -1.0]]), "sigmoid", 1)
+    assert not near[0]
+
+
+# ---------------------------------------------------------------- O7-O8 plan/pack
+def test_plan_hand_example():
+    ids = np.array([[1, 0], [0, 2], [1, 2]])
+    p = oracle.dispatch_plan(ids, 3, ep_size=3)
+    assert p["counts"].tolist() == [2, 2, 2]
+    assert p["offsets"].tolist() == [0, 2, 4, 6]
+    assert p["slot_to_row"].tolist() == [2, 0, 1, 4, 3, 5]
+    assert p["row_to_slot"].tolist() == [1, 2, 0, 4, 3, 5]
+    assert p["rank_offsets"].tolist() == [0, 2, 4, 6]
+
+
+@pytest.mark.parametrize("N,E,k,R", [(1, 4, 1, 1), (37, 16, 4, 4), (200, 64, 6, 8), (5, 8, 8, 2)])
+def test_plan_is_stable_sort_and_bijection(N, E, k, R):
+    g = rng(N + E)
+    ids = np.stack([g.choice(E, size=k, replace=False) for _ in range(N)])
+    p = oracle.dispatch_plan(ids, E, R)
+    flat = ids.reshape(-1)
+    assert np.array_equal(p["counts"], np.bincount(flat, minlength=E))
+    assert np.array_equal(p["offsets"], np.concatenate([[0], np.cumsum(np.bincount(flat, minlength=E))]))
+    assert np.array_equal(p["row_to_slot"], np.argsort(flat, kind="stable"))
+    assert np.array_equal(np.sort(p["slot_to_row"]), np.arange(N * k))
+    assert np.array_equal(p["row_to_slot"][p["slot_to_row"]], np.arange(N * k))
+    assert np.array_equal(p["rank_offsets"], p["offsets"][::E // R])
+    x = g.standard_normal((N, 3))
+    send = oracle.pack(x, p["slot_to_row"], k)
+    assert np.array_equal(send, x[np.argsort(flat, kind="stable") // k])
+
+
+# ---------------------------------------------------------------- O9 receive
+def test_receive_rows_decomposition():
+    g = rng(5)
+    R, N, E, k, r = 4, 19, 16, 3, 2
+    E_loc, cap = E // R, N * k
+    plans, ids_all = [], []
+    for s in range(R):
+        ids = np.stack([g.choice(E, size=k, replace=False) for _ in range(N)])
+        ids_all.append(ids)
+        plans.append(oracle.dispatch_plan(ids, E, R))
+    rows, goff = oracle.receive_rows(np.stack([p["counts"] for p in plans]),
+                                     np.stack([p["offsets"] for p in plans]), cap, r, E_loc)
+    # brute force: scan every source's slots in (source, token) order
+    for e in range(E_loc):
+        want = []
+        for s in range(R):
+            for t in range(N):
+                for j in range(k):
+                    if ids_all[s][t, j] == r * E_loc + e:
+                        want.append(s * cap + plans[s]["slot_to_row"][t * k + j])
+        assert rows[goff[e]:goff[e + 1]].tolist() == want
+
+
+# ---------------------------------------------------------------- O10 SwiGLU
+def test_swiglu_scalar_and_roles():
+    # d = F = 1: x = 2, gate 1, up 3, down 0.5 -> SiLU(2) * 6 * 0.5
+    y = oracle.swiglu([[2.0]], [[1.0], [3.0]], [[0.5]])
+    assert y[0, 0] == pytest.approx(3.0 * 2.0 / (1.0 + math.exp(-2.0)), rel=1e-15)
+    assert oracle.silu([1.0])[0] == pytest.approx(0.7310585786300049, rel=1e-15)
+    assert oracle.silu([0.0])[0] == 0.0
+    assert oracle.silu([-800.0])[0] == 0.0
+
+
+def test_swiglu_identity_weights():
+    g = rng(6)
+    d = 5
+    x = g.standard_normal((4, d))
+    gu = np.concatenate([np.eye(d), np.eye(d)])
+    y = oracle.swiglu(x, gu, np.eye(d))
+    assert np.allclose(y, x * x / (1 + np.exp(-x)), rtol=1e-14, atol=0)
+    # a permuted down projection moves output columns
+    P = np.eye(d)[::-1]
+    assert np.allclose(oracle.swiglu(x, gu, P), (x * x / (1 + np.exp(-x)))[:, ::-1], rtol=1e-14)
+
+
+# ---------------------------------------------------------------- whole block
+def _tiny_cfg(**kw):
+    from workloads.configs import MoEConfig
+    base = dict(name="t", n_tokens=11, hidden=8, n_experts=6, top_k=2, ffn=4,
+                score="softmax", norm_topk=False, dtype="f32", seed=0, next_linear=True)
+    base.update(kw)
+    return MoEConfig(**base)
+
+
+def _tiny_inputs(cfg, g):
+    R, N, d, E, F = cfg.ep_size, cfg.n_tokens, cfg.hidden, cfg.n_experts, cfg.ffn
+    x_all = g.standard_normal((R, N, d)).astype(np.float32)
+    wr = (0.5 * g.standard_normal((E, d))).astype(np.float32)
+    gu = (0.3 * g.standard_normal((cfg.n_local, 2 * F, d))).astype(np.float32)
+    dn = (0.3 * g.standard_normal((cfg.n_local, d, F))).astype(np.float32)
+    bias = (0.1 * g.standard_normal(E)).astype(np.float32) if cfg.score == "sigmoid" else None
+    yr = g.standard_normal((cfg.cap, d)).astype(np.float32) if R > 1 else None
+    return x_all, wr, bias, gu, dn, yr
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(score="sigmoid", norm_topk=True),
+                                dict(score="sigmoid", n_groups=3, topk_groups=2, top_k=3),
+                                dict(ep_size=3, ep_rank=1), dict(ep_size=2, ep_rank=0, score="sigmoid")])
+def test_block_packed_equals_dense_masked(kw):
+    # P6: evaluate every expert on every token and mask by the selection;
+    # no plan, no pack.  Remote experts' rows come from the return buffer.
+    cfg = _tiny_cfg(**kw)
+    g = rng(7)
+    x_all, wr, bias, gu, dn, yr = _tiny_inputs(cfg, g)
+    out = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, y_remote=yr)
+    me = out["me"]
+    x = x_all[cfg.ep_rank].astype(np.float64)
+    dense = np.zeros_like(x)
+    lo = cfg.ep_rank * cfg.n_local
+    for t in range(cfg.n_tokens):
+        for j in range(cfg.top_k):
+            e = me["ids"][t, j]
+            if lo <= e < lo + cfg.n_local:
+                ye = (oracle.silu(x[t] @ gu[e - lo][:cfg.ffn].T) * (x[t] @ gu[e - lo][cfg.ffn:].T)) @ dn[e - lo].T
+            else:
+                ye = yr[me["plan"]["slot_to_row"][t * cfg.top_k + j]]
+            dense[t] += me["w"][t, j] * ye
+    assert np.allclose(out["routed"], dense, rtol=1e-12, atol=1e-12)
+
+
+def test_block_ep_decomposition():
+    # P8: the R-rank path gives each received row the output of its expert
+    # applied to the token that sent it.
+    cfg = _tiny_cfg(ep_size=3, ep_rank=2, n_experts=6)
+    g = rng(8)
+    x_all, wr, bias, gu, dn, yr = _tiny_inputs(cfg, g)
+    out = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, y_remote=yr)
+    for e in range(cfg.n_local):
+        for row in out["group_rows"][out["group_offsets"][e]:out["group_offsets"][e + 1]]:
+            s, pos = divmod(int(row), cfg.cap)
+            slot = out["src"][s]["plan"]["row_to_slot"][pos]
+            t = slot // cfg.top_k
+            assert out["src"][s]["ids"][t, slot % cfg.top_k] == cfg.ep_rank * cfg.n_local + e
+            want = oracle.swiglu(x_all[s][t:t + 1], gu[e], dn[e])[0]
+            assert np.allclose(out["y"][row], want, rtol=1e-13, atol=1e-13)
+
+
+def test_dense_mixture_special_case():
+    # P7: k = E with softmax and no renormalisation is the dense mixture
+    # sum_e p_e MLP_e(x) with p the softmax over all experts.
+    cfg = _tiny_cfg(top_k=6)
+    g = rng(9)
+    x_all, wr, _, gu, dn, _ = _tiny_inputs(cfg, g)
+    out = oracle.moe_block(cfg, x_all, wr, None, gu, dn)
+    x = x_all[0].astype(np.float64)
+    p = scipy.special.softmax(oracle.logits_routing_f32(x_all[0], wr).astype(np.float64), axis=1)
+    want = sum(p[:, e:e + 1] * oracle.swiglu(x, gu[e], dn[e]) for e in range(6))
+    assert np.allclose(out["routed"], want, rtol=1e-12, atol=1e-12)
+
+
+def test_identical_experts_reduce_to_dense_mlp():
+    # P5: identical experts with renormalised top-k weights: sum_j G_j = 1,
+    # so the MoE equals the one MLP, whatever the routing.
+    cfg = _tiny_cfg(score="sigmoid", norm_topk=True, top_k=3)
+    g = rng(10)
+    x_all, wr, bias, gu, dn, _ = _tiny_inputs(cfg, g)
+    gu[:] = gu[0]
+    dn[:] = dn[0]
+    out = oracle.moe_block(cfg, x_all, wr, bias, gu, dn)
+    x = x_all[0].astype(np.float64)
+    g1 = x @ gu[0][:cfg.ffn].T.astype(np.float64)
+    u1 = x @ gu[0][cfg.ffn:].T.astype(np.float64)
+    want = (g1 / (1 + np.exp(-g1)) * u1) @ dn[0].T.astype(np.float64)
+    assert np.allclose(out["routed"], want, rtol=1e-12, atol=1e-12)
+    # E = 1, k = 1: a plain MLP
+    cfg1 = _tiny_cfg(n_experts=1, top_k=1)
+    out1 = oracle.moe_block(cfg1, x_all, wr[:1], None, gu[:1], dn[:1])
+    assert np.allclose(out1["routed"], want, rtol=1e-12, atol=1e-12)
+
+
+def test_shared_experts_sum():
+    g = rng(11)
+    x = g.standard_normal((3, 4))
+    a = g.standard_normal((2, 6, 4))
+    b = g.standard_normal((2, 4, 3))
+    want = oracle.swiglu(x, a[0], b[0]) + oracle.swiglu(x, a[1], b[1])
+    assert np.allclose(oracle.shared_ffn(x, a, b), want, rtol=1e-14)
+
+
+# ---------------------------------------------------------------- O14 FarSkip pair
+def test_zero_moe_output_farskip_equals_regular():
+    # P3 (Eq. 6 vs Eq. 7 with f = 0): with zero routed output the FarSkip
+    # pair and the regular pair are the same computation.
+    cfg = _tiny_cfg()
+    g = rng(12)
+    x_all, wr, _, gu, dn, _ = _tiny_inputs(cfg, g)
+    dn[:] = 0
+    out = oracle.moe_block(cfg, x_all, wr, None, gu, dn)
+    assert not out["routed"].any()
+    wn = g.standard_normal((cfg.hidden, cfg.hidden))
+    shared = g.standard_normal(out["x"].shape)
+    fs, _, _ = oracle.farskip_pair(out["x"], shared, out["routed"], wn)
+    rg, _, _ = oracle.regular_pair(out["x"], shared, out["routed"], wn)
+    assert np.array_equal(fs, rg)
+
+
+def test_farskip_conservation_and_dropped_input():
+    # P4 (Eq. 7, Section 3): every block output is added once into the final
+    # residual; the next layer's input lacks exactly the routed output.
+    g = rng(13)
+    x, sh, ro = g.standard_normal((3, 4, 5))
+    wn = g.standard_normal((5, 5))
+    out, partial, nxt = oracle.farskip_pair(x, sh, ro, wn)
+    assert np.allclose(out - x, sh + nxt + ro, rtol=1e-14, atol=1e-14)
+    assert np.allclose(partial, x + sh, rtol=0, atol=0)
+    assert np.allclose(nxt, (x + sh) @ wn.T, rtol=1e-14)
+    rout, r1, rn = oracle.regular_pair(x, sh, ro, wn)
+    assert np.allclose(rn, (x + sh + ro) @ wn.T, rtol=1e-14)
+    # a stack of L FarSkip layers: the final residual holds every layer's
+    # outputs exactly once, and layer l+1's dense input misses only layer l's
+    # routed part.
+    L = 4
+    o = x.copy()
+    total = x.copy()
+    pending = np.zeros_like(x)
+    for layer in range(L):
+        o = o + pending
+        shl, rol = g.standard_normal((2, 4, 5))
+        out_l, part_l, nxt_l = oracle.farskip_pair(o, shl, rol, wn)
+        assert np.allclose(part_l, o + shl)
+        total = total + shl + nxt_l + rol
+        o = out_l - rol
+        pending = rol
+    o = o + pending
+    assert np.allclose(o, total, rtol=1e-13, atol=1e-13)
