@@ -1,0 +1,306 @@
+/*
+ * farskip.h -- C ABI of libfarskip.so: the forward pass of one FarSkip MoE
+ * block on one expert-parallel (EP) rank's share, on an AMD Instinct MI355X
+ * (gfx950).
+ *
+ * What is computed (arXiv 2511.11505):
+ *   Section 2.1  MoE(A) = sum_j G(A)_j MLP^j(A), G(A) = s(A W_R^T); experts
+ *                are split over EP ranks; Dispatch permutes A and sends each
+ *                token row to the ranks of its experts; Combine returns the
+ *                expert outputs and sums them with the gate weights; shared
+ *                experts run on every token.  The expert MLP is read as
+ *                SwiGLU: (SiLU(A Wg^T) * (A Wu^T)) Wd^T.
+ *   Section 3    FarSkip residual (Eq. 7): the next layer reads an input
+ *                that lacks this block's routed-expert output (the partial
+ *                input of Eq. 8b: residual + shared-expert output); the MoE
+ *                itself reads the outdated residual o_{k-1} (Eq. 8a); the
+ *                routed output is added into the residual afterwards.
+ *   Section 4.1  Dispatch overlaps the next computation; the gate and the
+ *                routed experts are the parts that cannot overlap (Eq. 9).
+ *
+ * Conventions shared by every entry point
+ *   Memory      Every array argument is DEVICE memory owned by the caller,
+ *               row-major with the leading dimension stated.  The library
+ *               never allocates or frees device memory; scratch space is a
+ *               caller-provided workspace sized by fs_workspace_size().
+ *   Alignment   Device pointers must be 16-byte aligned.
+ *   Element     FS_F32 or FS_BF16 selects the type of tokens, weights,
+ *   types       expert outputs and residuals (desc->dtype); router logits,
+ *               gate weights and the selection bias are always fp32;
+ *               accumulation is always fp32; index arrays are int32.
+ *   Streams     Calls enqueue work on the given HIP stream (a hipStream_t
+ *               passed as void*, NULL = the null stream) and return without
+ *               synchronising.
+ *   Errors      Argument checks run on the host before anything is
+ *               enqueued: FS_ERR_INVALID (bad value or pointer),
+ *               FS_ERR_UNSUPPORTED (valid but outside what the kernels
+ *               handle), FS_ERR_WORKSPACE (workspace too small).  A failing
+ *               HIP call returns FS_ERR_HIP.  fs_last_error_message() gives
+ *               the detail for the calling thread.  Device faults surface at
+ *               the caller's next synchronisation.  The library never
+ *               aborts and never prints.
+ *   Shapes      hidden % 64 == 0, ffn % 64 == 0, 1 <= top_k <= min(E, 32),
+ *               E <= 512, E % n_groups == 0, n_groups <= 64,
+ *               top_k <= topk_groups * E / n_groups, E % ep_size == 0,
+ *               ep_size * n_tokens * top_k < 2^31.  n_tokens == 0 is a
+ *               valid no-op.
+ */
+#ifndef FARSKIP_H
+#define FARSKIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FS_ABI_VERSION 1
+
+typedef enum {
+  FS_OK = 0,
+  FS_ERR_INVALID = 1,
+  FS_ERR_UNSUPPORTED = 2,
+  FS_ERR_WORKSPACE = 3,
+  FS_ERR_HIP = 4
+} fs_status;
+
+typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
+typedef enum { FS_SOFTMAX = 0, FS_SIGMOID = 1 } fs_score;
+typedef enum { FS_PHASE_ALL = 0, FS_PHASE_BEGIN = 1, FS_PHASE_FINISH = 2 } fs_phase;
+typedef enum {
+  FS_OP_ROUTER_TOPK = 0,
+  FS_OP_DISPATCH_PACK = 1,
+  FS_OP_GROUPED_FFN = 2,
+  FS_OP_BLOCK = 3
+} fs_op;
+
+/* One MoE block on one EP rank (Section 2.1).  A plain host struct, read
+ * only during the call. */
+typedef struct {
+  int32_t abi_version;   /* FS_ABI_VERSION */
+  int32_t n_tokens;      /* N: tokens this rank routes (its own batch) */
+  int32_t hidden;        /* d */
+  int32_t n_experts;     /* E: routed experts over all ranks */
+  int32_t top_k;         /* k */
+  int32_t n_groups;      /* G: expert groups for group-limited routing; 1 = off */
+  int32_t topk_groups;   /* groups kept per token when G > 1 */
+  int32_t score;         /* fs_score */
+  int32_t norm_topk;     /* 1: renormalise the k gate weights to sum to 1 */
+  float routed_scale;    /* gate weights are multiplied by this last */
+  int32_t ffn;           /* F: routed expert width */
+  int32_t n_shared;      /* S: shared experts (0 = none) */
+  int32_t ffn_shared;    /* width of each shared expert */
+  int32_t ep_size;       /* R */
+  int32_t ep_rank;       /* r: owns experts [r*E/R, (r+1)*E/R) */
+  int32_t dtype;         /* fs_dtype */
+} fs_moe_desc;
+
+typedef void* fs_stream; /* a hipStream_t */
+
+const char* fs_status_string(int32_t status);
+const char* fs_last_error_message(void);
+int32_t fs_abi_version(void);
+
+/* Bytes of workspace an entry point needs.
+ *   op = FS_OP_ROUTER_TOPK:   fs_router_topk (max_rows, ffn ignored)
+ *   op = FS_OP_DISPATCH_PACK: fs_dispatch_pack (max_rows, ffn ignored)
+ *   op = FS_OP_GROUPED_FFN:   fs_grouped_expert_ffn with up to max_rows rows
+ *                             and width ffn
+ *   op = FS_OP_BLOCK:         fs_moe_block_forward with up to max_rows rows
+ *                             landing on local experts (ffn ignored) */
+fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_rows,
+                            int32_t ffn, size_t* bytes);
+
+/* Router scoring and top-k (Section 2.1: G(A) = s(A W_R^T)).
+ *   x          [N, d] dtype: the MoE input o_{k-1}
+ *   w_router   [E, d] dtype
+ *   sel_bias   [E] fp32 or NULL; sigmoid scoring only: the selection key is
+ *              sigmoid(z) + bias, the gate weight the unbiased sigmoid(z)
+ *   logits_in  [N, E] fp32 or NULL: when given, the logits are taken from
+ *              here and x / w_router are not read
+ *   logits_out [N, E] fp32 or NULL: receives the logits
+ *   topk_ids   [N, k] int32 out: selected experts, descending key order,
+ *              ties to the lower expert index
+ *   topk_w     [N, k] fp32 out: gate weights (softmax over all E experts or
+ *              sigmoid; renormalised over the k when norm_topk; * scale)
+ * Logits are fp32 sums in a fixed order: the hidden dimension is cut into
+ * slices of 256 consecutive elements, products are added one at a time in
+ * ascending order within a slice, and slice sums are added in ascending
+ * slice order; every operation rounds to fp32.  With G > 1 a group's score
+ * is the sum of its two largest keys; the topk_groups best groups are kept
+ * (ties to the lower group).  Inputs must be finite. */
+fs_status fs_router_topk(const fs_moe_desc* desc, const void* x, const void* w_router,
+                         const float* sel_bias, const float* logits_in, float* logits_out,
+                         int32_t* topk_ids, float* topk_w, void* ws, size_t ws_bytes,
+                         fs_stream stream);
+
+/* Dispatch plan and pack (Section 2.1, Dispatch: the permutation of A that
+ * precedes the all-to-all).  One send row per (token, selected expert);
+ * rows are ordered by expert, then token, so the buffer is expert-contiguous
+ * and, experts being rank-blocked, rank-contiguous.  Bit-exact and
+ * deterministic (no global atomics).
+ *   topk_ids       [N, k] int32 in: distinct ids in [0, E) per token
+ *   x              [N, d] dtype
+ *   expert_counts  [E] int32 out
+ *   expert_offsets [E+1] int32 out: exclusive prefix sum of the counts
+ *   rank_offsets   [R+1] int32 out: expert_offsets[r * E/R]
+ *   slot_to_row    [N*k] int32 out: send row of slot t*k+j
+ *   row_to_slot    [N*k] int32 out: its inverse
+ *   send           [N*k, d] dtype out: send[slot_to_row[t*k+j]] = x[t] */
+fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
+                           int32_t* expert_counts, int32_t* expert_offsets,
+                           int32_t* rank_offsets, int32_t* slot_to_row, int32_t* row_to_slot,
+                           void* send, void* ws, size_t ws_bytes, fs_stream stream);
+
+/* Rows landing on this rank's experts after Dispatch (Section 2.1).  The
+ * receive buffer holds, for every source rank s, that rank's whole send
+ * buffer at rows [s*N*k, (s+1)*N*k).
+ *   src_counts    [R, E] int32 in: expert_counts of every source rank
+ *   src_offsets   [R, E+1] int32 in: expert_offsets of every source rank
+ *   group_rows    [R*N*k] int32 out: for each local expert e ascending, the
+ *                 rows of source 0, 1, .. R-1 in that source's send order:
+ *                 s*N*k + src_offsets[s][r*E/R + e] + j
+ *   group_offsets [E/R + 1] int32 out: start of each local expert's rows */
+fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
+                          const int32_t* src_offsets, int32_t* group_rows,
+                          int32_t* group_offsets, fs_stream stream);
+
+/* Grouped SwiGLU expert FFN (Section 2.1, MLP^j read as SwiGLU): for each
+ * group g and its rows X_g, Y_g = (SiLU(X_g Wg^T) * (X_g Wu^T)) Wd^T.
+ * bf16 runs on MFMA with fp32 accumulation and the hidden activation
+ * rounded to bf16; fp32 runs on the vector ALUs.
+ *   n_groups      groups (local experts, or 1 for merged shared experts)
+ *   ffn           F of every group
+ *   in_rows       [*, d] dtype: row i of the grouped order is
+ *                 in_rows[group_rows[i]] (or in_rows[i] when group_rows is
+ *                 NULL)
+ *   group_rows    [M] int32 or NULL
+ *   group_offsets [n_groups+1] int32 device, non-decreasing, [0] = 0; NULL
+ *                 only with n_groups == 1, meaning one group of max_rows rows
+ *   max_rows      host-known bound on M = group_offsets[n_groups]; sizes the
+ *                 launch and the workspace (any M <= max_rows is correct)
+ *   w_gate_up     [n_groups, 2F, d] dtype: rows [0,F) gate, [F,2F) up
+ *   w_down        [n_groups, d, F] dtype
+ *   out_rows      [*, d] dtype out: output i goes to out_rows[group_rows[i]]
+ *                 (or out_rows[i]) */
+fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                const void* in_rows, const int32_t* group_rows,
+                                const int32_t* group_offsets, int64_t max_rows,
+                                const void* w_gate_up, const void* w_down, void* out_rows,
+                                void* ws, size_t ws_bytes, fs_stream stream);
+
+/* Combine and unpack (Section 2.1, Combine: weighted sum of the returned
+ * expert outputs), fused with the deferred residual add of Eq. 7.
+ *   acc[t] = sum_{j<k} topk_w[t,j] * y_ret[slot_to_row[t*k+j]]  (fp32, j
+ *            ascending) + shared_out[t] (when given)
+ *   y_ret       [N*k, d] dtype: expert outputs in send order
+ *   shared_out  [N, d] dtype or NULL
+ *   routed_out  [N, d] dtype or NULL: receives acc
+ *   residual    [N, d] dtype or NULL: residual[t] += acc[t], one rounding
+ * At least one of routed_out / residual must be given. */
+fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
+                            const int32_t* slot_to_row, const float* topk_w,
+                            const void* shared_out, void* routed_out, void* residual,
+                            fs_stream stream);
+
+/* FarSkip residual add (Eq. 7): out = residual + deferred (+ extra), in
+ * fp32 with one rounding.  out may equal residual (in place).  [N, d]
+ * dtype each; extra may be NULL. */
+fs_status fs_farskip_residual(const fs_moe_desc* desc, void* out, const void* residual,
+                              const void* deferred, const void* extra, fs_stream stream);
+
+/* Weights of one block.  Shared experts are passed merged into one SwiGLU
+ * of width S*F_s: ws_gate_up [2*S*F_s, d] holds the gate rows of every
+ * shared expert followed by their up rows; ws_down [d, S*F_s]. */
+typedef struct {
+  const void* w_router;   /* [E, d] */
+  const float* sel_bias;  /* [E] or NULL */
+  const void* w_gate_up;  /* [E/R, 2F, d]: this rank's experts */
+  const void* w_down;     /* [E/R, d, F] */
+  const void* ws_gate_up; /* NULL when S = 0 */
+  const void* ws_down;
+} fs_moe_weights;
+
+/* Caller-owned buffers of one block (device memory). */
+typedef struct {
+  float* logits;          /* [N, E] or NULL */
+  int32_t* topk_ids;      /* [N, k] */
+  float* topk_w;          /* [N, k] */
+  int32_t* src_counts;    /* [R, E]: row r written by BEGIN, other rows by the
+                             caller before FINISH (the counts exchange) */
+  int32_t* src_offsets;   /* [R, E+1]: likewise */
+  int32_t* rank_offsets;  /* [R+1] */
+  int32_t* slot_to_row;   /* [N*k] */
+  int32_t* row_to_slot;   /* [N*k] */
+  void* send;             /* [N*k, d] */
+  void* recv;             /* [R*N*k, d]: slot s = source s's send buffer; the
+                             caller fills slots s != r (R > 1); may be NULL
+                             when R = 1 and no comm stream is given */
+  int32_t* group_rows;    /* [R*N*k] (R > 1) */
+  int32_t* group_offsets; /* [E/R+1] (R > 1) */
+  void* y;                /* [R*N*k, d]: expert outputs at their receive row;
+                             slot r is this rank's Combine return y_ret, whose
+                             rows for other ranks' experts the caller fills */
+  void* shared_out;       /* [N, d] (S > 0) */
+} fs_block_buffers;
+
+/* Events that order the two streams of one block. */
+typedef struct fs_block_sync fs_block_sync;
+fs_status fs_block_sync_create(fs_block_sync** out);
+fs_status fs_block_sync_destroy(fs_block_sync* sync);
+
+/* One FarSkip MoE block forward (Section 3 connectivity, Section 4.1
+ * schedule), split in two phases around the far-skipped next computation.
+ *   FS_PHASE_BEGIN on `compute`: router + top-k, plan + pack; then the
+ *     Dispatch stand-in: on `comm` (after an event), a device-to-device copy
+ *     of the whole send buffer into receive slot r; then the shared experts
+ *     on residual_in and partial_out = residual_in + shared_out (Eq. 8b:
+ *     the next layer's input without the routed output).
+ *   The caller then enqueues the next computation on `compute`, reading
+ *     partial_out; it overlaps the copy.
+ *   FS_PHASE_FINISH on `compute`: wait for the copy, receive rows (R > 1),
+ *     grouped SwiGLU experts, Combine and the deferred add
+ *     residual_io += routed (Eq. 7).
+ *   FS_PHASE_ALL runs both with nothing in between.
+ * With comm == NULL the copy runs on `compute` (R > 1) or is skipped and the
+ * experts read `send` (R = 1).  residual_in [N, d] is o_{k-1}, the MoE input
+ * (Eq. 8a); partial_out [N, d]; residual_io [N, d] is updated in place
+ * (normally partial_out after the caller added its next-layer output).
+ * max_recv_rows bounds the rows landing on local experts (N*k when R = 1).
+ * sync may be NULL only with comm == NULL.  One sync object serves one block
+ * at a time: FINISH of a block is enqueued before the next BEGIN that uses
+ * the same object. */
+fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
+                               const fs_moe_weights* weights, const void* residual_in,
+                               void* partial_out, void* residual_io, fs_block_buffers* buffers,
+                               int64_t max_recv_rows, void* ws, size_t ws_bytes,
+                               fs_block_sync* sync, fs_stream compute, fs_stream comm);
+
+/* Dense linear out[m, n] = a[m, :] . w[n, :] in dtype with fp32
+ * accumulation; stands in for the next layer's computation.  a [m, kdim],
+ * w [n, kdim], out [m, n]; kdim % 64 == 0, n % 64 == 0. */
+fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, const void* a,
+                          const void* w, void* out, fs_stream stream);
+
+/* Per-kernel timing with HIP events recorded on the launch stream around
+ * selected kernels.  fs_profile_read synchronises those events. */
+typedef enum {
+  FS_K_ROUTER = 0,
+  FS_K_TOPK = 1,
+  FS_K_PLAN = 2,
+  FS_K_PACK = 3,
+  FS_K_GATE_UP = 4,
+  FS_K_DOWN = 5,
+  FS_K_COMBINE = 6,
+  FS_K_COUNT = 7
+} fs_kernel_id;
+fs_status fs_profile_enable(int32_t on);
+fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);
+fs_status fs_profile_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FARSKIP_H */

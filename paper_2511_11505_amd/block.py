@@ -1,0 +1,126 @@
+"""One FarSkip MoE block on one EP rank: caller-side buffers around the C ABI.
+
+``MoEBlock`` owns the device buffers and workspace of one block and calls
+``fs_moe_block_forward`` for its two phases (Section 3 connectivity, Section
+4.1 schedule).  ``prepare_remote_sources`` sets up, on one GPU, what the
+other EP ranks would have sent: their routing and packed send buffers land
+in their receive slots, their counts in the source-count rows, and the
+Combine return rows of other ranks' experts in this rank's return slot.
+All arithmetic runs in the library's kernels; torch only allocates memory.
+"""
+
+import torch
+
+from . import _lib as L
+from ._lib import make_desc
+
+
+def _dt(cfg):
+    return torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+
+
+class MoEBlock:
+    def __init__(self, cfg, w_router, sel_bias, w_gate_up, w_down, ws_gate_up=None, ws_down=None,
+                 max_recv_rows=None, device="cuda", with_comm=True):
+        self.cfg = cfg
+        self.desc = make_desc(cfg)
+        R, N, d, E, k = cfg.ep_size, cfg.n_tokens, cfg.hidden, cfg.n_experts, cfg.top_k
+        cap = N * k
+        self.cap = cap
+        self.max_recv_rows = cap if max_recv_rows is None else int(max_recv_rows)
+        dt = _dt(cfg)
+        i32 = torch.int32
+        dev = device
+        self.t = dict(
+            logits=torch.empty((N, E), dtype=torch.float32, device=dev),
+            topk_ids=torch.empty((N, k), dtype=i32, device=dev),
+            topk_w=torch.empty((N, k), dtype=torch.float32, device=dev),
+            src_counts=torch.zeros((R, E), dtype=i32, device=dev),
+            src_offsets=torch.zeros((R, E + 1), dtype=i32, device=dev),
+            rank_offsets=torch.empty((R + 1,), dtype=i32, device=dev),
+            slot_to_row=torch.empty((cap,), dtype=i32, device=dev),
+            row_to_slot=torch.empty((cap,), dtype=i32, device=dev),
+            send=torch.empty((cap, d), dtype=dt, device=dev),
+            recv=torch.empty((R * cap, d), dtype=dt, device=dev) if (R > 1 or with_comm) else None,
+            group_rows=torch.empty((R * cap,), dtype=i32, device=dev) if R > 1 else None,
+            group_offsets=torch.empty((E // R + 1,), dtype=i32, device=dev) if R > 1 else None,
+            y=torch.empty((R * cap, d), dtype=dt, device=dev),
+            shared_out=torch.empty((N, d), dtype=dt, device=dev) if cfg.n_shared > 0 else None,
+        )
+        self.weights_keep = (w_router, sel_bias, w_gate_up, w_down, ws_gate_up, ws_down)
+        self.weights = L.fs_moe_weights(L.ptr(w_router), L.ptr(sel_bias), L.ptr(w_gate_up),
+                                        L.ptr(w_down), L.ptr(ws_gate_up), L.ptr(ws_down))
+        self.buffers = L.fs_block_buffers(*[L.ptr(self.t[n]) for n, _ in L.fs_block_buffers._fields_])
+        ws_bytes = L.fs_workspace_size(self.desc, L.FS_OP_BLOCK, self.max_recv_rows)
+        self.ws = torch.empty((max(ws_bytes, 256),), dtype=torch.uint8, device=dev)
+        self.sync = L.fs_block_sync_create()
+
+    def close(self):
+        if self.sync:
+            L.fs_block_sync_destroy(self.sync)
+            self.sync = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_max_recv_rows(self, m):
+        m = int(m)
+        if m != self.max_recv_rows:
+            self.max_recv_rows = m
+            ws_bytes = L.fs_workspace_size(self.desc, L.FS_OP_BLOCK, m)
+            if ws_bytes > self.ws.numel():
+                self.ws = torch.empty((ws_bytes,), dtype=torch.uint8, device=self.ws.device)
+
+    def run(self, phase, residual_in, partial_out, residual_io, compute=None, comm=None):
+        L.fs_moe_block_forward(self.desc, phase, self.weights, residual_in, partial_out,
+                               residual_io, self.buffers, self.max_recv_rows, self.ws,
+                               sync=self.sync if comm is not None else None,
+                               compute=compute, comm=comm)
+
+    def begin(self, residual_in, partial_out, compute=None, comm=None):
+        self.run(L.FS_PHASE_BEGIN, residual_in, partial_out, None, compute, comm)
+
+    def finish(self, residual_in, residual_io, compute=None, comm=None):
+        self.run(L.FS_PHASE_FINISH, residual_in, None, residual_io, compute, comm)
+
+    def y_ret(self):
+        r = self.cfg.ep_rank
+        return self.t["y"][r * self.cap:(r + 1) * self.cap]
+
+
+def prepare_remote_sources(block, x_all, w_router, sel_bias, y_remote, stream=None):
+    """Single-GPU stand-in for the other EP ranks (R > 1).
+
+    For every source rank s != r, run the library's router + top-k and plan
+    + pack on that rank's tokens; the packed send buffer is written straight
+    into receive slot s and the counts / offsets into row s.  Fill this
+    rank's Combine-return slot with the rows other ranks' experts send back.
+    Then run this rank's routing once to learn how many rows land on the
+    local experts (what the counts exchange tells the receiver) and return
+    that number."""
+    cfg = block.cfg
+    R, r, N, E, k = cfg.ep_size, cfg.ep_rank, cfg.n_tokens, cfg.n_experts, cfg.top_k
+    cap = block.cap
+    t = block.t
+    dev = t["send"].device
+    desc = block.desc
+    ids = torch.empty((N, k), dtype=torch.int32, device=dev)
+    w = torch.empty((N, k), dtype=torch.float32, device=dev)
+    ro = torch.empty((R + 1,), dtype=torch.int32, device=dev)
+    s2r = torch.empty((cap,), dtype=torch.int32, device=dev)
+    r2s = torch.empty((cap,), dtype=torch.int32, device=dev)
+    ws_r = torch.empty((max(L.fs_workspace_size(desc, L.FS_OP_ROUTER_TOPK), 256),), dtype=torch.uint8, device=dev)
+    ws_p = torch.empty((max(L.fs_workspace_size(desc, L.FS_OP_DISPATCH_PACK), 256),), dtype=torch.uint8, device=dev)
+    for s in range(R):
+        send_s = t["recv"][s * cap:(s + 1) * cap] if s != r else t["send"]
+        L.fs_router_topk(desc, x_all[s], w_router, sel_bias, None, None, ids, w, ws_r, stream)
+        L.fs_dispatch_pack(desc, ids, x_all[s], t["src_counts"][s], t["src_offsets"][s], ro, s2r, r2s,
+                           send_s, ws_p, stream)
+    if y_remote is not None:
+        block.y_ret().copy_(y_remote)
+    torch.cuda.synchronize()
+    lo = r * (E // R)
+    return int(t["src_counts"][:, lo:lo + E // R].sum().item())

@@ -1,0 +1,621 @@
+// C ABI of libfarskip.so: argument checks, workspace layout, the two-phase
+// FarSkip block driver and per-kernel timing.  Every check runs on the host
+// before anything is enqueued.
+
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/farskip.h"
+#include "internal.hpp"
+
+namespace {
+
+thread_local std::string g_msg;
+
+fs_status fail(fs_status st, const std::string& m) {
+  g_msg = m;
+  return st;
+}
+fs_status hip_fail(hipError_t e, const char* where) {
+  g_msg = std::string(where) + ": " + hipGetErrorString(e);
+  return FS_ERR_HIP;
+}
+#define FS_HIP(expr, where)                     \
+  do {                                          \
+    hipError_t e_ = (expr);                     \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define NEED(ptr, name)                                                                      \
+  do {                                                                                       \
+    if (!(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must not be NULL");        \
+    if (!aligned16(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must be 16-byte aligned"); \
+  } while (0)
+#define OPT(ptr, name)                                                                       \
+  do {                                                                                       \
+    if ((ptr) && !aligned16(ptr))                                                            \
+      return fail(FS_ERR_INVALID, std::string(name) + " must be 16-byte aligned");           \
+  } while (0)
+
+size_t elem(int dtype) { return dtype == FS_F32 ? 4 : 2; }
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+fs_status check_desc(const fs_moe_desc* d) {
+  if (!d) return fail(FS_ERR_INVALID, "desc must not be NULL");
+  if (d->abi_version != FS_ABI_VERSION) return fail(FS_ERR_INVALID, "desc->abi_version mismatch");
+  if (d->n_tokens < 0) return fail(FS_ERR_INVALID, "n_tokens must be >= 0");
+  if (d->hidden <= 0) return fail(FS_ERR_INVALID, "hidden must be > 0");
+  if (d->hidden % 128 != 0) return fail(FS_ERR_UNSUPPORTED, "hidden must be a multiple of 128");
+  if (d->n_experts < 1) return fail(FS_ERR_INVALID, "n_experts must be >= 1");
+  if (d->n_experts > 512) return fail(FS_ERR_UNSUPPORTED, "n_experts must be <= 512");
+  if (d->top_k < 1 || d->top_k > d->n_experts)
+    return fail(FS_ERR_INVALID, "top_k must be in [1, n_experts]");
+  if (d->top_k > 32) return fail(FS_ERR_UNSUPPORTED, "top_k must be <= 32");
+  if (d->n_groups < 1 || d->n_experts % d->n_groups != 0)
+    return fail(FS_ERR_INVALID, "n_groups must divide n_experts");
+  if (d->n_groups > 64) return fail(FS_ERR_UNSUPPORTED, "n_groups must be <= 64");
+  if (d->n_groups > 1) {
+    if (d->topk_groups < 1 || d->topk_groups > d->n_groups)
+      return fail(FS_ERR_INVALID, "topk_groups must be in [1, n_groups]");
+    if (d->top_k > d->topk_groups * (d->n_experts / d->n_groups))
+      return fail(FS_ERR_INVALID, "top_k exceeds the experts of the kept groups");
+  }
+  if (d->score != FS_SOFTMAX && d->score != FS_SIGMOID)
+    return fail(FS_ERR_INVALID, "score must be FS_SOFTMAX or FS_SIGMOID");
+  if (d->norm_topk != 0 && d->norm_topk != 1) return fail(FS_ERR_INVALID, "norm_topk must be 0/1");
+  if (!(d->routed_scale == d->routed_scale)) return fail(FS_ERR_INVALID, "routed_scale is NaN");
+  if (d->ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
+  if (d->ffn % 64 != 0) return fail(FS_ERR_UNSUPPORTED, "ffn must be a multiple of 64");
+  if (d->n_shared < 0) return fail(FS_ERR_INVALID, "n_shared must be >= 0");
+  if (d->n_shared > 0) {
+    if (d->ffn_shared <= 0) return fail(FS_ERR_INVALID, "ffn_shared must be > 0");
+    if ((int64_t)d->n_shared * d->ffn_shared % 64 != 0)
+      return fail(FS_ERR_UNSUPPORTED, "n_shared * ffn_shared must be a multiple of 64");
+  }
+  if (d->ep_size < 1 || d->n_experts % d->ep_size != 0)
+    return fail(FS_ERR_INVALID, "ep_size must divide n_experts");
+  if (d->ep_rank < 0 || d->ep_rank >= d->ep_size) return fail(FS_ERR_INVALID, "ep_rank out of range");
+  if (d->dtype != FS_F32 && d->dtype != FS_BF16) return fail(FS_ERR_INVALID, "dtype must be FS_F32 or FS_BF16");
+  if ((int64_t)d->ep_size * d->n_tokens * d->top_k >= (int64_t)1 << 31)
+    return fail(FS_ERR_UNSUPPORTED, "ep_size * n_tokens * top_k must be < 2^31");
+  return FS_OK;
+}
+
+hipStream_t S(fs_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---------------------------------------------------------------- profiling
+struct ProfState {
+  std::mutex mu;
+  bool on = false;
+  struct Rec {
+    int kernel;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> open;         // recorded, not yet read
+  std::vector<hipEvent_t> pool;  // reusable events
+  hipEvent_t pending[FS_K_COUNT] = {};
+  double total_ms[FS_K_COUNT] = {};
+  int64_t count[FS_K_COUNT] = {};
+};
+ProfState& prof() {
+  static ProfState p;
+  return p;
+}
+hipEvent_t take_event(ProfState& p) {
+  if (!p.pool.empty()) {
+    hipEvent_t e = p.pool.back();
+    p.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// ---------------------------------------------------------------- workspace
+struct Carve {
+  char* base;
+  size_t off = 0;
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  }
+};
+
+size_t router_bytes(const fs_moe_desc* d) {
+  return align256(fs::router_ws_bytes(d->n_tokens, d->hidden, d->n_experts));
+}
+size_t plan_bytes(const fs_moe_desc* d) { return align256(fs::plan_ws_bytes(d->n_tokens, d->n_experts)); }
+
+}  // namespace
+
+namespace fs {
+void prof_begin(int kernel, hipStream_t s) {
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  if (!p.on) return;
+  hipEvent_t e = take_event(p);
+  if (e && hipEventRecord(e, s) == hipSuccess) p.pending[kernel] = e;
+}
+void prof_end(int kernel, hipStream_t s) {
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  if (!p.on || !p.pending[kernel]) return;
+  hipEvent_t e = take_event(p);
+  if (e && hipEventRecord(e, s) == hipSuccess) p.open.push_back({kernel, p.pending[kernel], e});
+  p.pending[kernel] = nullptr;
+}
+}  // namespace fs
+
+extern "C" {
+
+const char* fs_status_string(int32_t status) {
+  switch (status) {
+    case FS_OK: return "FS_OK";
+    case FS_ERR_INVALID: return "FS_ERR_INVALID";
+    case FS_ERR_UNSUPPORTED: return "FS_ERR_UNSUPPORTED";
+    case FS_ERR_WORKSPACE: return "FS_ERR_WORKSPACE";
+    case FS_ERR_HIP: return "FS_ERR_HIP";
+    default: return "FS_ERR_UNKNOWN";
+  }
+}
+
+const char* fs_last_error_message(void) { return g_msg.c_str(); }
+
+int32_t fs_abi_version(void) { return FS_ABI_VERSION; }
+
+fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_rows, int32_t ffn,
+                            size_t* bytes) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (!bytes) return fail(FS_ERR_INVALID, "bytes must not be NULL");
+  if (max_rows < 0) return fail(FS_ERR_INVALID, "max_rows must be >= 0");
+  switch (op) {
+    case FS_OP_ROUTER_TOPK: *bytes = router_bytes(desc); return FS_OK;
+    case FS_OP_DISPATCH_PACK: *bytes = plan_bytes(desc); return FS_OK;
+    case FS_OP_GROUPED_FFN:
+      if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
+      *bytes = fs::ffn_ws_bytes(desc->dtype, max_rows, ffn);
+      return FS_OK;
+    case FS_OP_BLOCK: {
+      size_t b = router_bytes(desc) + plan_bytes(desc);
+      b += fs::ffn_ws_bytes(desc->dtype, max_rows, desc->ffn);
+      if (desc->n_shared > 0)
+        b += fs::ffn_ws_bytes(desc->dtype, desc->n_tokens, desc->n_shared * desc->ffn_shared);
+      *bytes = b;
+      return FS_OK;
+    }
+    default: return fail(FS_ERR_INVALID, "unknown op");
+  }
+}
+
+// ---- router + top-k
+static fs_status router_impl(const fs_moe_desc* d, const void* x, const void* w_router,
+                             const float* sel_bias, const float* logits_in, float* logits_out,
+                             int32_t* topk_ids, float* topk_w, void* ws, hipStream_t s) {
+  const int N = d->n_tokens, D = d->hidden, E = d->n_experts;
+  if (N == 0) return FS_OK;
+  const float* src = logits_in;
+  int n_partials = 0;
+  float* lout = logits_out;
+  if (!logits_in) {
+    Carve c{reinterpret_cast<char*>(ws)};
+    float* scratch_logits = reinterpret_cast<float*>(c.take((size_t)N * E * sizeof(float)));
+    const bool split = fs::router_split(N, D, E);
+    float* dst;
+    if (split) {
+      dst = reinterpret_cast<float*>(c.take((size_t)fs::router_slices(D) * N * E * sizeof(float)));
+      n_partials = fs::router_slices(D);
+    } else {
+      dst = logits_out ? logits_out : scratch_logits;
+      lout = nullptr;  // already written by the router kernel
+    }
+    fs::prof_begin(FS_K_ROUTER, s);
+    FS_HIP(fs::launch_router_logits(d->dtype, x, w_router, N, D, E, split, dst, s), "router");
+    fs::prof_end(FS_K_ROUTER, s);
+    src = dst;
+  } else {
+    lout = (logits_out && logits_out != logits_in) ? logits_out : nullptr;
+  }
+  fs::prof_begin(FS_K_TOPK, s);
+  FS_HIP(fs::launch_topk(src, n_partials, N, E, sel_bias, d->score, d->top_k, d->n_groups,
+                         d->n_groups > 1 ? d->topk_groups : 1, d->norm_topk, d->routed_scale,
+                         lout, topk_ids, topk_w, s),
+         "topk");
+  fs::prof_end(FS_K_TOPK, s);
+  return FS_OK;
+}
+
+fs_status fs_router_topk(const fs_moe_desc* desc, const void* x, const void* w_router,
+                         const float* sel_bias, const float* logits_in, float* logits_out,
+                         int32_t* topk_ids, float* topk_w, void* ws, size_t ws_bytes,
+                         fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  if (!logits_in) {
+    NEED(x, "x");
+    NEED(w_router, "w_router");
+    if (ws_bytes < router_bytes(desc))
+      return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_ROUTER_TOPK)");
+    NEED(ws, "ws");
+  } else {
+    OPT(logits_in, "logits_in");
+  }
+  if (sel_bias && desc->score == FS_SOFTMAX)
+    return fail(FS_ERR_UNSUPPORTED, "a selection bias is defined for sigmoid scoring only");
+  OPT(sel_bias, "sel_bias");
+  OPT(logits_out, "logits_out");
+  NEED(topk_ids, "topk_ids");
+  NEED(topk_w, "topk_w");
+  return router_impl(desc, x, w_router, sel_bias, logits_in, logits_out, topk_ids, topk_w, ws,
+                     S(stream));
+}
+
+// ---- dispatch plan + pack
+static fs_status plan_pack_impl(const fs_moe_desc* d, const int32_t* ids, const void* x,
+                                int32_t* counts, int32_t* offsets, int32_t* rank_offsets,
+                                int32_t* s2r, int32_t* r2s, void* send, void* ws, hipStream_t s) {
+  const int N = d->n_tokens;
+  if (N == 0) return FS_OK;
+  fs::prof_begin(FS_K_PLAN, s);
+  FS_HIP(fs::launch_plan(ids, N, d->top_k, d->n_experts, d->ep_size, counts, offsets,
+                         rank_offsets, s2r, r2s, ws, s),
+         "plan");
+  fs::prof_end(FS_K_PLAN, s);
+  if (send) {
+    fs::prof_begin(FS_K_PACK, s);
+    FS_HIP(fs::launch_pack(d->dtype, x, s2r, N, d->top_k, d->hidden, send, s), "pack");
+    fs::prof_end(FS_K_PACK, s);
+  }
+  return FS_OK;
+}
+
+fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
+                           int32_t* expert_counts, int32_t* expert_offsets,
+                           int32_t* rank_offsets, int32_t* slot_to_row, int32_t* row_to_slot,
+                           void* send, void* ws, size_t ws_bytes, fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED(topk_ids, "topk_ids");
+  NEED(x, "x");
+  NEED(expert_counts, "expert_counts");
+  NEED(expert_offsets, "expert_offsets");
+  NEED(rank_offsets, "rank_offsets");
+  NEED(slot_to_row, "slot_to_row");
+  NEED(row_to_slot, "row_to_slot");
+  NEED(send, "send");
+  if (ws_bytes < plan_bytes(desc))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_DISPATCH_PACK)");
+  NEED(ws, "ws");
+  return plan_pack_impl(desc, topk_ids, x, expert_counts, expert_offsets, rank_offsets,
+                        slot_to_row, row_to_slot, send, ws, S(stream));
+}
+
+fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
+                          const int32_t* src_offsets, int32_t* group_rows, int32_t* group_offsets,
+                          fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  NEED(src_counts, "src_counts");
+  NEED(src_offsets, "src_offsets");
+  NEED(group_rows, "group_rows");
+  NEED(group_offsets, "group_offsets");
+  FS_HIP(fs::launch_receive_rows(src_counts, src_offsets, desc->ep_size, desc->n_experts,
+                                 desc->ep_rank, (int64_t)desc->n_tokens * desc->top_k,
+                                 group_rows, group_offsets, S(stream)),
+         "receive_rows");
+  return FS_OK;
+}
+
+// ---- grouped FFN
+fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                const void* in_rows, const int32_t* group_rows,
+                                const int32_t* group_offsets, int64_t max_rows,
+                                const void* w_gate_up, const void* w_down, void* out_rows,
+                                void* ws, size_t ws_bytes, fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (n_groups < 1) return fail(FS_ERR_INVALID, "n_groups must be >= 1");
+  if (n_groups > 512) return fail(FS_ERR_UNSUPPORTED, "n_groups must be <= 512");
+  if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
+  if (ffn % 64 != 0) return fail(FS_ERR_UNSUPPORTED, "ffn must be a multiple of 64");
+  if (max_rows < 0) return fail(FS_ERR_INVALID, "max_rows must be >= 0");
+  if (max_rows >= ((int64_t)1 << 31)) return fail(FS_ERR_UNSUPPORTED, "max_rows must be < 2^31");
+  if (!group_offsets && n_groups != 1)
+    return fail(FS_ERR_INVALID, "group_offsets may be NULL only with n_groups == 1");
+  if (max_rows == 0) return FS_OK;
+  NEED(in_rows, "in_rows");
+  OPT(group_rows, "group_rows");
+  OPT(group_offsets, "group_offsets");
+  NEED(w_gate_up, "w_gate_up");
+  NEED(w_down, "w_down");
+  NEED(out_rows, "out_rows");
+  if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
+  NEED(ws, "ws");
+  FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, in_rows, group_rows,
+                                group_offsets, max_rows, w_gate_up, w_down, out_rows, ws,
+                                S(stream), true),
+         "grouped_ffn");
+  return FS_OK;
+}
+
+// ---- combine + residual
+fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
+                            const int32_t* slot_to_row, const float* topk_w,
+                            const void* shared_out, void* routed_out, void* residual,
+                            fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED(y_ret, "y_ret");
+  NEED(slot_to_row, "slot_to_row");
+  NEED(topk_w, "topk_w");
+  OPT(shared_out, "shared_out");
+  OPT(routed_out, "routed_out");
+  OPT(residual, "residual");
+  if (!routed_out && !residual) return fail(FS_ERR_INVALID, "routed_out and residual are both NULL");
+  hipStream_t s = S(stream);
+  fs::prof_begin(FS_K_COMBINE, s);
+  FS_HIP(fs::launch_combine(desc->dtype, y_ret, slot_to_row, topk_w, shared_out, routed_out,
+                            residual, desc->n_tokens, desc->top_k, desc->hidden, s),
+         "combine");
+  fs::prof_end(FS_K_COMBINE, s);
+  return FS_OK;
+}
+
+fs_status fs_farskip_residual(const fs_moe_desc* desc, void* out, const void* residual,
+                              const void* deferred, const void* extra, fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED(out, "out");
+  NEED(residual, "residual");
+  NEED(deferred, "deferred");
+  OPT(extra, "extra");
+  FS_HIP(fs::launch_residual(desc->dtype, out, residual, deferred, extra,
+                             (int64_t)desc->n_tokens * desc->hidden, S(stream)),
+         "residual");
+  return FS_OK;
+}
+
+// ---- dense linear
+fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, const void* a,
+                          const void* w, void* out, fs_stream stream) {
+  if (dtype != FS_F32 && dtype != FS_BF16) return fail(FS_ERR_INVALID, "dtype must be FS_F32 or FS_BF16");
+  if (m < 0 || n <= 0 || kdim <= 0) return fail(FS_ERR_INVALID, "m >= 0, n > 0, kdim > 0 required");
+  if (kdim % 64 != 0) return fail(FS_ERR_UNSUPPORTED, "kdim must be a multiple of 64");
+  if (n % (dtype == FS_BF16 ? 128 : 64) != 0)
+    return fail(FS_ERR_UNSUPPORTED, "n must be a multiple of 128 (bf16) or 64 (fp32)");
+  if (m == 0) return FS_OK;
+  NEED(a, "a");
+  NEED(w, "w");
+  NEED(out, "out");
+  FS_HIP(fs::launch_dense_linear(dtype, m, n, kdim, a, w, out, S(stream)), "dense_linear");
+  return FS_OK;
+}
+
+// ---- block sync
+struct fs_block_sync {
+  hipEvent_t packed = nullptr;
+  hipEvent_t dispatched = nullptr;
+  bool have_dispatch = false;
+};
+
+fs_status fs_block_sync_create(fs_block_sync** out) {
+  if (!out) return fail(FS_ERR_INVALID, "out must not be NULL");
+  fs_block_sync* s = new (std::nothrow) fs_block_sync();
+  if (!s) return fail(FS_ERR_INVALID, "out of host memory");
+  hipError_t e = hipEventCreateWithFlags(&s->packed, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->dispatched, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    if (s->packed) (void)hipEventDestroy(s->packed);
+    delete s;
+    return hip_fail(e, "hipEventCreate");
+  }
+  *out = s;
+  return FS_OK;
+}
+
+fs_status fs_block_sync_destroy(fs_block_sync* s) {
+  if (!s) return FS_OK;
+  if (s->packed) (void)hipEventDestroy(s->packed);
+  if (s->dispatched) (void)hipEventDestroy(s->dispatched);
+  delete s;
+  return FS_OK;
+}
+
+// ---- the block
+fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
+                               const fs_moe_weights* wt, const void* residual_in,
+                               void* partial_out, void* residual_io, fs_block_buffers* b,
+                               int64_t max_recv_rows, void* ws, size_t ws_bytes,
+                               fs_block_sync* sync, fs_stream compute, fs_stream comm) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (phase != FS_PHASE_ALL && phase != FS_PHASE_BEGIN && phase != FS_PHASE_FINISH)
+    return fail(FS_ERR_INVALID, "phase must be FS_PHASE_ALL, BEGIN or FINISH");
+  if (!wt) return fail(FS_ERR_INVALID, "weights must not be NULL");
+  if (!b) return fail(FS_ERR_INVALID, "buffers must not be NULL");
+  if (comm && !sync) return fail(FS_ERR_INVALID, "a comm stream needs a sync object");
+  const int N = desc->n_tokens, D = desc->hidden, K = desc->top_k, E = desc->n_experts;
+  const int R = desc->ep_size, r = desc->ep_rank, E_loc = E / R;
+  const int64_t cap = (int64_t)N * K;
+  if (max_recv_rows < 0) return fail(FS_ERR_INVALID, "max_recv_rows must be >= 0");
+  if (R == 1 && max_recv_rows < cap)
+    return fail(FS_ERR_INVALID, "max_recv_rows must be >= n_tokens * top_k when ep_size == 1");
+  if (max_recv_rows > (int64_t)R * cap)
+    return fail(FS_ERR_INVALID, "max_recv_rows must be <= ep_size * n_tokens * top_k");
+  const bool begin = phase != FS_PHASE_FINISH, finish = phase != FS_PHASE_BEGIN;
+  size_t need = 0;
+  st = fs_workspace_size(desc, FS_OP_BLOCK, max_recv_rows, 0, &need);
+  if (st != FS_OK) return st;
+  if (ws_bytes < need) return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_BLOCK)");
+  if (N == 0) return FS_OK;
+  NEED(ws, "ws");
+  NEED(residual_in, "residual_in");
+  if (begin) {
+    NEED(wt->w_router, "weights->w_router");
+    OPT(wt->sel_bias, "weights->sel_bias");
+    if (wt->sel_bias && desc->score == FS_SOFTMAX)
+      return fail(FS_ERR_UNSUPPORTED, "a selection bias is defined for sigmoid scoring only");
+    NEED(partial_out, "partial_out");
+    NEED(b->send, "buffers->send");
+    NEED(b->row_to_slot, "buffers->row_to_slot");
+    if (desc->n_shared > 0) {
+      NEED(wt->ws_gate_up, "weights->ws_gate_up");
+      NEED(wt->ws_down, "weights->ws_down");
+      NEED(b->shared_out, "buffers->shared_out");
+    }
+    OPT(b->logits, "buffers->logits");
+  }
+  if (finish) {
+    NEED(wt->w_gate_up, "weights->w_gate_up");
+    NEED(wt->w_down, "weights->w_down");
+    NEED(residual_io, "residual_io");
+    NEED(b->y, "buffers->y");
+    if (R > 1) {
+      NEED(b->group_rows, "buffers->group_rows");
+      NEED(b->group_offsets, "buffers->group_offsets");
+    }
+  }
+  NEED(b->topk_ids, "buffers->topk_ids");
+  NEED(b->topk_w, "buffers->topk_w");
+  NEED(b->src_counts, "buffers->src_counts");
+  NEED(b->src_offsets, "buffers->src_offsets");
+  NEED(b->rank_offsets, "buffers->rank_offsets");
+  NEED(b->slot_to_row, "buffers->slot_to_row");
+  if (R > 1 || comm) NEED(b->recv, "buffers->recv");
+
+  hipStream_t sc = S(compute), sm = S(comm);
+  const size_t es = elem(desc->dtype);
+  Carve c{reinterpret_cast<char*>(ws)};
+  void* ws_router = c.take(router_bytes(desc));
+  void* ws_plan = c.take(plan_bytes(desc));
+  void* ws_ffn = c.take(fs::ffn_ws_bytes(desc->dtype, max_recv_rows, desc->ffn));
+  void* ws_shared = desc->n_shared > 0
+                        ? c.take(fs::ffn_ws_bytes(desc->dtype, N, desc->n_shared * desc->ffn_shared))
+                        : nullptr;
+  int32_t* my_counts = b->src_counts + (size_t)r * E;
+  int32_t* my_offsets = b->src_offsets + (size_t)r * (E + 1);
+  char* recv_slot = b->recv ? reinterpret_cast<char*>(b->recv) + (size_t)r * cap * D * es : nullptr;
+
+  if (begin) {
+    // gate: router + top-k (not overlappable, Eq. 9), then plan + pack
+    st = router_impl(desc, residual_in, wt->w_router, wt->sel_bias, nullptr, b->logits,
+                     b->topk_ids, b->topk_w, ws_router, sc);
+    if (st != FS_OK) return st;
+    st = plan_pack_impl(desc, b->topk_ids, residual_in, my_counts, my_offsets, b->rank_offsets,
+                        b->slot_to_row, b->row_to_slot, b->send, ws_plan, sc);
+    if (st != FS_OK) return st;
+    // Dispatch stand-in: the whole send buffer leaves on the comm stream.
+    if (sm) {
+      FS_HIP(hipEventRecord(sync->packed, sc), "hipEventRecord");
+      FS_HIP(hipStreamWaitEvent(sm, sync->packed, 0), "hipStreamWaitEvent");
+      FS_HIP(hipMemcpyAsync(recv_slot, b->send, (size_t)cap * D * es, hipMemcpyDeviceToDevice, sm),
+             "hipMemcpyAsync");
+      FS_HIP(hipEventRecord(sync->dispatched, sm), "hipEventRecord");
+      sync->have_dispatch = true;
+    } else if (R > 1) {
+      FS_HIP(hipMemcpyAsync(recv_slot, b->send, (size_t)cap * D * es, hipMemcpyDeviceToDevice, sc),
+             "hipMemcpyAsync");
+    }
+    // shared experts on o_{k-1}, then the next layer's partial input
+    if (desc->n_shared > 0) {
+      FS_HIP(fs::launch_grouped_ffn(desc->dtype, 1, desc->n_shared * desc->ffn_shared, D,
+                                    residual_in, nullptr, nullptr, N, wt->ws_gate_up, wt->ws_down,
+                                    b->shared_out, ws_shared, sc, false),
+             "shared_ffn");
+    }
+    FS_HIP(fs::launch_residual(desc->dtype, partial_out, residual_in,
+                               desc->n_shared > 0 ? b->shared_out : nullptr, nullptr,
+                               (int64_t)N * D, sc),
+           "partial");
+  }
+  if (finish) {
+    if (sm && sync && sync->have_dispatch) {
+      FS_HIP(hipStreamWaitEvent(sc, sync->dispatched, 0), "hipStreamWaitEvent");
+      sync->have_dispatch = false;
+    }
+    const void* in_rows;
+    const int32_t* rows;
+    const int32_t* goff;
+    if (R > 1) {
+      FS_HIP(fs::launch_receive_rows(b->src_counts, b->src_offsets, R, E, r, cap, b->group_rows,
+                                     b->group_offsets, sc),
+             "receive_rows");
+      in_rows = b->recv;
+      rows = b->group_rows;
+      goff = b->group_offsets;
+    } else {
+      in_rows = sm ? b->recv : b->send;
+      rows = nullptr;
+      goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
+    }
+    FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, goff,
+                                  max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc, true),
+           "grouped_ffn");
+    const char* y_ret = reinterpret_cast<const char*>(b->y) + (size_t)r * cap * D * es;
+    fs::prof_begin(FS_K_COMBINE, sc);
+    FS_HIP(fs::launch_combine(desc->dtype, y_ret, b->slot_to_row, b->topk_w, nullptr, nullptr,
+                              residual_io, N, K, D, sc),
+           "combine");
+    fs::prof_end(FS_K_COMBINE, sc);
+  }
+  return FS_OK;
+}
+
+// ---- profiling
+fs_status fs_profile_enable(int32_t on) {
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.on = on != 0;
+  return FS_OK;
+}
+
+fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches) {
+  if (kernel < 0 || kernel >= FS_K_COUNT) return fail(FS_ERR_INVALID, "kernel id out of range");
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  for (auto& rec : p.open) {
+    hipError_t e = hipEventSynchronize(rec.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, rec.a, rec.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    p.total_ms[rec.kernel] += ms;
+    p.count[rec.kernel] += 1;
+    p.pool.push_back(rec.a);
+    p.pool.push_back(rec.b);
+  }
+  p.open.clear();
+  if (total_ms) *total_ms = p.total_ms[kernel];
+  if (launches) *launches = p.count[kernel];
+  return FS_OK;
+}
+
+fs_status fs_profile_reset(void) {
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  for (auto& rec : p.open) {
+    (void)hipEventSynchronize(rec.b);
+    p.pool.push_back(rec.a);
+    p.pool.push_back(rec.b);
+  }
+  p.open.clear();
+  for (int k = 0; k < FS_K_COUNT; ++k) {
+    p.total_ms[k] = 0;
+    p.count[k] = 0;
+  }
+  return FS_OK;
+}
+
+}  // extern "C"

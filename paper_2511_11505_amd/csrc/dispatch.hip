@@ -1,0 +1,213 @@
+// Dispatch plan, pack and receive rows (Section 2.1, Dispatch).
+//
+// The plan is a stable counting sort of the N*k (token, expert) slots by
+// expert, with no global atomics, so it is deterministic:
+//   1. per 64-token tile, a bit mask per expert of the tile's tokens that
+//      chose it (LDS OR, order-independent) and its population count;
+//   2. one workgroup scans the per-tile counts into per-tile bases and the
+//      expert offsets;
+//   3. each slot's row = its tile's base for the expert + the number of
+//      earlier tokens of the tile with the same expert (popcount of the mask
+//      below the token's lane).
+// Pack copies each token row once from HBM and writes it to its k rows with
+// 16-byte vector accesses.
+
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace fs {
+namespace {
+
+constexpr int kTile = 64;  // tokens per plan tile (one wavefront)
+
+__global__ __launch_bounds__(64) void plan_hist_kernel(const int32_t* __restrict__ ids, int N,
+                                                       int k, int E, uint64_t* __restrict__ bits,
+                                                       int32_t* __restrict__ hist) {
+  extern __shared__ uint64_t sb[];
+  const int tile = blockIdx.x, lane = threadIdx.x;
+  for (int e = lane; e < E; e += 64) sb[e] = 0;
+  __syncthreads();
+  const int t = tile * kTile + lane;
+  if (t < N) {
+    for (int j = 0; j < k; ++j) {
+      const int e = ids[(size_t)t * k + j];
+      if ((unsigned)e < (unsigned)E) atomicOr((unsigned long long*)&sb[e], 1ull << lane);
+    }
+  }
+  __syncthreads();
+  for (int e = lane; e < E; e += 64) {
+    const uint64_t b = sb[e];
+    bits[(size_t)tile * E + e] = b;
+    hist[(size_t)tile * E + e] = __popcll(b);
+  }
+}
+
+// One workgroup of 512 threads; thread e owns expert e (E <= 512).
+__global__ __launch_bounds__(512) void plan_scan_kernel(const int32_t* __restrict__ hist,
+                                                        int n_tiles, int E, int R,
+                                                        int32_t* __restrict__ tile_base,
+                                                        int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ offsets,
+                                                        int32_t* __restrict__ rank_offsets) {
+  __shared__ int32_t sc[512];
+  const int e = threadIdx.x;
+  int run = 0;
+  if (e < E) {
+    for (int tl = 0; tl < n_tiles; ++tl) {
+      tile_base[(size_t)tl * E + e] = run;
+      run += hist[(size_t)tl * E + e];
+    }
+  }
+  sc[e] = (e < E) ? run : 0;
+  __syncthreads();
+  for (int o = 1; o < 512; o <<= 1) {
+    const int v = (e >= o) ? sc[e - o] : 0;
+    __syncthreads();
+    sc[e] += v;
+    __syncthreads();
+  }
+  const int incl = sc[e];
+  const int excl = incl - ((e < E) ? run : 0);
+  if (e < E) {
+    counts[e] = run;
+    offsets[e] = excl;
+    for (int tl = 0; tl < n_tiles; ++tl) tile_base[(size_t)tl * E + e] += excl;
+  }
+  if (e == E - 1) offsets[E] = incl;
+  // rank_offsets[r] = offsets[r * E / R]
+  __syncthreads();
+  if (e <= R) {
+    const int ge = e * (E / R);
+    rank_offsets[e] = (ge == 0) ? 0 : sc[ge - 1];
+  }
+}
+
+__global__ __launch_bounds__(64) void plan_rank_kernel(const int32_t* __restrict__ ids, int N,
+                                                       int k, int E,
+                                                       const uint64_t* __restrict__ bits,
+                                                       const int32_t* __restrict__ tile_base,
+                                                       int32_t* __restrict__ slot_to_row,
+                                                       int32_t* __restrict__ row_to_slot) {
+  const int tile = blockIdx.x, lane = threadIdx.x;
+  const int t = tile * kTile + lane;
+  if (t >= N) return;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int j = 0; j < k; ++j) {
+    const int slot = t * k + j;
+    const int e = ids[slot];
+    int row = -1;
+    if ((unsigned)e < (unsigned)E) {
+      const size_t te = (size_t)tile * E + e;
+      row = tile_base[te] + __popcll(bits[te] & below);
+      row_to_slot[row] = slot;
+    }
+    slot_to_row[slot] = row;
+  }
+}
+
+// One wavefront per token; each lane moves 16-byte chunks, four at a time.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ x,
+                                                   const int32_t* __restrict__ slot_to_row, int N,
+                                                   int k, int d, T* __restrict__ send) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= N) return;
+  const int nch = d * (int)sizeof(T) / 16;
+  const uint4* src = reinterpret_cast<const uint4*>(x + (size_t)t * d);
+  for (int cb = 0; cb < nch; cb += 4 * 64) {
+    uint4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = cb + i * 64 + lane;
+      if (c < nch) v[i] = src[c];
+    }
+    for (int j = 0; j < k; ++j) {
+      const int row = slot_to_row[(size_t)t * k + j];
+      if (row < 0) continue;
+      uint4* dst = reinterpret_cast<uint4*>(send + (size_t)row * d);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = cb + i * 64 + lane;
+        if (c < nch) dst[c] = v[i];
+      }
+    }
+  }
+}
+
+// One workgroup per local expert e.  Its rows start after all rows of the
+// local experts before it; within e, source 0's rows come first.
+__global__ __launch_bounds__(256) void receive_rows_kernel(const int32_t* __restrict__ counts,
+                                                           const int32_t* __restrict__ offsets,
+                                                           int R, int E, int r, int64_t cap,
+                                                           int32_t* __restrict__ group_rows,
+                                                           int32_t* __restrict__ goff) {
+  __shared__ int red[256];
+  const int E_loc = E / R;
+  const int e = blockIdx.x;
+  const int ge = r * E_loc + e;
+  const int tid = threadIdx.x;
+  int part = 0;
+  for (int i = tid; i < e * R; i += 256) {
+    const int ep = i / R, s = i % R;
+    part += counts[(size_t)s * E + r * E_loc + ep];
+  }
+  red[tid] = part;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) red[tid] += red[tid + o];
+    __syncthreads();
+  }
+  int base = red[0];
+  if (tid == 0) goff[e] = base;
+  for (int s = 0; s < R; ++s) {
+    const int c = counts[(size_t)s * E + ge];
+    const int64_t start = (int64_t)s * cap + offsets[(size_t)s * (E + 1) + ge];
+    for (int j = tid; j < c; j += 256) group_rows[base + j] = (int32_t)(start + j);
+    base += c;
+  }
+  if (e == E_loc - 1 && tid == 0) goff[E_loc] = base;
+}
+
+}  // namespace
+
+size_t plan_ws_bytes(int N, int E) {
+  const size_t n_tiles = (size_t)(N + kTile - 1) / kTile;
+  return n_tiles * E * (sizeof(uint64_t) + 2 * sizeof(int32_t));
+}
+
+hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* counts,
+                       int32_t* offsets, int32_t* rank_offsets, int32_t* slot_to_row,
+                       int32_t* row_to_slot, void* ws, hipStream_t s) {
+  const int n_tiles = (N + kTile - 1) / kTile;
+  uint64_t* bits = reinterpret_cast<uint64_t*>(ws);
+  int32_t* hist = reinterpret_cast<int32_t*>(bits + (size_t)n_tiles * E);
+  int32_t* tile_base = hist + (size_t)n_tiles * E;
+  plan_hist_kernel<<<n_tiles, 64, E * sizeof(uint64_t), s>>>(ids, N, k, E, bits, hist);
+  plan_scan_kernel<<<1, 512, 0, s>>>(hist, n_tiles, E, R, tile_base, counts, offsets,
+                                     rank_offsets);
+  plan_rank_kernel<<<n_tiles, 64, 0, s>>>(ids, N, k, E, bits, tile_base, slot_to_row,
+                                          row_to_slot);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int N, int k, int d,
+                       void* send, hipStream_t s) {
+  dim3 grid((N + 3) / 4);
+  if (dtype == 0)
+    pack_kernel<float><<<grid, 256, 0, s>>>((const float*)x, slot_to_row, N, k, d, (float*)send);
+  else
+    pack_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)x, slot_to_row, N, k, d,
+                                             (bf16_t*)send);
+  return hipGetLastError();
+}
+
+hipError_t launch_receive_rows(const int32_t* src_counts, const int32_t* src_offsets, int R,
+                               int E, int r, int64_t cap, int32_t* group_rows,
+                               int32_t* group_offsets, hipStream_t s) {
+  receive_rows_kernel<<<E / R, 256, 0, s>>>(src_counts, src_offsets, R, E, r, cap, group_rows,
+                                            group_offsets);
+  return hipGetLastError();
+}
+
+}  // namespace fs

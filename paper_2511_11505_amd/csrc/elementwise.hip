@@ -1,0 +1,119 @@
+// Combine + unpack with the deferred FarSkip residual add, and the plain
+// residual add (Section 2.1 Combine; Section 3, Eq. 7).
+//
+// Combine is a gather: token t reads its k expert-output rows through
+// slot_to_row, so no atomics are needed and the fp32 sum runs in slot order
+// j = 0..k-1.  All adds run in fp32 and round once at the store.
+
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace fs {
+namespace {
+
+// One wavefront per token; each lane handles 16-byte chunks of the row.
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
+                                                      const int32_t* __restrict__ slot_to_row,
+                                                      const float* __restrict__ topk_w,
+                                                      const T* __restrict__ shared_out,
+                                                      T* __restrict__ routed_out,
+                                                      T* __restrict__ residual, int N, int k,
+                                                      int d) {
+  constexpr int V = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= N) return;
+  const int nch = d / V;
+  const size_t rowoff = (size_t)t * d;
+  for (int c = lane; c < nch; c += 64) {
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      const int row = slot_to_row[(size_t)t * k + j];
+      if (row < 0) continue;
+      const float wj = topk_w[(size_t)t * k + j];
+      Vec16<T> v;
+      v.raw = ld16(y + (size_t)row * d + (size_t)c * V);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = fmaf(wj, v.get(i), acc[i]);
+    }
+    if (shared_out) {
+      Vec16<T> v;
+      v.raw = ld16(shared_out + rowoff + (size_t)c * V);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += v.get(i);
+    }
+    if (routed_out) {
+      Vec16<T> o;
+#pragma unroll
+      for (int i = 0; i < V; ++i) o.set(i, acc[i]);
+      st16(routed_out + rowoff + (size_t)c * V, o.raw);
+    }
+    if (residual) {
+      Vec16<T> rv, o;
+      rv.raw = ld16(residual + rowoff + (size_t)c * V);
+#pragma unroll
+      for (int i = 0; i < V; ++i) o.set(i, rv.get(i) + acc[i]);
+      st16(residual + rowoff + (size_t)c * V, o.raw);
+    }
+  }
+}
+
+// out = a + b (+ c), elementwise in fp32, 16-byte vectors, grid-stride.
+template <typename T>
+__global__ __launch_bounds__(256) void residual_kernel(T* out, const T* a, const T* b,
+                                                       const T* c, int64_t n_vec) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_vec;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    Vec16<T> va, vb, vc, o;
+    va.raw = ld16(a + i * Vec16<T>::N);
+    if (b) vb.raw = ld16(b + i * Vec16<T>::N);
+    if (c) vc.raw = ld16(c + i * Vec16<T>::N);
+#pragma unroll
+    for (int v = 0; v < Vec16<T>::N; ++v) {
+      float s = va.get(v);
+      if (b) s += vb.get(v);
+      if (c) s += vc.get(v);
+      o.set(v, s);
+    }
+    st16(out + i * Vec16<T>::N, o.raw);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_row,
+                          const float* topk_w, const void* shared_out, void* routed_out,
+                          void* residual, int N, int k, int d, hipStream_t s) {
+  dim3 grid((N + 3) / 4);
+  if (dtype == 0)
+    combine_kernel<float><<<grid, 256, 0, s>>>((const float*)y_ret, slot_to_row, topk_w,
+                                               (const float*)shared_out, (float*)routed_out,
+                                               (float*)residual, N, k, d);
+  else
+    combine_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)y_ret, slot_to_row, topk_w,
+                                                (const bf16_t*)shared_out, (bf16_t*)routed_out,
+                                                (bf16_t*)residual, N, k, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_residual(int dtype, void* out, const void* a, const void* b, const void* c,
+                           int64_t n_elems, hipStream_t s) {
+  const int V = dtype == 0 ? 4 : 8;
+  const int64_t n_vec = n_elems / V;
+  int64_t blocks = (n_vec + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  if (dtype == 0)
+    residual_kernel<float><<<(int)blocks, 256, 0, s>>>((float*)out, (const float*)a,
+                                                       (const float*)b, (const float*)c, n_vec);
+  else
+    residual_kernel<bf16_t><<<(int)blocks, 256, 0, s>>>((bf16_t*)out, (const bf16_t*)a,
+                                                        (const bf16_t*)b, (const bf16_t*)c,
+                                                        n_vec);
+  return hipGetLastError();
+}
+
+}  // namespace fs

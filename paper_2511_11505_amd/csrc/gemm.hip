@@ -1,0 +1,436 @@
+// Grouped SwiGLU expert FFN (Section 2.1: MLP^j read as SwiGLU) on gfx950.
+//
+// Two passes per call:
+//   gate/up:  H[i, n] = SiLU(X_i . Wg[n]) * (X_i . Wu[n])   (rows gathered
+//             through group_rows; a tile owns matching gate and up columns so
+//             the SwiGLU runs in the epilogue; H is stored in the element type)
+//   down:     Y[row_i] = H[i] . Wd^T                        (rows scattered
+//             through group_rows)
+// bf16 runs on MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) with both
+// operand tiles staged through LDS, double-buffered, with the next K block
+// prefetched into registers.  fp32 runs on the vector ALUs.
+//
+// Groups have ragged row counts known only on the device.  Every workgroup
+// rebuilds the per-group m-tile prefix from group_offsets in LDS, then walks
+// the tile space (group, n-tile, m-tile; m fastest) in a persistent loop.
+// The tile space is cut into eight contiguous ranges, one per XCD
+// (workgroups are dispatched round-robin over the XCDs), so tiles sharing a
+// weight panel or a row panel run under one L2.
+
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace fs {
+namespace {
+
+constexpr int kMaxGroups = 512;
+constexpr int kXcd = 8;
+enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
+
+// Group offsets and the exclusive prefix of m-tiles per group, in LDS.
+template <int NT, int BM>
+__device__ void sched_setup(const int32_t* __restrict__ goff, int G, int64_t m_total,
+                            int* s_goff, int* s_tpre, int* s_wtot) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Offsets are clamped to [0, m_total]: rows past the host bound are never
+  // read or written, so a short bound cannot overrun the H workspace.
+  for (int g = tid; g <= G; g += NT) {
+    int v = goff ? goff[g] : (g == 0 ? 0 : (int)m_total);
+    s_goff[g] = v < 0 ? 0 : (v > (int)m_total ? (int)m_total : v);
+  }
+  __syncthreads();
+  constexpr int IPT = (kMaxGroups + 1 + NT - 1) / NT;
+  int cnt[IPT];
+  int local = 0;
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int g = tid * IPT + i;
+    const int c = (g < G && s_goff[g + 1] > s_goff[g]) ? (s_goff[g + 1] - s_goff[g] + BM - 1) / BM : 0;
+    cnt[i] = c;
+    local += c;
+  }
+  int incl = local;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, FS_WAVE);
+    if (lane >= o) incl += v;
+  }
+  if (lane == 63) s_wtot[wave] = incl;
+  __syncthreads();
+  int pre = 0;
+  for (int w = 0; w < wave; ++w) pre += s_wtot[w];
+  int run = pre + incl - local;
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int g = tid * IPT + i;
+    if (g <= G) s_tpre[g] = run;
+    run += cnt[i];
+  }
+  __syncthreads();
+}
+
+// Largest g in [0, G) with nn * tpre[g] <= L.
+__device__ __forceinline__ int find_group(const int* s_tpre, int G, int nn, int64_t L) {
+  int lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int64_t)nn * s_tpre[mid] <= L)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  return lo;
+}
+
+// ---------------------------------------------------------------- bf16 MFMA
+template <int MODE, int BM, int BN, int BK, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
+    int NOUT, bf16_t* __restrict__ C, int ldc) {
+  constexpr int NT = 64 * WAVES_M * WAVES_N;
+  constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int LDK = BK + 8;  // LDS row stride in bf16: 16-byte skew per row
+  constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
+  constexpr int ACH = BM * CPR / NT, BCH = BN * CPR / NT;
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
+  constexpr int STAGE = (BM + BN) * LDK;
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile loads must divide evenly");
+  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
+
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(16) bf16_t lds[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const int KT = K / BK;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group(s_tpre, G, nn, L);
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const int m0 = mt * BM, n0 = nt * NCOL;
+    const bf16_t* Bg = B + (size_t)g * bstride;
+
+    const bf16_t* pa[ACH];
+    bool va[ACH];
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      const int c = tid + i * NT;
+      const int r = c / CPR, kc = (c % CPR) * 8;
+      const int m = m0 + r;
+      va[i] = m < rows_g;
+      const int grow = row_base + (va[i] ? m : 0);
+      const int64_t src = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      pa[i] = A + src * K + kc;
+    }
+    const bf16_t* pb[BCH];
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int c = tid + i * NT;
+      const int r = c / CPR, kc = (c % CPR) * 8;
+      int wrow;
+      if (MODE == MODE_GATEUP)
+        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
+      else
+        wrow = n0 + r;
+      pb[i] = Bg + (size_t)wrow * K + kc;
+    }
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
+
+    uint4 ra[ACH], rb[BCH];
+    auto gload = [&](int k0) {
+#pragma unroll
+      for (int i = 0; i < ACH; ++i) ra[i] = va[i] ? ld16(pa[i] + k0) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) rb[i] = ld16(pb[i] + k0);
+    };
+    auto lstore = [&](int buf) {
+      bf16_t* As = lds + buf * STAGE;
+      bf16_t* Bs = As + BM * LDK;
+#pragma unroll
+      for (int i = 0; i < ACH; ++i) {
+        const int c = tid + i * NT;
+        st16(As + (c / CPR) * LDK + (c % CPR) * 8, ra[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) {
+        const int c = tid + i * NT;
+        st16(Bs + (c / CPR) * LDK + (c % CPR) * 8, rb[i]);
+      }
+    };
+
+    gload(0);
+    for (int kt = 0; kt < KT; ++kt) {
+      lstore(kt & 1);
+      __syncthreads();
+      if (kt + 1 < KT) gload((kt + 1) * BK);
+      const bf16_t* As = lds + (kt & 1) * STAGE;
+      const bf16_t* Bs = As + BM * LDK;
+#pragma unroll
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int kofs = ks * 16 + (lane >> 5) * 8;
+        bf16x8 af[TM], bfr[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = wm * WTM + i * 32 + (lane & 31);
+          af[i] = *reinterpret_cast<const bf16x8*>(As + r * LDK + kofs);
+        }
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) {
+          int br;
+          if (MODE == MODE_GATEUP)
+            br = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32
+                               : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+          else
+            br = wn * WTN + jn * 32;
+          bfr[jn] = *reinterpret_cast<const bf16x8*>(Bs + (br + (lane & 31)) * LDK + kofs);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn)
+            acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[jn], acc[i][jn], 0,
+                                                                 0, 0);
+      }
+    }
+
+    // Epilogue.  Accumulator element v of lane l holds row
+    // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32x32 tile.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        if (m >= rows_g) continue;
+        const int grow = row_base + m;
+        if (MODE == MODE_GATEUP) {
+#pragma unroll
+          for (int jn = 0; jn < TN / 2; ++jn) {
+            const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+            const float h = gt / (1.0f + __expf(-gt)) * up;
+            const int col = n0 + wn * (WTN / 2) + jn * 32 + (lane & 31);
+            C[(size_t)grow * ldc + col] = f2bf(h);
+          }
+        } else {
+          const int64_t orow = rows ? (int64_t)rows[grow] : (int64_t)grow;
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) {
+            const int col = n0 + wn * WTN + jn * 32 + (lane & 31);
+            C[orow * ldc + col] = f2bf(acc[i][jn][v]);
+          }
+        }
+      }
+    }
+    __syncthreads();  // LDS stages are reused by the next tile
+  }
+}
+
+// ---------------------------------------------------------------- fp32 VALU
+// 64 x 64 tiles, 256 threads, 4 rows x 4 columns per thread.  For gate/up a
+// tile holds 32 gate and the matching 32 up columns; a thread owns 2 H
+// columns (their gate and up values).
+template <int MODE>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A,
+                                                       const int32_t* __restrict__ rows,
+                                                       const int32_t* __restrict__ goff, int G,
+                                                       int64_t m_total,
+                                                       const float* __restrict__ B, int K,
+                                                       int NOUT, float* __restrict__ C,
+                                                       int ldc) {
+  constexpr int BM = 64, BN = 64, BK = 16, NT = 256;
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(16) float As[BK][BM + 4];
+  __shared__ __align__(16) float Bs[BK][BN + 4];
+
+  const int tid = threadIdx.x;
+  const int tm = tid % 16, tn = tid / 16;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group(s_tpre, G, nn, L);
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const int m0 = mt * BM, n0 = nt * NCOL;
+    const float* Bg = B + (size_t)g * bstride;
+
+    // one 16-byte chunk of A and of B per thread per K step
+    const int lr = tid / 4, lk = (tid % 4) * 4;
+    const bool va = m0 + lr < rows_g;
+    const int grow_l = row_base + (va ? m0 + lr : 0);
+    const int64_t src = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow_l] : (int64_t)grow_l;
+    const float* pa = A + src * K + lk;
+    int wrow;
+    if (MODE == MODE_GATEUP)
+      wrow = (lr < BN / 2) ? n0 + lr : NOUT + n0 + (lr - BN / 2);
+    else
+      wrow = n0 + lr;
+    const float* pb = Bg + (size_t)wrow * K + lk;
+
+    float acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[i][c] = 0.f;
+
+    float4 ra = va ? *reinterpret_cast<const float4*>(pa) : make_float4(0, 0, 0, 0);
+    float4 rb = *reinterpret_cast<const float4*>(pb);
+    for (int k0 = 0; k0 < K; k0 += BK) {
+      __syncthreads();
+      As[lk + 0][lr] = ra.x;
+      As[lk + 1][lr] = ra.y;
+      As[lk + 2][lr] = ra.z;
+      As[lk + 3][lr] = ra.w;
+      Bs[lk + 0][lr] = rb.x;
+      Bs[lk + 1][lr] = rb.y;
+      Bs[lk + 2][lr] = rb.z;
+      Bs[lk + 3][lr] = rb.w;
+      __syncthreads();
+      if (k0 + BK < K) {
+        ra = va ? *reinterpret_cast<const float4*>(pa + k0 + BK) : make_float4(0, 0, 0, 0);
+        rb = *reinterpret_cast<const float4*>(pb + k0 + BK);
+      }
+#pragma unroll
+      for (int kk = 0; kk < BK; ++kk) {
+        const float4 av = *reinterpret_cast<const float4*>(&As[kk][tm * 4]);
+        float bv[4];
+        if (MODE == MODE_GATEUP) {
+          bv[0] = Bs[kk][tn * 2];
+          bv[1] = Bs[kk][tn * 2 + 1];
+          bv[2] = Bs[kk][BN / 2 + tn * 2];
+          bv[3] = Bs[kk][BN / 2 + tn * 2 + 1];
+        } else {
+          const float4 b4 = *reinterpret_cast<const float4*>(&Bs[kk][tn * 4]);
+          bv[0] = b4.x;
+          bv[1] = b4.y;
+          bv[2] = b4.z;
+          bv[3] = b4.w;
+        }
+        const float a4[4] = {av.x, av.y, av.z, av.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(a4[i], bv[c], acc[i][c]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + tm * 4 + i;
+      if (m >= rows_g) continue;
+      const int grow = row_base + m;
+      if (MODE == MODE_GATEUP) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const float gt = acc[i][c], up = acc[i][c + 2];
+          C[(size_t)grow * ldc + n0 + tn * 2 + c] = gt / (1.0f + expf(-gt)) * up;
+        }
+      } else {
+        const int64_t orow = rows ? (int64_t)rows[grow] : (int64_t)grow;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) C[orow * ldc + n0 + tn * 4 + c] = acc[i][c];
+      }
+    }
+  }
+}
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+
+int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
+  int64_t upper = (cdiv64(max_rows, BM) + G) * nn;
+  upper = ((upper + kXcd - 1) / kXcd) * kXcd;
+  if (upper < kXcd) upper = kXcd;
+  const int64_t cap = (int64_t)kXcd * 65536;
+  return upper > cap ? cap : upper;
+}
+
+}  // namespace
+
+size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn) {
+  const size_t b = (size_t)max_rows * ffn * (dtype == 0 ? 4 : 2);
+  return (b + 255) / 256 * 256;
+}
+
+hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
+                              const int32_t* rows, const int32_t* goff, int64_t max_rows,
+                              const void* w_gate_up, const void* w_down, void* out, void* ws,
+                              hipStream_t s, bool profile) {
+  if (max_rows <= 0) return hipSuccess;
+  if (dtype == 1) {
+    bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+    const int64_t g1 = grid_for(max_rows, G, kBM, ffn / (kBN / 2));
+    if (profile) prof_begin(4, s);
+    gemm_bf16_kernel<MODE_GATEUP, kBM, kBN, kBK, 2, 2><<<(unsigned)g1, 256, 0, s>>>(
+        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn);
+    if (profile) prof_end(4, s);
+    const int64_t g2 = grid_for(max_rows, G, kBM, d / kBN);
+    if (profile) prof_begin(5, s);
+    gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g2, 256, 0, s>>>(
+        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);
+    if (profile) prof_end(5, s);
+  } else {
+    float* H = reinterpret_cast<float*>(ws);
+    const int64_t g1 = grid_for(max_rows, G, 64, ffn / 32);
+    if (profile) prof_begin(4, s);
+    gemm_f32_kernel<MODE_GATEUP><<<(unsigned)g1, 256, 0, s>>>(
+        (const float*)in, rows, goff, G, max_rows, (const float*)w_gate_up, d, ffn, H, ffn);
+    if (profile) prof_end(4, s);
+    const int64_t g2 = grid_for(max_rows, G, 64, d / 64);
+    if (profile) prof_begin(5, s);
+    gemm_f32_kernel<MODE_DOWN><<<(unsigned)g2, 256, 0, s>>>(
+        H, rows, goff, G, max_rows, (const float*)w_down, ffn, d, (float*)out, d);
+    if (profile) prof_end(5, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
+                               void* out, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  if (dtype == 1) {
+    const int64_t g = grid_for(m, 1, kBM, n / kBN);
+    gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g, 256, 0, s>>>(
+        (const bf16_t*)a, nullptr, nullptr, 1, m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n);
+  } else {
+    const int64_t g = grid_for(m, 1, 64, n / 64);
+    gemm_f32_kernel<MODE_DOWN><<<(unsigned)g, 256, 0, s>>>(
+        (const float*)a, nullptr, nullptr, 1, m, (const float*)w, kdim, n, (float*)out, n);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fs

@@ -1,0 +1,54 @@
+// Launchers behind the C ABI.  Each enqueues kernels on `s` and returns the
+// first HIP error; arguments were validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fs {
+
+constexpr int kRouterSlice = 256;  // router reduction-order slice length
+
+// Per-kernel event timing (implemented in api.cpp).
+void prof_begin(int kernel, hipStream_t s);
+void prof_end(int kernel, hipStream_t s);
+
+// ---- router (router.hip)
+int router_slices(int d);
+bool router_split(int N, int d, int E);
+size_t router_ws_bytes(int N, int d, int E);
+hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, int d, int E,
+                                bool split, float* out, hipStream_t s);
+hipError_t launch_topk(const float* src, int n_partials, int N, int E, const float* bias,
+                       int score, int k, int G, int TG, int norm, float scale,
+                       float* logits_out, int32_t* ids, float* w, hipStream_t s);
+
+// ---- dispatch (dispatch.hip)
+size_t plan_ws_bytes(int N, int E);
+hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* counts,
+                       int32_t* offsets, int32_t* rank_offsets, int32_t* slot_to_row,
+                       int32_t* row_to_slot, void* ws, hipStream_t s);
+hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int N, int k, int d,
+                       void* send, hipStream_t s);
+hipError_t launch_receive_rows(const int32_t* src_counts, const int32_t* src_offsets, int R,
+                               int E, int r, int64_t cap, int32_t* group_rows,
+                               int32_t* group_offsets, hipStream_t s);
+
+// ---- grouped SwiGLU FFN and dense linear (gemm.hip)
+size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn);
+hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const void* in,
+                              const int32_t* rows, const int32_t* goff, int64_t max_rows,
+                              const void* w_gate_up, const void* w_down, void* out, void* ws,
+                              hipStream_t s, bool profile);
+hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
+                               void* out, hipStream_t s);
+
+// ---- combine and residual (elementwise.hip)
+hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_row,
+                          const float* topk_w, const void* shared_out, void* routed_out,
+                          void* residual, int N, int k, int d, hipStream_t s);
+hipError_t launch_residual(int dtype, void* out, const void* a, const void* b, const void* c,
+                           int64_t n_elems, hipStream_t s);
+
+}  // namespace fs

@@ -1,0 +1,244 @@
+"""GPU parity of each step of the hot path against the CPU oracle, through the
+C ABI, at sizes the oracle finishes in seconds that span several tiles and a
+ragged tail.  Integers are compared bit for bit, floats with rel_err against
+the stated tolerance."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_11505_amd import _lib as L
+from tests._util import TOL, f64, rel_err
+from workloads import CONFIGS, make_workload
+from workloads.generate import synthetic_topk_ids
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+DEV = "cuda"
+
+# Small variants of the five workloads: several router slices (one ragged),
+# several GEMM tiles, ragged token counts.
+SMALL = {
+    "tiny": CONFIGS["tiny"],
+    "tiny_ragged": CONFIGS["tiny"].scaled(n_tokens=77, name="tiny_ragged"),
+    "dsv2lite_s": CONFIGS["dsv2lite"].scaled(n_tokens=333, hidden=512, ffn=256, ffn_shared=128,
+                                             name="dsv2lite_s"),
+    "scout_s": CONFIGS["scout"].scaled(n_tokens=517, hidden=640, ffn=384, ffn_shared=384,
+                                       name="scout_s"),
+    "dsv3_prefill_s": CONFIGS["dsv3_prefill"].scaled(n_tokens=150, hidden=512, ffn=256,
+                                                     ffn_shared=256, name="dsv3_prefill_s"),
+    "dsv3_decode_s": CONFIGS["dsv3_decode"].scaled(n_tokens=9, hidden=384, ffn=192, ffn_shared=192,
+                                                   name="dsv3_decode_s"),
+}
+
+
+def ws_for(desc, op, rows=0, ffn=0):
+    return torch.empty((max(L.fs_workspace_size(desc, op, rows, ffn), 256),), dtype=torch.uint8,
+                       device=DEV)
+
+
+def route_gpu(cfg, x, w_router, bias, logits_in=None):
+    desc = L.make_desc(cfg)
+    N, E, k = cfg.n_tokens, cfg.n_experts, cfg.top_k
+    logits = torch.empty((N, E), dtype=torch.float32, device=DEV)
+    ids = torch.empty((N, k), dtype=torch.int32, device=DEV)
+    w = torch.empty((N, k), dtype=torch.float32, device=DEV)
+    L.fs_router_topk(desc, x, w_router, bias, logits_in, logits, ids, w,
+                     ws_for(desc, L.FS_OP_ROUTER_TOPK))
+    torch.cuda.synchronize()
+    return logits, ids, w
+
+
+def check_ids(cfg, ids_gpu, ids_ref, near):
+    """Bit-exact ids except on near-tie tokens, where the selection must still
+    be a valid top-k set (checked by the caller's keys)."""
+    g = ids_gpu.cpu().numpy()
+    assert g.shape == ids_ref.shape
+    far = ~near
+    bad = np.where(np.any(g[far] != ids_ref[far], axis=1))[0]
+    assert bad.size == 0, f"{cfg.name}: {bad.size} non-tie tokens routed differently"
+    for t in np.where(near)[0]:
+        assert len(set(g[t].tolist())) == cfg.top_k
+        assert all(0 <= e < cfg.n_experts for e in g[t])
+    return int(near.sum())
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_router_logits_bitexact_and_topk(name):
+    cfg = SMALL[name]
+    wl = make_workload(cfg, DEV, with_experts=False)
+    for s in range(cfg.ep_size):
+        x = wl.x_all[s]
+        logits, ids, w = route_gpu(cfg, x, wl.w_router, wl.bias)
+        z_ref = oracle.logits_routing_f32(f64(x).astype(np.float32), f64(wl.w_router).astype(np.float32))
+        z_gpu = logits.cpu().numpy()
+        assert np.array_equal(z_gpu, z_ref), (
+            f"{name} src {s}: logits differ bitwise at {np.argwhere(z_gpu != z_ref)[:5].tolist()}")
+        bias = None if wl.bias is None else f64(wl.bias)
+        ids_ref, w_ref, near, _ = oracle.route(z_ref, cfg.score, cfg.top_k, cfg.n_groups,
+                                               cfg.topk_groups, cfg.norm_topk, cfg.routed_scale, bias)
+        check_ids(cfg, ids, ids_ref, near)
+        far = ~near
+        assert rel_err(w.cpu().numpy()[far], w_ref[far]) <= 2e-6
+
+
+@pytest.mark.parametrize("score,G,TG,k,E", [("softmax", 1, 1, 4, 40), ("sigmoid", 4, 2, 3, 96),
+                                            ("sigmoid", 8, 4, 8, 256), ("softmax", 16, 3, 5, 512),
+                                            ("sigmoid", 1, 1, 32, 200)])
+def test_topk_from_given_logits(score, G, TG, k, E):
+    # Quantised logits create exact ties: selection must break them toward
+    # the lower expert (softmax compares the logits themselves).
+    cfg = CONFIGS["tiny"].scaled(n_tokens=301, n_experts=E, top_k=k, score=score, n_groups=G,
+                                 topk_groups=TG, norm_topk=(score == "sigmoid"), routed_scale=1.5)
+    g = torch.Generator(device="cpu").manual_seed(11)
+    z = (torch.randint(-6, 7, (cfg.n_tokens, E), generator=g).float() * 0.25)
+    bias = (torch.rand(E, generator=g) * 0.2 - 0.1) if score == "sigmoid" else None
+    logits_in = z.to(DEV)
+    _, ids, w = route_gpu(cfg, None, None, None if bias is None else bias.to(DEV), logits_in=logits_in)
+    ids_ref, w_ref, near, _ = oracle.route(z.numpy(), score, k, G, TG, cfg.norm_topk, 1.5,
+                                           None if bias is None else bias.numpy().astype(np.float64))
+    n_near = check_ids(cfg, ids, ids_ref, near)
+    if score == "softmax" and G == 1:
+        assert n_near == 0
+    assert rel_err(w.cpu().numpy()[~near], w_ref[~near]) <= 2e-6
+
+
+def plan_gpu(cfg, ids, x):
+    desc = L.make_desc(cfg)
+    N, E, k, R, d = cfg.n_tokens, cfg.n_experts, cfg.top_k, cfg.ep_size, cfg.hidden
+    i32 = torch.int32
+    out = dict(counts=torch.empty(E, dtype=i32, device=DEV),
+               offsets=torch.empty(E + 1, dtype=i32, device=DEV),
+               rank_offsets=torch.empty(R + 1, dtype=i32, device=DEV),
+               slot_to_row=torch.empty(N * k, dtype=i32, device=DEV),
+               row_to_slot=torch.empty(N * k, dtype=i32, device=DEV),
+               send=torch.empty((N * k, d), dtype=x.dtype, device=DEV))
+    L.fs_dispatch_pack(desc, ids, x, out["counts"], out["offsets"], out["rank_offsets"],
+                       out["slot_to_row"], out["row_to_slot"], out["send"],
+                       ws_for(desc, L.FS_OP_DISPATCH_PACK))
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("N,E,k,R,dtype", [(1, 8, 2, 1, "f32"), (63, 16, 1, 4, "bf16"),
+                                           (64, 64, 6, 1, "bf16"), (65, 64, 6, 8, "bf16"),
+                                           (1000, 256, 8, 8, "bf16"), (777, 512, 32, 4, "f32"),
+                                           (4096, 16, 1, 1, "bf16")])
+def test_plan_pack_bitexact(N, E, k, R, dtype):
+    cfg = CONFIGS["tiny"].scaled(n_tokens=N, n_experts=E, top_k=k, ep_size=R, hidden=128, dtype=dtype)
+    ids = synthetic_topk_ids(N, E, k, seed=N + E, device=DEV, skew=1.1)
+    x = torch.randn((N, 128), device=DEV).to(torch.float32 if dtype == "f32" else torch.bfloat16)
+    out = plan_gpu(cfg, ids, x)
+    ref = oracle.dispatch_plan(ids.cpu().numpy(), E, R)
+    for key in ("counts", "offsets", "rank_offsets", "slot_to_row", "row_to_slot"):
+        assert np.array_equal(out[key].cpu().numpy(), ref[key]), key
+    send_ref = oracle.pack(x.cpu().float().numpy(), ref["slot_to_row"], k)
+    assert np.array_equal(out["send"].cpu().float().numpy(), send_ref)
+
+
+def test_receive_rows_bitexact():
+    cfg = CONFIGS["dsv3_prefill"].scaled(n_tokens=300, ep_rank=5)
+    R, N, E, k = cfg.ep_size, cfg.n_tokens, cfg.n_experts, cfg.top_k
+    plans = [oracle.dispatch_plan(synthetic_topk_ids(N, E, k, seed=s, skew=0.7).numpy(), E, R)
+             for s in range(R)]
+    cnt = np.stack([p["counts"] for p in plans])
+    off = np.stack([p["offsets"] for p in plans])
+    rows_ref, goff_ref = oracle.receive_rows(cnt, off, cfg.cap, cfg.ep_rank, cfg.n_local)
+    rows = torch.full((R * cfg.cap,), -7, dtype=torch.int32, device=DEV)
+    goff = torch.empty(cfg.n_local + 1, dtype=torch.int32, device=DEV)
+    L.fs_receive_rows(L.make_desc(cfg), torch.from_numpy(cnt).to(DEV), torch.from_numpy(off).to(DEV),
+                      rows, goff)
+    torch.cuda.synchronize()
+    assert np.array_equal(goff.cpu().numpy(), goff_ref)
+    assert np.array_equal(rows.cpu().numpy()[:len(rows_ref)], rows_ref)
+
+
+def ragged_groups(G, total_hint, seed):
+    g = np.random.default_rng(seed)
+    counts = g.integers(0, 2 * total_hint // G + 1, size=G)
+    counts[0] = 0                   # an empty group
+    counts[min(1, G - 1)] = 1       # a single row
+    if G > 2:
+        counts[2] = 300             # several m-tiles with a ragged tail
+    return counts
+
+
+@pytest.mark.parametrize("dtype,G,d,F,gather", [("f32", 5, 256, 512, False), ("f32", 3, 128, 192, True),
+                                                ("bf16", 6, 512, 256, False), ("bf16", 4, 384, 320, True),
+                                                ("bf16", 1, 256, 128, False)])
+def test_grouped_ffn(dtype, G, d, F, gather):
+    counts = ragged_groups(G, 600, seed=G + d)
+    M = int(counts.sum())
+    goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    gen = torch.Generator(device=DEV).manual_seed(d + F)
+    n_src = M + 37
+    X = torch.randn((n_src, d), generator=gen, device=DEV).to(tdt)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(tdt)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(tdt)
+    rows = torch.randperm(n_src, generator=gen, device=DEV)[:M].to(torch.int32) if gather else None
+    out = torch.full((n_src, d), float("nan"), device=DEV).to(tdt)
+    cfg = CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype=dtype)
+    desc = L.make_desc(cfg)
+    L.fs_grouped_expert_ffn(desc, G, F, X, rows, torch.from_numpy(goff).to(DEV), M, wgu, wd, out,
+                            ws_for(desc, L.FS_OP_GROUPED_FFN, M, F))
+    torch.cuda.synchronize()
+    Xn, gun, dnn = f64(X), f64(wgu), f64(wd)
+    rr = rows.cpu().numpy() if gather else np.arange(M)
+    outn = f64(out)
+    for gi in range(G):
+        sel = rr[goff[gi]:goff[gi + 1]]
+        if len(sel) == 0:
+            continue
+        want = oracle.swiglu(Xn[sel], gun[gi], dnn[gi])
+        assert rel_err(outn[sel], want) <= TOL[dtype], f"group {gi}"
+    untouched = np.setdiff1d(np.arange(n_src), rr)
+    assert np.all(np.isnan(outn[untouched]))
+
+
+@pytest.mark.parametrize("dtype,m,n,kd", [("f32", 70, 128, 256), ("bf16", 300, 256, 512), ("bf16", 1, 128, 64)])
+def test_dense_linear(dtype, m, n, kd):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    gen = torch.Generator(device=DEV).manual_seed(m)
+    a = torch.randn((m, kd), generator=gen, device=DEV).to(tdt)
+    w = (0.05 * torch.randn((n, kd), generator=gen, device=DEV)).to(tdt)
+    out = torch.empty((m, n), dtype=tdt, device=DEV)
+    L.fs_dense_linear(L.FS_F32 if dtype == "f32" else L.FS_BF16, m, n, kd, a, w, out)
+    torch.cuda.synchronize()
+    assert rel_err(out, oracle.dense_linear(f64(a), f64(w))) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,N,k,d,shared", [("f32", 37, 2, 256, False), ("bf16", 130, 8, 512, True),
+                                                ("bf16", 5, 1, 128, False)])
+def test_combine_and_residual(dtype, N, k, d, shared):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    cfg = CONFIGS["tiny"].scaled(n_tokens=N, top_k=k, hidden=d, n_experts=16, dtype=dtype)
+    desc = L.make_desc(cfg)
+    ids = synthetic_topk_ids(N, 16, k, seed=N)
+    plan = oracle.dispatch_plan(ids.numpy(), 16, 1)
+    gen = torch.Generator(device=DEV).manual_seed(d)
+    y = torch.randn((N * k, d), generator=gen, device=DEV).to(tdt)
+    w = torch.rand((N, k), generator=gen, device=DEV)
+    sh = torch.randn((N, d), generator=gen, device=DEV).to(tdt) if shared else None
+    resid = torch.randn((N, d), generator=gen, device=DEV).to(tdt)
+    resid0 = resid.clone()
+    routed = torch.empty((N, d), dtype=tdt, device=DEV)
+    s2r = torch.from_numpy(plan["slot_to_row"]).to(DEV)
+    L.fs_combine_unpack(desc, y, s2r, w, sh, routed, resid)
+    torch.cuda.synchronize()
+    acc = oracle.combine(f64(y), plan["slot_to_row"], f64(w))
+    if shared:
+        acc = acc + f64(sh)
+    assert rel_err(routed, acc) <= TOL[dtype]
+    assert rel_err(resid, oracle.residual_add(f64(resid0), acc)) <= TOL[dtype]
+    # the plain FarSkip residual add, out of place and in place
+    out = torch.empty_like(resid)
+    L.fs_farskip_residual(desc, out, resid0, routed, sh)
+    torch.cuda.synchronize()
+    extra = [f64(sh)] if shared else []
+    assert rel_err(out, oracle.residual_add(f64(resid0), f64(routed), *extra)) <= TOL[dtype]
+    want_inplace = oracle.residual_add(f64(resid0), f64(routed))
+    L.fs_farskip_residual(desc, resid0, resid0, routed)
+    torch.cuda.synchronize()
+    assert rel_err(resid0, want_inplace) <= TOL[dtype]
