@@ -23,7 +23,10 @@
  *               row-major with the leading dimension stated.  The library
  *               never allocates or frees device memory; scratch space is a
  *               caller-provided workspace sized by fs_workspace_size().
- *   Alignment   Device pointers must be 16-byte aligned.
+ *   Alignment   Arrays of tokens, weights, expert outputs and residuals
+ *               (accessed as 16-byte vectors) must be 16-byte aligned;
+ *               int32 index arrays and fp32 logit / gate / bias arrays
+ *               4-byte aligned.
  *   Element     FS_F32 or FS_BF16 selects the type of tokens, weights,
  *   types       expert outputs and residuals (desc->dtype); router logits,
  *               gate weights and the selection bias are always fp32;
@@ -39,7 +42,7 @@
  *               the detail for the calling thread.  Device faults surface at
  *               the caller's next synchronisation.  The library never
  *               aborts and never prints.
- *   Shapes      hidden % 64 == 0, ffn % 64 == 0, 1 <= top_k <= min(E, 32),
+ *   Shapes      hidden % 128 == 0, ffn % 64 == 0, 1 <= top_k <= min(E, 32),
  *               E <= 512, E % n_groups == 0, n_groups <= 64,
  *               top_k <= topk_groups * E / n_groups, E % ep_size == 0,
  *               ep_size * n_tokens * top_k < 2^31.  n_tokens == 0 is a

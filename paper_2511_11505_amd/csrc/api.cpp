@@ -30,11 +30,23 @@ fs_status hip_fail(hipError_t e, const char* where) {
   } while (0)
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool aligned4(const void* p) { return ((uintptr_t)p & 3u) == 0; }
 
 #define NEED(ptr, name)                                                                      \
   do {                                                                                       \
     if (!(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must not be NULL");        \
     if (!aligned16(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must be 16-byte aligned"); \
+  } while (0)
+// int32 index arrays and fp32 gate arrays are read element by element
+#define NEED4(ptr, name)                                                                     \
+  do {                                                                                       \
+    if (!(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must not be NULL");        \
+    if (!aligned4(ptr)) return fail(FS_ERR_INVALID, std::string(name) + " must be 4-byte aligned"); \
+  } while (0)
+#define OPT4(ptr, name)                                                                      \
+  do {                                                                                       \
+    if ((ptr) && !aligned4(ptr))                                                             \
+      return fail(FS_ERR_INVALID, std::string(name) + " must be 4-byte aligned");            \
   } while (0)
 #define OPT(ptr, name)                                                                       \
   do {                                                                                       \
@@ -246,14 +258,14 @@ fs_status fs_router_topk(const fs_moe_desc* desc, const void* x, const void* w_r
       return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_ROUTER_TOPK)");
     NEED(ws, "ws");
   } else {
-    OPT(logits_in, "logits_in");
+    OPT4(logits_in, "logits_in");
   }
   if (sel_bias && desc->score == FS_SOFTMAX)
     return fail(FS_ERR_UNSUPPORTED, "a selection bias is defined for sigmoid scoring only");
-  OPT(sel_bias, "sel_bias");
-  OPT(logits_out, "logits_out");
-  NEED(topk_ids, "topk_ids");
-  NEED(topk_w, "topk_w");
+  OPT4(sel_bias, "sel_bias");
+  OPT4(logits_out, "logits_out");
+  NEED4(topk_ids, "topk_ids");
+  NEED4(topk_w, "topk_w");
   return router_impl(desc, x, w_router, sel_bias, logits_in, logits_out, topk_ids, topk_w, ws,
                      S(stream));
 }
@@ -284,13 +296,13 @@ fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, con
   fs_status st = check_desc(desc);
   if (st != FS_OK) return st;
   if (desc->n_tokens == 0) return FS_OK;
-  NEED(topk_ids, "topk_ids");
+  NEED4(topk_ids, "topk_ids");
   NEED(x, "x");
-  NEED(expert_counts, "expert_counts");
-  NEED(expert_offsets, "expert_offsets");
-  NEED(rank_offsets, "rank_offsets");
-  NEED(slot_to_row, "slot_to_row");
-  NEED(row_to_slot, "row_to_slot");
+  NEED4(expert_counts, "expert_counts");
+  NEED4(expert_offsets, "expert_offsets");
+  NEED4(rank_offsets, "rank_offsets");
+  NEED4(slot_to_row, "slot_to_row");
+  NEED4(row_to_slot, "row_to_slot");
   NEED(send, "send");
   if (ws_bytes < plan_bytes(desc))
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_DISPATCH_PACK)");
@@ -304,10 +316,10 @@ fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
                           fs_stream stream) {
   fs_status st = check_desc(desc);
   if (st != FS_OK) return st;
-  NEED(src_counts, "src_counts");
-  NEED(src_offsets, "src_offsets");
-  NEED(group_rows, "group_rows");
-  NEED(group_offsets, "group_offsets");
+  NEED4(src_counts, "src_counts");
+  NEED4(src_offsets, "src_offsets");
+  NEED4(group_rows, "group_rows");
+  NEED4(group_offsets, "group_offsets");
   FS_HIP(fs::launch_receive_rows(src_counts, src_offsets, desc->ep_size, desc->n_experts,
                                  desc->ep_rank, (int64_t)desc->n_tokens * desc->top_k,
                                  group_rows, group_offsets, S(stream)),
@@ -333,8 +345,8 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
     return fail(FS_ERR_INVALID, "group_offsets may be NULL only with n_groups == 1");
   if (max_rows == 0) return FS_OK;
   NEED(in_rows, "in_rows");
-  OPT(group_rows, "group_rows");
-  OPT(group_offsets, "group_offsets");
+  OPT4(group_rows, "group_rows");
+  OPT4(group_offsets, "group_offsets");
   NEED(w_gate_up, "w_gate_up");
   NEED(w_down, "w_down");
   NEED(out_rows, "out_rows");
@@ -357,8 +369,8 @@ fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
   if (st != FS_OK) return st;
   if (desc->n_tokens == 0) return FS_OK;
   NEED(y_ret, "y_ret");
-  NEED(slot_to_row, "slot_to_row");
-  NEED(topk_w, "topk_w");
+  NEED4(slot_to_row, "slot_to_row");
+  NEED4(topk_w, "topk_w");
   OPT(shared_out, "shared_out");
   OPT(routed_out, "routed_out");
   OPT(residual, "residual");
@@ -464,18 +476,18 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   NEED(residual_in, "residual_in");
   if (begin) {
     NEED(wt->w_router, "weights->w_router");
-    OPT(wt->sel_bias, "weights->sel_bias");
+    OPT4(wt->sel_bias, "weights->sel_bias");
     if (wt->sel_bias && desc->score == FS_SOFTMAX)
       return fail(FS_ERR_UNSUPPORTED, "a selection bias is defined for sigmoid scoring only");
     NEED(partial_out, "partial_out");
     NEED(b->send, "buffers->send");
-    NEED(b->row_to_slot, "buffers->row_to_slot");
+    NEED4(b->row_to_slot, "buffers->row_to_slot");
     if (desc->n_shared > 0) {
       NEED(wt->ws_gate_up, "weights->ws_gate_up");
       NEED(wt->ws_down, "weights->ws_down");
       NEED(b->shared_out, "buffers->shared_out");
     }
-    OPT(b->logits, "buffers->logits");
+    OPT4(b->logits, "buffers->logits");
   }
   if (finish) {
     NEED(wt->w_gate_up, "weights->w_gate_up");
@@ -483,16 +495,16 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     NEED(residual_io, "residual_io");
     NEED(b->y, "buffers->y");
     if (R > 1) {
-      NEED(b->group_rows, "buffers->group_rows");
-      NEED(b->group_offsets, "buffers->group_offsets");
+      NEED4(b->group_rows, "buffers->group_rows");
+      NEED4(b->group_offsets, "buffers->group_offsets");
     }
   }
-  NEED(b->topk_ids, "buffers->topk_ids");
-  NEED(b->topk_w, "buffers->topk_w");
-  NEED(b->src_counts, "buffers->src_counts");
-  NEED(b->src_offsets, "buffers->src_offsets");
-  NEED(b->rank_offsets, "buffers->rank_offsets");
-  NEED(b->slot_to_row, "buffers->slot_to_row");
+  NEED4(b->topk_ids, "buffers->topk_ids");
+  NEED4(b->topk_w, "buffers->topk_w");
+  NEED4(b->src_counts, "buffers->src_counts");
+  NEED4(b->src_offsets, "buffers->src_offsets");
+  NEED4(b->rank_offsets, "buffers->rank_offsets");
+  NEED4(b->slot_to_row, "buffers->slot_to_row");
   if (R > 1 || comm) NEED(b->recv, "buffers->recv");
 
   hipStream_t sc = S(compute), sm = S(comm);

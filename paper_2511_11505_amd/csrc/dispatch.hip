@@ -6,7 +6,7 @@
 //      chose it (LDS OR, order-independent) and its population count;
 //   2. one workgroup scans the per-tile counts into per-tile bases and the
 //      expert offsets;
-//   3. each slot's row = its tile's base for the expert + the number of
+//   3. each slot's row = the expert's offset + its tile's base for the expert + the number of
 //      earlier tokens of the tile with the same expert (popcount of the mask
 //      below the token's lane).
 // Pack copies each token row once from HBM and writes it to its k rows with
@@ -42,7 +42,10 @@ __global__ __launch_bounds__(64) void plan_hist_kernel(const int32_t* __restrict
   }
 }
 
-// One workgroup of 512 threads; thread e owns expert e (E <= 512).
+// One workgroup of 512 threads; thread e owns expert e (E <= 512).  Writes,
+// per tile, the number of earlier tiles' slots on each expert
+// (tile_base[tile][e]), the counts, the exclusive offsets and rank offsets.
+// Tile counts are read 16 at a time so the loads overlap.
 __global__ __launch_bounds__(512) void plan_scan_kernel(const int32_t* __restrict__ hist,
                                                         int n_tiles, int E, int R,
                                                         int32_t* __restrict__ tile_base,
@@ -53,9 +56,15 @@ __global__ __launch_bounds__(512) void plan_scan_kernel(const int32_t* __restric
   const int e = threadIdx.x;
   int run = 0;
   if (e < E) {
-    for (int tl = 0; tl < n_tiles; ++tl) {
-      tile_base[(size_t)tl * E + e] = run;
-      run += hist[(size_t)tl * E + e];
+    for (int t0 = 0; t0 < n_tiles; t0 += 16) {
+      int h[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) h[i] = (t0 + i < n_tiles) ? hist[(size_t)(t0 + i) * E + e] : 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (t0 + i < n_tiles) tile_base[(size_t)(t0 + i) * E + e] = run;
+        run += h[i];
+      }
     }
   }
   sc[e] = (e < E) ? run : 0;
@@ -67,15 +76,12 @@ __global__ __launch_bounds__(512) void plan_scan_kernel(const int32_t* __restric
     __syncthreads();
   }
   const int incl = sc[e];
-  const int excl = incl - ((e < E) ? run : 0);
   if (e < E) {
     counts[e] = run;
-    offsets[e] = excl;
-    for (int tl = 0; tl < n_tiles; ++tl) tile_base[(size_t)tl * E + e] += excl;
+    offsets[e] = incl - run;
   }
   if (e == E - 1) offsets[E] = incl;
   // rank_offsets[r] = offsets[r * E / R]
-  __syncthreads();
   if (e <= R) {
     const int ge = e * (E / R);
     rank_offsets[e] = (ge == 0) ? 0 : sc[ge - 1];
@@ -86,6 +92,7 @@ __global__ __launch_bounds__(64) void plan_rank_kernel(const int32_t* __restrict
                                                        int k, int E,
                                                        const uint64_t* __restrict__ bits,
                                                        const int32_t* __restrict__ tile_base,
+                                                       const int32_t* __restrict__ offsets,
                                                        int32_t* __restrict__ slot_to_row,
                                                        int32_t* __restrict__ row_to_slot) {
   const int tile = blockIdx.x, lane = threadIdx.x;
@@ -98,40 +105,30 @@ __global__ __launch_bounds__(64) void plan_rank_kernel(const int32_t* __restrict
     int row = -1;
     if ((unsigned)e < (unsigned)E) {
       const size_t te = (size_t)tile * E + e;
-      row = tile_base[te] + __popcll(bits[te] & below);
+      row = offsets[e] + tile_base[te] + __popcll(bits[te] & below);
       row_to_slot[row] = slot;
     }
     slot_to_row[slot] = row;
   }
 }
 
-// One wavefront per token; each lane moves 16-byte chunks, four at a time.
+// Each lane moves one 16-byte chunk of one token row: it reads the chunk
+// once and writes it to the token's k send rows.  Waves are laid out
+// (token, 64-chunk block), so short batches still fill the machine.
 template <typename T>
 __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ x,
                                                    const int32_t* __restrict__ slot_to_row, int N,
                                                    int k, int d, T* __restrict__ send) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= N) return;
   const int nch = d * (int)sizeof(T) / 16;
-  const uint4* src = reinterpret_cast<const uint4*>(x + (size_t)t * d);
-  for (int cb = 0; cb < nch; cb += 4 * 64) {
-    uint4 v[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = cb + i * 64 + lane;
-      if (c < nch) v[i] = src[c];
-    }
-    for (int j = 0; j < k; ++j) {
-      const int row = slot_to_row[(size_t)t * k + j];
-      if (row < 0) continue;
-      uint4* dst = reinterpret_cast<uint4*>(send + (size_t)row * d);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = cb + i * 64 + lane;
-        if (c < nch) dst[c] = v[i];
-      }
-    }
+  const int nb = (nch + 63) / 64;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = (int)(wave / nb);
+  const int c = (int)(wave % nb) * 64 + (threadIdx.x & 63);
+  if (t >= N || c >= nch) return;
+  const uint4 v = reinterpret_cast<const uint4*>(x + (size_t)t * d)[c];
+  for (int j = 0; j < k; ++j) {
+    const int row = slot_to_row[(size_t)t * k + j];
+    if (row >= 0) reinterpret_cast<uint4*>(send + (size_t)row * d)[c] = v;
   }
 }
 
@@ -186,14 +183,15 @@ hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* 
   plan_hist_kernel<<<n_tiles, 64, E * sizeof(uint64_t), s>>>(ids, N, k, E, bits, hist);
   plan_scan_kernel<<<1, 512, 0, s>>>(hist, n_tiles, E, R, tile_base, counts, offsets,
                                      rank_offsets);
-  plan_rank_kernel<<<n_tiles, 64, 0, s>>>(ids, N, k, E, bits, tile_base, slot_to_row,
+  plan_rank_kernel<<<n_tiles, 64, 0, s>>>(ids, N, k, E, bits, tile_base, offsets, slot_to_row,
                                           row_to_slot);
   return hipGetLastError();
 }
 
 hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int N, int k, int d,
                        void* send, hipStream_t s) {
-  dim3 grid((N + 3) / 4);
+  const int64_t nb = ((int64_t)d * (dtype == 0 ? 4 : 2) / 16 + 63) / 64;
+  dim3 grid((unsigned)((N * nb + 3) / 4));
   if (dtype == 0)
     pack_kernel<float><<<grid, 256, 0, s>>>((const float*)x, slot_to_row, N, k, d, (float*)send);
   else

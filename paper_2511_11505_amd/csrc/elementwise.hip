@@ -11,7 +11,8 @@
 namespace fs {
 namespace {
 
-// One wavefront per token; each lane handles 16-byte chunks of the row.
+// Each lane handles one 16-byte chunk of one token row; waves are laid out
+// (token, 64-chunk block) so that short batches still fill the machine.
 template <typename T>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
                                                       const int32_t* __restrict__ slot_to_row,
@@ -21,43 +22,43 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
                                                       T* __restrict__ residual, int N, int k,
                                                       int d) {
   constexpr int V = 16 / sizeof(T);
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= N) return;
   const int nch = d / V;
-  const size_t rowoff = (size_t)t * d;
-  for (int c = lane; c < nch; c += 64) {
-    float acc[V];
+  const int nb = (nch + 63) / 64;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int t = (int)(wave / nb);
+  const int c = (int)(wave % nb) * 64 + (threadIdx.x & 63);
+  if (t >= N || c >= nch) return;
+  const size_t off = (size_t)t * d + (size_t)c * V;
+  float acc[V];
 #pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.f;
-    for (int j = 0; j < k; ++j) {
-      const int row = slot_to_row[(size_t)t * k + j];
-      if (row < 0) continue;
-      const float wj = topk_w[(size_t)t * k + j];
-      Vec16<T> v;
-      v.raw = ld16(y + (size_t)row * d + (size_t)c * V);
+  for (int i = 0; i < V; ++i) acc[i] = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const int row = slot_to_row[(size_t)t * k + j];
+    if (row < 0) continue;
+    const float wj = topk_w[(size_t)t * k + j];
+    Vec16<T> v;
+    v.raw = ld16(y + (size_t)row * d + (size_t)c * V);
 #pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = fmaf(wj, v.get(i), acc[i]);
-    }
-    if (shared_out) {
-      Vec16<T> v;
-      v.raw = ld16(shared_out + rowoff + (size_t)c * V);
+    for (int i = 0; i < V; ++i) acc[i] = fmaf(wj, v.get(i), acc[i]);
+  }
+  if (shared_out) {
+    Vec16<T> v;
+    v.raw = ld16(shared_out + off);
 #pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] += v.get(i);
-    }
-    if (routed_out) {
-      Vec16<T> o;
+    for (int i = 0; i < V; ++i) acc[i] += v.get(i);
+  }
+  if (routed_out) {
+    Vec16<T> o;
 #pragma unroll
-      for (int i = 0; i < V; ++i) o.set(i, acc[i]);
-      st16(routed_out + rowoff + (size_t)c * V, o.raw);
-    }
-    if (residual) {
-      Vec16<T> rv, o;
-      rv.raw = ld16(residual + rowoff + (size_t)c * V);
+    for (int i = 0; i < V; ++i) o.set(i, acc[i]);
+    st16(routed_out + off, o.raw);
+  }
+  if (residual) {
+    Vec16<T> rv, o;
+    rv.raw = ld16(residual + off);
 #pragma unroll
-      for (int i = 0; i < V; ++i) o.set(i, rv.get(i) + acc[i]);
-      st16(residual + rowoff + (size_t)c * V, o.raw);
-    }
+    for (int i = 0; i < V; ++i) o.set(i, rv.get(i) + acc[i]);
+    st16(residual + off, o.raw);
   }
 }
 
@@ -87,7 +88,8 @@ __global__ __launch_bounds__(256) void residual_kernel(T* out, const T* a, const
 hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_row,
                           const float* topk_w, const void* shared_out, void* routed_out,
                           void* residual, int N, int k, int d, hipStream_t s) {
-  dim3 grid((N + 3) / 4);
+  const int64_t nb = ((int64_t)d / (dtype == 0 ? 4 : 8) + 63) / 64;
+  dim3 grid((unsigned)((N * nb + 3) / 4));
   if (dtype == 0)
     combine_kernel<float><<<grid, 256, 0, s>>>((const float*)y_ret, slot_to_row, topk_w,
                                                (const float*)shared_out, (float*)routed_out,

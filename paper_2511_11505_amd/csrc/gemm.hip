@@ -17,6 +17,10 @@
 // (workgroups are dispatched round-robin over the XCDs), so tiles sharing a
 // weight panel or a row panel run under one L2.
 
+#include <stdlib.h>
+
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -248,6 +252,507 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(
   }
 }
 
+// ---------------------------------------------------------------- bf16 MFMA, DMA ring
+// BM x BN x 64 tiles, four waves (2 x 2), each wave BM/2 x BN/2 through
+// v_mfma_f32_32x32x16_bf16.  Operand tiles stream into an LDS ring of
+// STAGES slots with direct global->LDS 16-byte loads (no staging
+// registers), STAGES-1 K blocks ahead of the MFMAs.  A 64-element K row is
+// 8 chunks of 16 bytes; chunk c of row r sits at position c ^ ((r / 2) % 8):
+// the LDS serves a ds_read_b128 sixteen lanes at a time over 64 banks, and
+// sixteen consecutive rows then cover all 64 banks once.  Rows past the end of a group load a valid row of the
+// group instead (a DMA cannot write zeros); their results are never stored.
+// The epilogue stages the output tile through LDS so that global stores are
+// whole 16-byte row chunks.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// lds_wave_base + 16 * l.  Issued as inline assembly so that the compiler
+// does not add a conservative wait for every outstanding DMA before each LDS
+// read; the kernel orders them itself with explicit vmcnt waits and
+// barriers.  M0 carries the LDS base and has no other user in this kernel.
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave_base) {
+  const unsigned lds = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(lds_void_t*)lds_wave_base);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds), "v"(g)
+               : "memory");
+}
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int MODE, int BM, int BN, int BK, int STAGES, int OCC>
+__global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
+    int NOUT, bf16_t* __restrict__ C, int ldc) {
+  constexpr int NT = 256;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int ROWB = BK * 2;                       // bytes per staged row
+  constexpr int CPR = BK / 8;                        // 16-byte chunks per staged row
+  constexpr int RPB = 1024 / ROWB;                   // rows per 1 KB DMA block
+  constexpr int SWD = 16 / CPR;                      // rows sharing one swizzle value
+  constexpr int STAGE = (BM + BN) * ROWB;            // bytes per ring slot
+  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;  // DMA blocks per wave per slot
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
+  constexpr int ECOL = 128;                          // output columns staged per epilogue pass
+  constexpr int CST = ECOL + 8;                      // epilogue LDS row stride (bf16)
+  constexpr int KS = BK / 16;                        // MFMA K steps per block
+  static_assert(BK == 32 || BK == 64, "K block");
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
+  static_assert(NCOL % ECOL == 0, "epilogue passes");
+  static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
+  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
+  static_assert(MODE != MODE_DOWN || WTN == ECOL, "one epilogue pass per wave column");
+  static_assert(STAGES >= 2, "ring");
+
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const int KT = K / BK;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+  // This lane's place inside a 1 KB DMA block: row l / CPR, position l % CPR;
+  // it fetches the logical chunk stored at that position.
+  const int drow = lane / CPR, dpos = lane % CPR;
+  auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group(s_tpre, G, nn, L);
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const int m0 = mt * BM, n0 = nt * NCOL;
+    const bf16_t* Bg = B + (size_t)g * bstride;
+
+    const bf16_t* pa[A_LD];
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int blk = wave * A_LD + i;
+      int m = m0 + blk * RPB + drow;
+      if (m >= rows_g) m = rows_g - 1;
+      const int grow = row_base + m;
+      const int64_t src = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      pa[i] = A + src * K + dchunk(blk) * 8;
+    }
+    const bf16_t* pb[B_LD];
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int blk = wave * B_LD + i;
+      const int r = blk * RPB + drow;
+      int wrow;
+      if (MODE == MODE_GATEUP)
+        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
+      else
+        wrow = n0 + r;
+      pb[i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
+    }
+    auto issue = [&](int kt) {
+      unsigned char* slot = ring + (kt % STAGES) * STAGE;
+#pragma unroll
+      for (int i = 0; i < A_LD; ++i) dma16(pa[i] + kt * BK, slot + (wave * A_LD + i) * 1024);
+#pragma unroll
+      for (int i = 0; i < B_LD; ++i)
+        dma16(pb[i] + kt * BK, slot + BM * ROWB + (wave * B_LD + i) * 1024);
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
+
+    // fragment rows of this lane and their byte offsets inside a slot
+    int aoff[TM], boff[TN], asw[TM], bsw[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WTM + i * 32 + (lane & 31);
+      aoff[i] = r * ROWB;
+      asw[i] = (r / SWD) % CPR;
+    }
+#pragma unroll
+    for (int jn = 0; jn < TN; ++jn) {
+      int r;
+      if (MODE == MODE_GATEUP)
+        r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+      else
+        r = wn * WTN + jn * 32;
+      r += lane & 31;
+      boff[jn] = BM * ROWB + r * ROWB;
+      bsw[jn] = (r / SWD) % CPR;
+    }
+
+#pragma unroll
+    for (int st = 0; st < STAGES - 1; ++st)
+      if (st < KT) issue(st);
+    for (int kt = 0; kt < KT; ++kt) {
+      // block kt has landed once at most the blocks issued after it remain
+      const int after = min(STAGES - 2, KT - 1 - kt);
+      if (after >= STAGES - 2)
+        wait_vmcnt<(STAGES - 2) * (A_LD + B_LD)>();
+      else if (STAGES > 3 && after == 1)
+        wait_vmcnt<(STAGES > 3 ? 1 : 0) * (A_LD + B_LD)>();
+      else if (STAGES > 4 && after == 2)
+        wait_vmcnt<(STAGES > 4 ? 2 : 0) * (A_LD + B_LD)>();
+      else if (STAGES > 5 && after == 3)
+        wait_vmcnt<(STAGES > 5 ? 3 : 0) * (A_LD + B_LD)>();
+      else if (STAGES > 6 && after == 4)
+        wait_vmcnt<(STAGES > 6 ? 4 : 0) * (A_LD + B_LD)>();
+      else
+        wait_vmcnt<0>();
+      barrier_nofence();
+      if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1);
+      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
+      // all fragments of the K block first, then its MFMAs: the LDS latency
+      // is exposed once per block instead of once per 16-wide K step
+      bf16x8 af[KS][TM], bfr[KS][TN];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c = ks * 2 + (lane >> 5);   // logical 16-byte chunk of this lane
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[ks][i] = *reinterpret_cast<const bf16x8*>(slot + aoff[i] + ((c ^ asw[i]) << 4));
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn)
+          bfr[ks][jn] = *reinterpret_cast<const bf16x8*>(slot + boff[jn] + ((c ^ bsw[jn]) << 4));
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn)
+            acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][jn],
+                                                                 acc[i][jn], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, KS * (TM + TN), 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, KS * TM * TN, 0);
+    }
+
+    // Epilogue: accumulator element v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
+    // column l%32 of its 32x32 tile.  Passes of 128 output columns are
+    // staged as bf16 in the ring, then stored as 16-byte row chunks.
+    bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
+    constexpr int PASSES = NCOL / ECOL;
+#pragma unroll
+    for (int pass = 0; pass < PASSES; ++pass) {
+      barrier_nofence();
+      if (MODE == MODE_GATEUP || wn == pass) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            if (MODE == MODE_GATEUP) {
+#pragma unroll
+              for (int jn = 0; jn < TN / 2; ++jn) {
+                const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+                const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
+                Cs[r * CST + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+              }
+            } else {
+#pragma unroll
+              for (int jn = 0; jn < TN; ++jn) {
+                const int col = jn * 32 + (lane & 31);
+                Cs[r * CST + col] = f2bf(acc[i][jn][v]);
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();
+      constexpr int CPRC = ECOL / 8;   // 16-byte chunks per staged row
+#pragma unroll 4
+      for (int c = tid; c < BM * CPRC; c += NT) {
+        const int r = c / CPRC, ch = c % CPRC;
+        const int m = m0 + r;
+        if (m < rows_g) {
+          const int grow = row_base + m;
+          const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+          st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
+               *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
+        }
+      }
+    }
+    __syncthreads();   // the ring is reused by the next tile
+  }
+}
+
+// ---------------------------------------------------------------- bf16 MFMA, interleaved
+// Same tiles, ring and swizzle as above, with the memory work hidden under
+// the MFMAs by a rolling pipeline over 16-wide K steps.  Each step first
+// issues the LDS reads of the next step's fragments (double-buffered
+// registers), then its own MFMAs; the DMAs of the block two ahead are spread
+// over the first steps of a block, one after each of the first MFMAs.  The
+// block's last step starts with the only barrier of the block, once the
+// next block has landed.  A wave issues memory instructions in the shadow of
+// an executing MFMA, so with one wave per SIMD the MFMA pipe stays busy.
+// The grid is persistent (one workgroup per CU).
+
+__device__ __forceinline__ void wait_lgkm0() {
+  // lgkmcnt(0), vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
+}
+
+template <int MODE, int BM, int BN, int BK, int OCC>
+__global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
+    int NOUT, bf16_t* __restrict__ C, int ldc) {
+  constexpr int NT = 256, STAGES = 3;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int ROWB = BK * 2;
+  constexpr int CPR = BK / 8;
+  constexpr int RPB = 1024 / ROWB;
+  constexpr int SWD = 16 / CPR;
+  constexpr int STAGE = (BM + BN) * ROWB;
+  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;
+  constexpr int NLD = A_LD + B_LD;
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
+  constexpr int ECOL = 128;
+  constexpr int CST = ECOL + 8;
+  constexpr int KS = BK / 16;                      // K steps per block
+  constexpr int NF = TM + TN;                      // fragments per K step
+  constexpr int MPS = TM * TN;                     // MFMAs per K step
+  constexpr int DPS = (NLD + KS - 2) / (KS - 1);   // DMAs per step (steps 0..KS-2)
+  static_assert(KS >= 2, "at least two K steps per block");
+  static_assert(DPS <= MPS, "one DMA per MFMA at most");
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
+  static_assert(NCOL % ECOL == 0, "epilogue passes");
+  static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
+  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
+  static_assert(MODE != MODE_DOWN || WTN == ECOL, "one epilogue pass per wave column");
+
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const int KT = K / BK;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+  const int drow = lane / CPR, dpos = lane % CPR;
+  auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
+
+  // fragment byte offsets inside a slot, per K step (tile-independent)
+  int aoff[TM], boff[TN], asw[TM], bsw[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + (lane & 31);
+    aoff[i] = r * ROWB;
+    asw[i] = (r / SWD) % CPR;
+  }
+#pragma unroll
+  for (int jn = 0; jn < TN; ++jn) {
+    int r;
+    if (MODE == MODE_GATEUP)
+      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+    else
+      r = wn * WTN + jn * 32;
+    r += lane & 31;
+    boff[jn] = BM * ROWB + r * ROWB;
+    bsw[jn] = (r / SWD) % CPR;
+  }
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group(s_tpre, G, nn, L);
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const int m0 = mt * BM, n0 = nt * NCOL;
+    const bf16_t* Bg = B + (size_t)g * bstride;
+
+    // DMA sources: NLD 16-byte chunks per lane per K block
+    const bf16_t* src[NLD];
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int blk = wave * A_LD + i;
+      int m = m0 + blk * RPB + drow;
+      if (m >= rows_g) m = rows_g - 1;
+      const int grow = row_base + m;
+      const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      src[i] = A + sr * K + dchunk(blk) * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int blk = wave * B_LD + i;
+      const int r = blk * RPB + drow;
+      int wrow;
+      if (MODE == MODE_GATEUP)
+        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
+      else
+        wrow = n0 + r;
+      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
+    }
+    auto dst_of = [&](int i) {
+      return i < A_LD ? (wave * A_LD + i) * 1024 : BM * ROWB + (wave * B_LD + (i - A_LD)) * 1024;
+    };
+    auto dma_one = [&](int i, int kt) {
+      dma16(src[i] + kt * BK, ring + (kt % STAGES) * STAGE + dst_of(i));
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
+
+    bf16x8 Fa[NF], Fb[NF];
+    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
+      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
+      const int c = ks * 2 + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        F[i] = *reinterpret_cast<const bf16x8*>(slot + aoff[i] + ((c ^ asw[i]) << 4));
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+        F[TM + jn] = *reinterpret_cast<const bf16x8*>(slot + boff[jn] + ((c ^ bsw[jn]) << 4));
+    };
+    // One K step: reads of the next step, then the MFMAs of this one with
+    // up to DPS DMAs of block kt+2 after the first MFMAs.
+    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks) {
+      if (ks == KS - 1) {
+        // the next block must have landed for every wave before its reads
+        if (kt + 1 < KT) {
+          wait_lgkm0();
+          if (kt + 2 < KT)
+            wait_vmcnt<NLD>();
+          else
+            wait_vmcnt<0>();
+          barrier_nofence();
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (ks < KS - 1)
+        read_step(Fn, kt, ks + 1);
+      else if (kt + 1 < KT)
+        read_step(Fn, kt + 1, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < MPS; ++q) {
+        const int i = q / TN, jn = q % TN;
+        acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
+        if (ks < KS - 1 && q < DPS) {
+          const int d = ks * DPS + q;
+          if (d < NLD) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (kt + 2 < KT) dma_one(d, kt + 2);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // prologue: blocks 0 and 1 in flight, block 0's first fragments read
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) dma_one(i, 0);
+    if (KT > 1) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) dma_one(i, 1);
+      wait_vmcnt<NLD>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    barrier_nofence();
+    read_step(Fa, 0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 2) {
+        step(Fa, Fb, kt, ks);
+        step(Fb, Fa, kt, ks + 1);
+      }
+    }
+
+    // Epilogue (as in the kernel above).
+    bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
+    constexpr int PASSES = NCOL / ECOL;
+#pragma unroll
+    for (int pass = 0; pass < PASSES; ++pass) {
+      __syncthreads();
+      if (MODE == MODE_GATEUP || wn == pass) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            if (MODE == MODE_GATEUP) {
+#pragma unroll
+              for (int jn = 0; jn < TN / 2; ++jn) {
+                const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+                const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
+                Cs[r * CST + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+              }
+            } else {
+#pragma unroll
+              for (int jn = 0; jn < TN; ++jn) {
+                const int col = jn * 32 + (lane & 31);
+                Cs[r * CST + col] = f2bf(acc[i][jn][v]);
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();
+      constexpr int CPRC = ECOL / 8;
+#pragma unroll 4
+      for (int c = tid; c < BM * CPRC; c += NT) {
+        const int r = c / CPRC, ch = c % CPRC;
+        const int m = m0 + r;
+        if (m < rows_g) {
+          const int grow = row_base + m;
+          const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+          st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
+               *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------- fp32 VALU
 // 64 x 64 tiles, 256 threads, 4 rows x 4 columns per thread.  For gate/up a
 // tile holds 32 gate and the matching 32 up columns; a thread owns 2 H
@@ -370,12 +875,37 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 
+// Tile shape of the DMA-ring GEMM.  The default (4: 128 x 256 x 32, three
+// slots, two workgroups per CU) was the fastest measured; FS_GEMM_TILE (0-6)
+// selects another shape for tuning.
+int dma_tile_choice() {
+  static const int choice = [] {
+    const char* e = getenv("FS_GEMM_TILE");
+    return e ? atoi(e) : 4;
+  }();
+  return choice;
+}
+
 int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
   int64_t upper = (cdiv64(max_rows, BM) + G) * nn;
   upper = ((upper + kXcd - 1) / kXcd) * kXcd;
   if (upper < kXcd) upper = kXcd;
   const int64_t cap = (int64_t)kXcd * 65536;
   return upper > cap ? cap : upper;
+}
+
+// occ workgroups per compute unit (capped by the tile count, a multiple of 8).
+int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  const int64_t upper = grid_for(max_rows, G, BM, nn);
+  int64_t g = ((int64_t)cus * occ + kXcd - 1) / kXcd * kXcd;
+  return g < upper ? g : upper;
 }
 
 }  // namespace
@@ -390,7 +920,48 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
                               hipStream_t s, bool profile) {
   if (max_rows <= 0) return hipSuccess;
-  if (dtype == 1) {
+  if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
+    bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+    const int cfg = dma_tile_choice();
+#define FS_DMA(BM_, BN_, BK_, ST_, OCC_)                                                         \
+  do {                                                                                         \
+    const int64_t g1 = grid_for(max_rows, G, BM_, ffn / (BN_ / 2));                            \
+    if (profile) prof_begin(4, s);                                                             \
+    gemm_bf16_dma_kernel<MODE_GATEUP, BM_, BN_, BK_, ST_, OCC_><<<(unsigned)g1, 256, 0, s>>>(  \
+        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn); \
+    if (profile) prof_end(4, s);                                                               \
+    const int64_t g2 = grid_for(max_rows, G, BM_, d / BN_);                                    \
+    if (profile) prof_begin(5, s);                                                             \
+    gemm_bf16_dma_kernel<MODE_DOWN, BM_, BN_, BK_, ST_, OCC_><<<(unsigned)g2, 256, 0, s>>>(    \
+        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);           \
+    if (profile) prof_end(5, s);                                                               \
+  } while (0)
+#define FS_IL(BM_, BN_, BK_, OCC_)                                                               \
+  do {                                                                                         \
+    const int64_t g1 = persistent_grid(max_rows, G, BM_, ffn / (BN_ / 2), OCC_);               \
+    if (profile) prof_begin(4, s);                                                             \
+    gemm_bf16_il_kernel<MODE_GATEUP, BM_, BN_, BK_, OCC_><<<(unsigned)g1, 256, 0, s>>>(        \
+        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn); \
+    if (profile) prof_end(4, s);                                                               \
+    const int64_t g2 = persistent_grid(max_rows, G, BM_, d / BN_, OCC_);                       \
+    if (profile) prof_begin(5, s);                                                             \
+    gemm_bf16_il_kernel<MODE_DOWN, BM_, BN_, BK_, OCC_><<<(unsigned)g2, 256, 0, s>>>(          \
+        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);           \
+    if (profile) prof_end(5, s);                                                               \
+  } while (0)
+    switch (cfg) {
+      case 0: FS_DMA(128, 256, 64, 3, 1); break;
+      case 1: FS_DMA(128, 256, 32, 6, 1); break;
+      case 2: FS_DMA(256, 256, 64, 2, 1); break;
+      case 3: FS_DMA(256, 256, 32, 4, 1); break;
+      case 4: FS_DMA(128, 256, 32, 3, 2); break;
+      case 5: FS_IL(128, 256, 64, 1); break;
+      case 6: FS_IL(128, 256, 32, 2); break;
+      default: FS_DMA(128, 256, 32, 3, 2); break;
+    }
+#undef FS_DMA
+#undef FS_IL
+  } else if (dtype == 1) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     const int64_t g1 = grid_for(max_rows, G, kBM, ffn / (kBN / 2));
     if (profile) prof_begin(4, s);

@@ -191,8 +191,17 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       if (n_partials == 0) {
         v = src[(size_t)t * E + e];
       } else {
+        // slice sums in ascending order; loads are issued eight at a time
         float a = 0.f;
-        for (int s = 0; s < n_partials; ++s) a = a + src[((size_t)s * N + t) * E + e];
+        int s = 0;
+        for (; s + 8 <= n_partials; s += 8) {
+          float p[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) p[i] = src[((size_t)(s + i) * N + t) * E + e];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) a = a + p[i];
+        }
+        for (; s < n_partials; ++s) a = a + src[((size_t)s * N + t) * E + e];
         v = a;
       }
       if (logits_out) logits_out[(size_t)t * E + e] = v;

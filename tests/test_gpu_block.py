@@ -159,5 +159,10 @@ def test_farskip_differs_from_regular_only_through_the_dropped_input():
     want = oracle.dense_linear(ref["x"] + ref["shared"], wn) - oracle.dense_linear(
         ref["x"] + ref["shared"] + ref["routed"], wn)
     got = f64(fs_out) - f64(reg_out)
-    assert rel_err(got, want) <= 1e-4
+    # Each output is an fp32 sum rounded a few times (residual adds, the
+    # next-layer GEMM): the difference carries at most a few ulps of the
+    # outputs' magnitude, which cancellation does not shrink.
+    ulp = 2.0 ** -23 * max(np.abs(f64(fs_out)).max(), np.abs(f64(reg_out)).max())
+    assert np.max(np.abs(got - want)) <= 16 * ulp
+    assert np.abs(want).max() > 100 * 16 * ulp   # the dropped input is visible
     blk.close()
