@@ -44,7 +44,7 @@ def measured_traffic(cfg_name):
     src = os.path.join(ROOT, rec["source"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
         return None
-    if os.environ.get("FS_GEMM_TILE") not in (None, "", "4"):
+    if os.environ.get("FS_GEMM_TILE") not in (None, "", str(rec.get("tile", ""))):
         return None
     return rec["hbm_bytes_per_launch"]
 
@@ -170,20 +170,36 @@ def main():
     ms = start.elapsed_time(end) / args.steps
     kernels = kernel_table(L, args.steps)
 
-    # roofline of the dominant kernel: the routed gate/up SwiGLU GEMM
+    # roofline of the dominant kernel: the routed gate/up SwiGLU GEMM.  Its
+    # algorithmic work is 2 M d 2F flops; its algorithmic HBM bytes are the
+    # weights of the experts that received rows, the M input rows and the M
+    # rows of H it writes.  The bound is the roof that takes longer.
+    es = cfg.elem_bytes
     flops_gate_up = 2.0 * M * cfg.hidden * 2 * cfg.ffn
+    lo = cfg.ep_rank * cfg.n_local
+    rows_per_expert = blk.t["src_counts"][:, lo:lo + cfg.n_local].sum(0)
+    active = int((rows_per_expert > 0).sum().item())
+    bytes_gate_up = (active * 2 * cfg.ffn * cfg.hidden + M * cfg.hidden + M * cfg.ffn) * es
     gu = kernels.get("gate_up")
     roof = None
     if gu:
-        achieved = flops_gate_up / (gu["us_per_launch"] * 1e-6) / 1e12
-        peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS
-        roof = {"bound": "mfma" if cfg.dtype == "bf16" else "alu", "kernel": "gate_up SwiGLU grouped GEMM",
-                "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+        t = gu["us_per_launch"] * 1e-6
+        peak_f = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS
+        compute_bound = flops_gate_up / (peak_f * 1e12) >= bytes_gate_up / (PEAK_HBM_GBS * 1e9)
+        if compute_bound:
+            achieved, peak, unit = flops_gate_up / t / 1e12, peak_f, "TFLOP/s"
+            bound = "mfma" if cfg.dtype == "bf16" else "alu"
+        else:
+            achieved, peak, unit, bound = bytes_gate_up / t / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
+        roof = {"bound": bound, "kernel": "gate_up SwiGLU grouped GEMM",
+                "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(cfg.name),
                 "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                "algorithmic_flops_per_launch": flops_gate_up}
+                "algorithmic_flops_per_launch": flops_gate_up,
+                "algorithmic_bytes_per_launch": bytes_gate_up, "experts_with_rows": active,
+                "mfma_frac": round(flops_gate_up / t / 1e12 / peak_f, 4),
+                "hbm_frac": round(bytes_gate_up / t / 1e9 / PEAK_HBM_GBS, 4)}
     # permute kernels against HBM (algorithmic bytes)
-    es = cfg.elem_bytes
     N, d, k, E = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts
     hbm = {}
     if "pack" in kernels:
@@ -215,7 +231,7 @@ def main():
                    "shared": cfg.n_shared, "ep_size": cfg.ep_size, "rows_local_experts": M,
                    "second_stream": comm is not None},
         "roofline": roof,
-        "grouped_gemm_frac_bf16_peak": None if roof is None else roof["frac"],
+        "grouped_gemm_frac_bf16_peak": None if roof is None else roof["mfma_frac"],
         "permute_frac_hbm": {k2: round(v / PEAK_HBM_GBS, 4) for k2, v in hbm.items()},
         "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in kernels.items()},
     }

@@ -7,15 +7,17 @@
 //   down:     Y[row_i] = H[i] . Wd^T                        (rows scattered
 //             through group_rows)
 // bf16 runs on MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) with both
-// operand tiles staged through LDS, double-buffered, with the next K block
-// prefetched into registers.  fp32 runs on the vector ALUs.
+// operand tiles staged through a ring of LDS slots: direct global->LDS copies
+// (DMA kernels) or loads a block ahead into registers (register-staged
+// kernel).  The launcher picks the tile variant per pass from the shape.
+// fp32 runs on the vector ALUs.
 //
 // Groups have ragged row counts known only on the device.  Every workgroup
 // rebuilds the per-group m-tile prefix from group_offsets in LDS, then walks
-// the tile space (group, n-tile, m-tile; m fastest) in a persistent loop.
-// The tile space is cut into eight contiguous ranges, one per XCD
-// (workgroups are dispatched round-robin over the XCDs), so tiles sharing a
-// weight panel or a row panel run under one L2.
+// the tile space (group, n-tile, m-tile; m fastest) in a loop.  The tile
+// space is cut into eight contiguous ranges, one per XCD (workgroups are
+// dispatched round-robin over the XCDs), so tiles sharing a weight panel or
+// a row panel run under one L2.
 
 #include <stdlib.h>
 
@@ -30,6 +32,13 @@ namespace {
 constexpr int kMaxGroups = 512;
 constexpr int kXcd = 8;
 enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
+
+// SiLU(g) * u for the bf16 epilogues, whose result is rounded to bf16: the
+// hardware exponential and reciprocal (about 1 ulp each in fp32) replace the
+// IEEE division, which costs ten instructions per element.
+__device__ __forceinline__ float swiglu_bf16_epi(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
 
 // Group offsets and the exclusive prefix of m-tiles per group, in LDS.
 template <int NT, int BM>
@@ -234,7 +243,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(
 #pragma unroll
           for (int jn = 0; jn < TN / 2; ++jn) {
             const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
-            const float h = gt / (1.0f + __expf(-gt)) * up;
+            const float h = swiglu_bf16_epi(gt, up);
             const int col = n0 + wn * (WTN / 2) + jn * 32 + (lane & 31);
             C[(size_t)grow * ldc + col] = f2bf(h);
           }
@@ -294,31 +303,91 @@ __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
-template <int MODE, int BM, int BN, int BK, int STAGES, int OCC>
-__global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
+// Tile epilogue shared by the LDS-ring kernels.  Accumulator element v of
+// lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32 of its 32x32 tile.
+// Passes of 128 output columns are staged as bf16 in the ring (which must be
+// idle), then stored as 16-byte row chunks; gate/up tiles apply SwiGLU to
+// matching gate and up accumulators first.  Ends with a barrier, after which
+// the ring may be refilled.
+template <int MODE, int BM, int NCOL, int TM, int TN, int WTM, int WTN, int NT>
+__device__ __forceinline__ void store_tile(floatx16 (&acc)[TM][TN], unsigned char* ring, int wm,
+                                           int wn, int lane, int tid, int m0, int rows_g,
+                                           int row_base, const int32_t* __restrict__ rows,
+                                           bf16_t* __restrict__ C, int ldc, int n0) {
+  constexpr int ECOL = 128;
+  constexpr int CST = ECOL + 8;
+  constexpr int PASSES = NCOL / ECOL;
+  static_assert(NCOL % ECOL == 0, "epilogue passes");
+  static_assert(MODE != MODE_GATEUP || (TN % 2 == 0 && 2 * (WTN / 2) == ECOL), "gate/up pairing");
+  static_assert(MODE != MODE_DOWN || ECOL % WTN == 0, "a wave's columns stay in one pass");
+  bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
+#pragma unroll
+  for (int pass = 0; pass < PASSES; ++pass) {
+    __syncthreads();
+    if (MODE == MODE_GATEUP || (wn * WTN) / ECOL == pass) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          if (MODE == MODE_GATEUP) {
+#pragma unroll
+            for (int jn = 0; jn < TN / 2; ++jn) {
+              const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+              Cs[r * CST + wn * (WTN / 2) + jn * 32 + (lane & 31)] = f2bf(swiglu_bf16_epi(gt, up));
+            }
+          } else {
+#pragma unroll
+            for (int jn = 0; jn < TN; ++jn)
+              Cs[r * CST + (wn * WTN) % ECOL + jn * 32 + (lane & 31)] = f2bf(acc[i][jn][v]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    constexpr int CPRC = ECOL / 8;
+#pragma unroll 4
+    for (int c = tid; c < BM * CPRC; c += NT) {
+      const int r = c / CPRC, ch = c % CPRC;
+      const int m = m0 + r;
+      if (m < rows_g) {
+        const int grow = row_base + m;
+        const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+        st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
+             *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
+      }
+    }
+  }
+  __syncthreads();
+}
+
+template <int MODE, int BM, int BN, int BK, int STAGES, int WM, int WN, int OCC>
+__global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
     const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
     int NOUT, bf16_t* __restrict__ C, int ldc) {
-  constexpr int NT = 256;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int NW = WM * WN, NT = 64 * NW;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int ROWB = BK * 2;                       // bytes per staged row
   constexpr int CPR = BK / 8;                        // 16-byte chunks per staged row
   constexpr int RPB = 1024 / ROWB;                   // rows per 1 KB DMA block
   constexpr int SWD = 16 / CPR;                      // rows sharing one swizzle value
   constexpr int STAGE = (BM + BN) * ROWB;            // bytes per ring slot
-  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;  // DMA blocks per wave per slot
+  constexpr int A_LD = BM / RPB / NW, B_LD = BN / RPB / NW;  // DMA blocks per wave per slot
+  constexpr int NLD = A_LD + B_LD;
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
   constexpr int ECOL = 128;                          // output columns staged per epilogue pass
   constexpr int CST = ECOL + 8;                      // epilogue LDS row stride (bf16)
   constexpr int KS = BK / 16;                        // MFMA K steps per block
   static_assert(BK == 32 || BK == 64, "K block");
-  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (NW * RPB) == 0 && BN % (NW * RPB) == 0, "tile");
   static_assert(NCOL % ECOL == 0, "epilogue passes");
   static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
-  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
-  static_assert(MODE != MODE_DOWN || WTN == ECOL, "one epilogue pass per wave column");
-  static_assert(STAGES >= 2, "ring");
+  static_assert(MODE != MODE_GATEUP || (TN % 2 == 0 && WN * WTN / 2 == ECOL), "gate/up pairing");
+  static_assert(MODE != MODE_DOWN || ECOL % WTN == 0, "a wave's columns stay in one pass");
+  static_assert(STAGES >= 2 && STAGES <= 6, "ring");
+  static_assert(NLD * (STAGES - 2) < 64, "vmcnt range");
 
   __shared__ int s_goff[kMaxGroups + 1];
   __shared__ int s_tpre[kMaxGroups + 1];
@@ -326,7 +395,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
   __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
 
   const int nn = NOUT / NCOL;
@@ -340,6 +409,26 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
   // it fetches the logical chunk stored at that position.
   const int drow = lane / CPR, dpos = lane % CPR;
   auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
+
+  // fragment rows of this lane and their byte offsets inside a slot
+  int aoff[TM], boff[TN], asw[TM], bsw[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + (lane & 31);
+    aoff[i] = r * ROWB;
+    asw[i] = (r / SWD) % CPR;
+  }
+#pragma unroll
+  for (int jn = 0; jn < TN; ++jn) {
+    int r;
+    if (MODE == MODE_GATEUP)
+      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+    else
+      r = wn * WTN + jn * 32;
+    r += lane & 31;
+    boff[jn] = BM * ROWB + r * ROWB;
+    bsw[jn] = (r / SWD) % CPR;
+  }
 
   for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
     const int64_t L = xcd_base + j;
@@ -391,26 +480,6 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
 
-    // fragment rows of this lane and their byte offsets inside a slot
-    int aoff[TM], boff[TN], asw[TM], bsw[TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int r = wm * WTM + i * 32 + (lane & 31);
-      aoff[i] = r * ROWB;
-      asw[i] = (r / SWD) % CPR;
-    }
-#pragma unroll
-    for (int jn = 0; jn < TN; ++jn) {
-      int r;
-      if (MODE == MODE_GATEUP)
-        r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
-      else
-        r = wn * WTN + jn * 32;
-      r += lane & 31;
-      boff[jn] = BM * ROWB + r * ROWB;
-      bsw[jn] = (r / SWD) % CPR;
-    }
-
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st)
       if (st < KT) issue(st);
@@ -418,15 +487,13 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
       // block kt has landed once at most the blocks issued after it remain
       const int after = min(STAGES - 2, KT - 1 - kt);
       if (after >= STAGES - 2)
-        wait_vmcnt<(STAGES - 2) * (A_LD + B_LD)>();
-      else if (STAGES > 3 && after == 1)
-        wait_vmcnt<(STAGES > 3 ? 1 : 0) * (A_LD + B_LD)>();
-      else if (STAGES > 4 && after == 2)
-        wait_vmcnt<(STAGES > 4 ? 2 : 0) * (A_LD + B_LD)>();
-      else if (STAGES > 5 && after == 3)
-        wait_vmcnt<(STAGES > 5 ? 3 : 0) * (A_LD + B_LD)>();
-      else if (STAGES > 6 && after == 4)
-        wait_vmcnt<(STAGES > 6 ? 4 : 0) * (A_LD + B_LD)>();
+        wait_vmcnt<(STAGES - 2) * NLD>();
+      else if (after == 3)
+        wait_vmcnt<(STAGES > 5 ? 3 : 0) * NLD>();
+      else if (after == 2)
+        wait_vmcnt<(STAGES > 4 ? 2 : 0) * NLD>();
+      else if (after == 1)
+        wait_vmcnt<(STAGES > 3 ? 1 : 0) * NLD>();
       else
         wait_vmcnt<0>();
       barrier_nofence();
@@ -465,7 +532,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
 #pragma unroll
     for (int pass = 0; pass < PASSES; ++pass) {
       barrier_nofence();
-      if (MODE == MODE_GATEUP || wn == pass) {
+      if (MODE == MODE_GATEUP || (wn * WTN) / ECOL == pass) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -476,12 +543,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_dma_kernel(
               for (int jn = 0; jn < TN / 2; ++jn) {
                 const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
                 const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+                Cs[r * CST + col] = f2bf(swiglu_bf16_epi(gt, up));
               }
             } else {
 #pragma unroll
               for (int jn = 0; jn < TN; ++jn) {
-                const int col = jn * 32 + (lane & 31);
+                const int col = (wn * WTN) % ECOL + jn * 32 + (lane & 31);
                 Cs[r * CST + col] = f2bf(acc[i][jn][v]);
               }
             }
@@ -522,12 +589,12 @@ __device__ __forceinline__ void wait_lgkm0() {
   __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
 }
 
-template <int MODE, int BM, int BN, int BK, int OCC>
+template <int MODE, int BM, int BN, int BK, int STAGES, int OCC>
 __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
     int NOUT, bf16_t* __restrict__ C, int ldc) {
-  constexpr int NT = 256, STAGES = 3;
+  constexpr int NT = 256;
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int ROWB = BK * 2;
@@ -543,7 +610,15 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   constexpr int KS = BK / 16;                      // K steps per block
   constexpr int NF = TM + TN;                      // fragments per K step
   constexpr int MPS = TM * TN;                     // MFMAs per K step
-  constexpr int DPS = (NLD + KS - 2) / (KS - 1);   // DMAs per step (steps 0..KS-2)
+  // read r of the next step goes out after MFMA read_slot(r) of this one
+  auto read_slot = [](int r) { return ((r + 1) * MPS) / NF - 1; };
+  // The DMAs of block kt + STAGES - 1 go out during block kt: spread over its
+  // steps 0..KS-2 with three or more slots, all in step 0 with two (they must
+  // land before the block's last step).
+  constexpr int DSTEPS = (STAGES == 2) ? 1 : KS - 1;
+  constexpr int DPS = (NLD + DSTEPS - 1) / DSTEPS;  // DMAs per step
+  static_assert(STAGES >= 2 && STAGES <= 6, "ring of two to six slots");
+  static_assert(NLD * (STAGES - 2) < 64, "vmcnt range");
   static_assert(KS >= 2, "at least two K steps per block");
   static_assert(DPS <= MPS, "one DMA per MFMA at most");
   static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
@@ -640,71 +715,91 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
 
     bf16x8 Fa[NF], Fb[NF];
-    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
+    // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
+    // A1..A(TM-1); read r is issued after MFMA read_slot(r) of the step before
+    auto read_one = [&](bf16x8 (&F)[NF], int kt, int ks, int r) {
       const unsigned char* slot = ring + (kt % STAGES) * STAGE;
       const int c = ks * 2 + (lane >> 5);
+      const int f = r == 0 ? 0 : (r <= TN ? TM + r - 1 : r - TN);
+      const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
+      F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
+    };
+    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        F[i] = *reinterpret_cast<const bf16x8*>(slot + aoff[i] + ((c ^ asw[i]) << 4));
-#pragma unroll
-      for (int jn = 0; jn < TN; ++jn)
-        F[TM + jn] = *reinterpret_cast<const bf16x8*>(slot + boff[jn] + ((c ^ bsw[jn]) << 4));
+      for (int r = 0; r < NF; ++r) read_one(F, kt, ks, r);
     };
     // One K step: reads of the next step, then the MFMAs of this one with
-    // up to DPS DMAs of block kt+2 after the first MFMAs.
-    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks) {
-      if (ks == KS - 1) {
-        // the next block must have landed for every wave before its reads
-        if (kt + 1 < KT) {
-          wait_lgkm0();
-          if (kt + 2 < KT)
-            wait_vmcnt<NLD>();
-          else
-            wait_vmcnt<0>();
-          barrier_nofence();
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (ks < KS - 1)
-        read_step(Fn, kt, ks + 1);
-      else if (kt + 1 < KT)
-        read_step(Fn, kt + 1, 0);
-      __builtin_amdgcn_sched_barrier(0);
+    // up to DPS DMAs of block kt + STAGES - 1 after the first MFMAs.  PF
+    // (a compile-time flag) says whether that block exists, so the main
+    // loop carries no per-DMA branch.
+    // One K step: the MFMAs of this step, with the reads of the next step's
+    // fragments spread between them (in the order the next step uses them)
+    // and up to DPS DMAs of block kt + STAGES - 1 after the first MFMAs.  A
+    // block's last step waits for the next block after its first MFMA, so the
+    // MFMA pipe is busy during the barrier.  PF (a compile-time flag) says
+    // whether block kt + STAGES - 1 exists, so the main loop carries no
+    // per-DMA branch.
+    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks, auto PF) {
+      constexpr bool pf = decltype(PF)::value;
+      const bool more = ks < KS - 1 || kt + 1 < KT;
+      const int rkt = ks < KS - 1 ? kt : kt + 1, rks = ks < KS - 1 ? ks + 1 : 0;
 #pragma unroll
       for (int q = 0; q < MPS; ++q) {
         const int i = q / TN, jn = q % TN;
         acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
-        if (ks < KS - 1 && q < DPS) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (q == 0 && ks == KS - 1 && (pf || kt + 1 < KT)) {
+          // block kt+1 has landed once at most the DMAs of the blocks issued
+          // after it (kt+2 .. kt+STAGES-1) remain; near the end fewer were
+          // issued, and the wait is complete
+          wait_lgkm0();
+          if (pf)
+            wait_vmcnt<(STAGES - 2) * NLD>();
+          else
+            wait_vmcnt<0>();
+          barrier_nofence();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int r = 0; r < NF; ++r)
+          if (q == read_slot(r) && more) read_one(Fn, rkt, rks, r);
+        if (ks < DSTEPS && q < DPS) {
           const int d = ks * DPS + q;
           if (d < NLD) {
-            __builtin_amdgcn_sched_barrier(0);
-            if (kt + 2 < KT) dma_one(d, kt + 2);
-            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (pf) dma_one(d, kt + STAGES - 1);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
     };
 
-    // prologue: blocks 0 and 1 in flight, block 0's first fragments read
+    // prologue: blocks 0 .. STAGES-2 in flight, block 0's first fragments read
 #pragma unroll
     for (int i = 0; i < NLD; ++i) dma_one(i, 0);
-    if (KT > 1) {
+    if (KT >= STAGES - 1) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) dma_one(i, 1);
-      wait_vmcnt<NLD>();
+      for (int b = 1; b < STAGES - 1; ++b)
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) dma_one(i, b);
+      wait_vmcnt<(STAGES - 2) * NLD>();
     } else {
+      for (int b = 1; b < KT; ++b)
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) dma_one(i, b);
       wait_vmcnt<0>();
     }
     barrier_nofence();
     read_step(Fa, 0, 0);
-    for (int kt = 0; kt < KT; ++kt) {
+    auto run_block = [&](int kt, auto PF) {
 #pragma unroll
       for (int ks = 0; ks < KS; ks += 2) {
-        step(Fa, Fb, kt, ks);
-        step(Fb, Fa, kt, ks + 1);
+        step(Fa, Fb, kt, ks, PF);
+        step(Fb, Fa, kt, ks + 1, PF);
       }
-    }
+    };
+    const int kt_pf = KT - (STAGES - 1);   // blocks that issue a prefetch
+    for (int kt = 0; kt < kt_pf; ++kt) run_block(kt, std::true_type{});
+    for (int kt = kt_pf < 0 ? 0 : kt_pf; kt < KT; ++kt) run_block(kt, std::false_type{});
 
     // Epilogue (as in the kernel above).
     bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
@@ -723,7 +818,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
               for (int jn = 0; jn < TN / 2; ++jn) {
                 const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
                 const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+                Cs[r * CST + col] = f2bf(swiglu_bf16_epi(gt, up));
               }
             } else {
 #pragma unroll
@@ -750,6 +845,205 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
       }
     }
     __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- bf16 MFMA, register-staged
+// 256 x 256 x 64 tiles: four waves of 128 x 128 (sixteen 32x32 accumulators
+// each, held in AGPRs), one wave per SIMD, two LDS slots of 64 KB.  A K block's
+// operand tiles are loaded into registers one whole block ahead (block kt+2
+// during block kt) and written to the free LDS slot at the start of the next
+// block, so a global load has a full block of MFMAs (64 per wave) to land,
+// where a direct-to-LDS copy into a two-slot ring would have three K steps.
+// Rows are 128 bytes (BK = 64 bf16), so every 8-lane group of a load reads
+// one whole cache line.
+//
+// Per block kt (four 16-wide K steps, rolling fragment reads as above):
+//   step 0: MFMAs, each followed by one LDS write of block kt+1
+//   step 1: MFMAs, each followed by one global load of block kt+2
+//   step 3: wait for this wave's LDS traffic, barrier, then read block kt+1.
+// The barrier of block kt-1 is what frees slot (kt+1) % 2 for the writes.
+template <int MODE, int BM, int BN, int BK>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_rs_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
+    int NOUT, bf16_t* __restrict__ C, int ldc) {
+  constexpr int NT = 256, STAGES = 2;
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int ROWB = BK * 2;
+  constexpr int CPR = BK / 8;
+  constexpr int RPB = 1024 / ROWB;
+  constexpr int SWD = 16 / CPR;
+  constexpr int STAGE = (BM + BN) * ROWB;
+  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;
+  constexpr int NLD = A_LD + B_LD;
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
+  constexpr int KS = BK / 16;
+  constexpr int NF = TM + TN;
+  constexpr int MPS = TM * TN;
+  auto read_slot = [](int r) { return ((r + 1) * MPS) / NF - 1; };
+  static_assert(KS >= 2 && KS % 2 == 0, "an even number of K steps per block");
+  static_assert(MPS >= NF, "one fragment read per MFMA at most");
+  static_assert(NLD <= MPS, "one LDS write and one global load per MFMA at most");
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
+  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
+
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const int KT = K / BK;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+  // lane l loads row l / CPR of a 1 KB block, the logical chunk that the
+  // swizzle stores at position l % CPR; it writes LDS linearly at l * 16
+  const int drow = lane / CPR, dpos = lane % CPR;
+  auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
+
+  int aoff[TM], boff[TN], asw[TM], bsw[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + (lane & 31);
+    aoff[i] = r * ROWB;
+    asw[i] = (r / SWD) % CPR;
+  }
+#pragma unroll
+  for (int jn = 0; jn < TN; ++jn) {
+    int r;
+    if (MODE == MODE_GATEUP)
+      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+    else
+      r = wn * WTN + jn * 32;
+    r += lane & 31;
+    boff[jn] = BM * ROWB + r * ROWB;
+    bsw[jn] = (r / SWD) % CPR;
+  }
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group(s_tpre, G, nn, L);
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const int m0 = mt * BM, n0 = nt * NCOL;
+    const bf16_t* Bg = B + (size_t)g * bstride;
+
+    const bf16_t* src[NLD];
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int blk = wave * A_LD + i;
+      int m = m0 + blk * RPB + drow;
+      if (m >= rows_g) m = rows_g - 1;
+      const int grow = row_base + m;
+      const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      src[i] = A + sr * K + dchunk(blk) * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int blk = wave * B_LD + i;
+      const int r = blk * RPB + drow;
+      int wrow;
+      if (MODE == MODE_GATEUP)
+        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
+      else
+        wrow = n0 + r;
+      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
+    }
+    auto dst_of = [&](int i) {
+      return (i < A_LD ? (wave * A_LD + i) * 1024 : BM * ROWB + (wave * B_LD + (i - A_LD)) * 1024) +
+             lane * 16;
+    };
+    uint4 stg[NLD];
+    auto gload = [&](int i, int kt) { stg[i] = ld16(src[i] + kt * BK); };
+    auto lwrite = [&](int i, int kt) { st16(ring + (kt % STAGES) * STAGE + dst_of(i), stg[i]); };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
+
+    bf16x8 Fa[NF], Fb[NF];
+    // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
+    // A1..A(TM-1); read r is issued after MFMA read_slot(r) of the step before
+    auto read_one = [&](bf16x8 (&F)[NF], int kt, int ks, int r) {
+      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
+      const int c = ks * 2 + (lane >> 5);
+      const int f = r == 0 ? 0 : (r <= TN ? TM + r - 1 : r - TN);
+      const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
+      F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
+    };
+    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
+#pragma unroll
+      for (int r = 0; r < NF; ++r) read_one(F, kt, ks, r);
+    };
+    // N1 / N2 (compile-time flags): blocks kt+1 / kt+2 exist.  Reads of the
+    // next step's fragments are spread between the MFMAs as in the DMA kernel.
+    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks, auto N1, auto N2) {
+      constexpr bool n1 = decltype(N1)::value, n2 = decltype(N2)::value;
+      const bool more = ks < KS - 1 || n1;
+      const int rkt = ks < KS - 1 ? kt : kt + 1, rks = ks < KS - 1 ? ks + 1 : 0;
+#pragma unroll
+      for (int q = 0; q < MPS; ++q) {
+        const int i = q / TN, jn = q % TN;
+        acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (n1 && q == 0 && ks == KS - 1) {
+          wait_lgkm0();
+          barrier_nofence();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int r = 0; r < NF; ++r)
+          if (q == read_slot(r) && more) read_one(Fn, rkt, rks, r);
+        if (q < NLD) {
+          if (n1 && ks == 0) lwrite(q, kt + 1);
+          if (n2 && ks == 1) gload(q, kt + 2);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    auto run_block = [&](int kt, auto N1, auto N2) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 2) {
+        step(Fa, Fb, kt, ks, N1, N2);
+        step(Fb, Fa, kt, ks + 1, N1, N2);
+      }
+    };
+
+    // prologue: block 0 in slot 0, block 1 in registers, block 0's first
+    // fragments read
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) gload(i, 0);
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) lwrite(i, 0);
+    if (KT > 1) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) gload(i, 1);
+    }
+    wait_lgkm0();
+    barrier_nofence();
+    read_step(Fa, 0, 0);
+    for (int kt = 0; kt + 2 < KT; ++kt) run_block(kt, std::true_type{}, std::true_type{});
+    if (KT >= 2) run_block(KT - 2, std::true_type{}, std::false_type{});
+    run_block(KT - 1, std::false_type{}, std::false_type{});
+
+    store_tile<MODE, BM, NCOL, TM, TN, WTM, WTN, NT>(acc, ring, wm, wn, lane, tid, m0, rows_g,
+                                                     row_base, rows, C, ldc, n0);
   }
 }
 
@@ -875,15 +1169,24 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 
-// Tile shape of the DMA-ring GEMM.  The default (4: 128 x 256 x 32, three
-// slots, two workgroups per CU) was the fastest measured; FS_GEMM_TILE (0-6)
-// selects another shape for tuning.
-int dma_tile_choice() {
-  static const int choice = [] {
+// Tile variant of the LDS-ring GEMMs, per pass, from the measured expert
+// shapes: gate/up takes the register-staged 256 x 256 x 64 kernel (8) when
+// the groups average at least 2048 rows (dense, shared-expert-like) and the
+// interleaved 128 x 256 x 64 ring (5) otherwise, where half-empty 256-row
+// tail tiles would waste MFMA work; down takes the interleaved ring (5) for
+// K >= 2816 and the eight-wave 256 x 256 x 32 DMA ring (2) below that.
+// FS_GEMM_TILE / FS_GEMM_TILE_DOWN (0-9) force a variant, for tuning.
+int tile_choice(bool down, int64_t max_rows, int G, int K) {
+  static const int gu_env = [] {
     const char* e = getenv("FS_GEMM_TILE");
-    return e ? atoi(e) : 4;
+    return e ? atoi(e) : -1;
   }();
-  return choice;
+  static const int dn_env = [] {
+    const char* e = getenv("FS_GEMM_TILE_DOWN");
+    return e ? atoi(e) : -1;
+  }();
+  if (down) return dn_env >= 0 ? dn_env : (K >= 2816 ? 5 : 2);
+  return gu_env >= 0 ? gu_env : (max_rows >= 2048 * (int64_t)G ? 8 : 5);
 }
 
 int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
@@ -908,6 +1211,55 @@ int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
   return g < upper ? g : upper;
 }
 
+// One bf16 GEMM pass with the LDS-ring variant v.  NCOL output columns per
+// tile: BN / 2 for gate/up (a tile holds matching gate and up rows), BN for
+// down.
+template <int MODE, int BM, int BN, int BK, int ST, int WM, int WN, int OCC>
+void run_dma(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
+             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
+  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
+  const int64_t g = grid_for(m_total, G, BM, NOUT / NCOL);
+  gemm_bf16_dma_kernel<MODE, BM, BN, BK, ST, WM, WN, OCC>
+      <<<(unsigned)g, 64 * WM * WN, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+}
+template <int MODE, int BM, int BN, int BK, int ST, int OCC>
+void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
+            const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
+  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
+  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, OCC);
+  gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>
+      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+}
+template <int MODE, int BM, int BN, int BK>
+void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
+            const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
+  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
+  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
+  gemm_bf16_rs_kernel<MODE, BM, BN, BK>
+      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+}
+// Every variant has BN = 256 and BK <= 64: it needs NOUT % 128 == 0 for
+// gate/up, NOUT % 256 == 0 for down and K % 64 == 0.
+template <int MODE>
+void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
+               int64_t m_total, const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc,
+               hipStream_t s) {
+#define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
+  switch (v) {
+    case 0: run_dma<MODE, 128, 256, 64, 3, 2, 2, 1>(FS_ARGS); break;
+    case 1: run_dma<MODE, 128, 256, 32, 6, 2, 2, 1>(FS_ARGS); break;
+    case 2: run_dma<MODE, 256, 256, 32, 4, 2, 4, 1>(FS_ARGS); break;
+    case 3: run_dma<MODE, 256, 256, 64, 2, 2, 4, 1>(FS_ARGS); break;
+    case 5: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS); break;
+    case 6: run_il<MODE, 128, 256, 32, 3, 2>(FS_ARGS); break;
+    case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS); break;
+    case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
+    case 9: run_il<MODE, 256, 256, 32, 4, 1>(FS_ARGS); break;
+    default: run_dma<MODE, 128, 256, 32, 3, 2, 2, 2>(FS_ARGS); break;
+  }
+#undef FS_ARGS
+}
+
 }  // namespace
 
 size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn) {
@@ -922,45 +1274,14 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
   if (max_rows <= 0) return hipSuccess;
   if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
-    const int cfg = dma_tile_choice();
-#define FS_DMA(BM_, BN_, BK_, ST_, OCC_)                                                         \
-  do {                                                                                         \
-    const int64_t g1 = grid_for(max_rows, G, BM_, ffn / (BN_ / 2));                            \
-    if (profile) prof_begin(4, s);                                                             \
-    gemm_bf16_dma_kernel<MODE_GATEUP, BM_, BN_, BK_, ST_, OCC_><<<(unsigned)g1, 256, 0, s>>>(  \
-        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn); \
-    if (profile) prof_end(4, s);                                                               \
-    const int64_t g2 = grid_for(max_rows, G, BM_, d / BN_);                                    \
-    if (profile) prof_begin(5, s);                                                             \
-    gemm_bf16_dma_kernel<MODE_DOWN, BM_, BN_, BK_, ST_, OCC_><<<(unsigned)g2, 256, 0, s>>>(    \
-        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);           \
-    if (profile) prof_end(5, s);                                                               \
-  } while (0)
-#define FS_IL(BM_, BN_, BK_, OCC_)                                                               \
-  do {                                                                                         \
-    const int64_t g1 = persistent_grid(max_rows, G, BM_, ffn / (BN_ / 2), OCC_);               \
-    if (profile) prof_begin(4, s);                                                             \
-    gemm_bf16_il_kernel<MODE_GATEUP, BM_, BN_, BK_, OCC_><<<(unsigned)g1, 256, 0, s>>>(        \
-        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn); \
-    if (profile) prof_end(4, s);                                                               \
-    const int64_t g2 = persistent_grid(max_rows, G, BM_, d / BN_, OCC_);                       \
-    if (profile) prof_begin(5, s);                                                             \
-    gemm_bf16_il_kernel<MODE_DOWN, BM_, BN_, BK_, OCC_><<<(unsigned)g2, 256, 0, s>>>(          \
-        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);           \
-    if (profile) prof_end(5, s);                                                               \
-  } while (0)
-    switch (cfg) {
-      case 0: FS_DMA(128, 256, 64, 3, 1); break;
-      case 1: FS_DMA(128, 256, 32, 6, 1); break;
-      case 2: FS_DMA(256, 256, 64, 2, 1); break;
-      case 3: FS_DMA(256, 256, 32, 4, 1); break;
-      case 4: FS_DMA(128, 256, 32, 3, 2); break;
-      case 5: FS_IL(128, 256, 64, 1); break;
-      case 6: FS_IL(128, 256, 32, 2); break;
-      default: FS_DMA(128, 256, 32, 3, 2); break;
-    }
-#undef FS_DMA
-#undef FS_IL
+    if (profile) prof_begin(4, s);
+    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d), (const bf16_t*)in, rows, goff, G,
+                           max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn, s);
+    if (profile) prof_end(4, s);
+    if (profile) prof_begin(5, s);
+    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn), H, rows, goff, G, max_rows,
+                         (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, s);
+    if (profile) prof_end(5, s);
   } else if (dtype == 1) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     const int64_t g1 = grid_for(max_rows, G, kBM, ffn / (kBN / 2));

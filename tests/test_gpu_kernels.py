@@ -166,7 +166,7 @@ def ragged_groups(G, total_hint, seed):
 
 @pytest.mark.parametrize("dtype,G,d,F,gather", [("f32", 5, 256, 512, False), ("f32", 3, 128, 192, True),
                                                 ("bf16", 6, 512, 256, False), ("bf16", 4, 384, 320, True),
-                                                ("bf16", 1, 256, 128, False)])
+                                                ("bf16", 1, 256, 128, False), ("bf16", 5, 768, 384, True)])
 def test_grouped_ffn(dtype, G, d, F, gather):
     counts = ragged_groups(G, 600, seed=G + d)
     M = int(counts.sum())
