@@ -49,15 +49,43 @@ def measured_traffic(cfg_name):
     return rec["hbm_bytes_per_launch"]
 
 
-def kernel_table(L, steps):
-    names = {L.FS_K_ROUTER: "router", L.FS_K_TOPK: "topk", L.FS_K_PLAN: "plan", L.FS_K_PACK: "pack",
-             L.FS_K_GATE_UP: "gate_up", L.FS_K_DOWN: "down", L.FS_K_COMBINE: "combine"}
+KERNEL_NAMES = ("router", "topk", "plan", "pack", "gate_up", "down", "combine", "shared_gate_up",
+                "shared_down", "dispatch_copy", "next_layer")
+
+
+def kernel_table(L):
+    """Average launch time of each profiled kernel (library HIP events on the
+    stream each one runs on) since the last fs_profile_reset."""
     out = {}
-    for kid, nm in names.items():
+    for kid, nm in enumerate(KERNEL_NAMES):
         ms, n = L.fs_profile_read(kid)
         if n:
             out[nm] = {"us_per_launch": 1e3 * ms / n, "launches": n}
     return out
+
+
+def step_roofs(cfg, M, active):
+    """Algorithmic (bytes, flops, roof time in us) of each step of one pass,
+    at HBM 8 TB/s, bf16 MFMA 2.5 PFLOP/s and fp32 vector 157.3 TFLOP/s."""
+    es = cfg.elem_bytes
+    N, d, k, E, F = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts, cfg.ffn
+    SF = cfg.n_shared * cfg.ffn_shared
+    mm = (PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS) * 1e12
+    hbm, valu = PEAK_HBM_GBS * 1e9, PEAK_F32_VALU_TFLOPS * 1e12
+    steps = {
+        "router": (N * d * es + E * d * es + N * E * 4, 2.0 * N * d * E, valu),
+        "topk": (N * E * 4 + N * k * 8, 0.0, valu),
+        "plan": (12 * N * k, 0.0, valu),
+        "pack": (N * d * es + N * k * d * es + 4 * N * k, 0.0, valu),
+        "gate_up": ((active * 2 * F * d + M * d + M * F) * es, 2.0 * M * d * 2 * F, mm),
+        "down": ((active * d * F + M * F + M * d) * es, 2.0 * M * d * F, mm),
+        "combine": (N * k * d * es + 8 * N * k + 2 * N * d * es, 0.0, valu),
+    }
+    if SF:
+        steps["shared_gate_up"] = ((2 * SF * d + N * d + N * SF) * es, 2.0 * N * d * 2 * SF, mm)
+        steps["shared_down"] = ((d * SF + N * SF + N * d) * es, 2.0 * N * d * SF, mm)
+        steps["partial"] = (3 * N * d * es, 0.0, valu)
+    return {k2: (b, f, 1e6 * max(b / hbm, f / peak)) for k2, (b, f, peak) in steps.items()}
 
 
 def cpu_baseline(cfg, wl, sample_tokens):
@@ -114,6 +142,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serial", action="store_true", help="no second stream")
     ap.add_argument("--rotate", type=int, default=4, help="input sets rotated across steps")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the next-layer stand-in (d x d linear) between BEGIN and FINISH and "
+                         "compare with a serial run")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {args.gpus})",
@@ -149,68 +180,111 @@ def main():
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f}s: {cfg.name}, rows on local experts M={M}")
 
-    def step(i):
+    dt_id = L.FS_F32 if cfg.dtype == "f32" else L.FS_BF16
+    nxts = [torch.empty_like(wl.x) for _ in xs] if args.overlap else None
+    outs = [torch.empty_like(wl.x) for _ in xs] if args.overlap else None
+
+    def step(i, comm_stream):
         j = i % len(xs)
-        blk.begin(xs[j], partials[j], compute=compute, comm=comm)
-        blk.finish(xs[j], partials[j], compute=compute, comm=comm)
+        blk.begin(xs[j], partials[j], compute=compute, comm=comm_stream)
+        if args.overlap:
+            # the far-skipped next layer reads the partial input while the
+            # Dispatch stand-in is in flight; its output joins the residual
+            # before the deferred routed add (Eq. 7)
+            L.fs_dense_linear(dt_id, cfg.n_tokens, cfg.hidden, cfg.hidden, partials[j], wl.w_next,
+                              nxts[j], stream=compute)
+            L.fs_farskip_residual(blk.desc, outs[j], partials[j], nxts[j], stream=compute)
+            blk.finish(xs[j], outs[j], compute=compute, comm=comm_stream)
+        else:
+            blk.finish(xs[j], partials[j], compute=compute, comm=comm_stream)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    L.fs_profile_reset()
-    L.fs_profile_enable(True)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(compute)
-    for i in range(args.steps):
-        step(i)
-    end.record(compute)
-    torch.cuda.synchronize()
-    L.fs_profile_enable(False)
-    ms = start.elapsed_time(end) / args.steps
-    kernels = kernel_table(L, args.steps)
+    def timed(comm_stream):
+        for i in range(args.warmup):
+            step(i, comm_stream)
+        torch.cuda.synchronize()
+        L.fs_profile_reset()
+        L.fs_profile_enable(True)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(compute)
+        for i in range(args.steps):
+            step(i, comm_stream)
+        end.record(compute)
+        torch.cuda.synchronize()
+        L.fs_profile_enable(False)
+        return start.elapsed_time(end) / args.steps, kernel_table(L)
 
-    # roofline of the dominant kernel: the routed gate/up SwiGLU GEMM.  Its
-    # algorithmic work is 2 M d 2F flops; its algorithmic HBM bytes are the
-    # weights of the experts that received rows, the M input rows and the M
-    # rows of H it writes.  The bound is the roof that takes longer.
+    ms, kernels = timed(comm)
+    serial = timed(None) if (args.overlap and comm is not None) else None
+
     es = cfg.elem_bytes
-    flops_gate_up = 2.0 * M * cfg.hidden * 2 * cfg.ffn
+    N, d, k, E = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts
     lo = cfg.ep_rank * cfg.n_local
     rows_per_expert = blk.t["src_counts"][:, lo:lo + cfg.n_local].sum(0)
     active = int((rows_per_expert > 0).sum().item())
-    bytes_gate_up = (active * 2 * cfg.ffn * cfg.hidden + M * cfg.hidden + M * cfg.ffn) * es
-    gu = kernels.get("gate_up")
+    roofs = step_roofs(cfg, M, active)
+    us = lambda name: kernels[name]["us_per_launch"] if name in kernels else None
+    peak_f = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS
+
+    # roofline of the dominant kernel, the routed gate/up SwiGLU GEMM: its
+    # algorithmic work is 2 M d 2F flops and (active experts' gate/up weights
+    # + M input rows + M rows of H) bytes; the bound is the roof that takes
+    # longer, and both fractions are given.
     roof = None
-    if gu:
-        t = gu["us_per_launch"] * 1e-6
-        peak_f = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS
-        compute_bound = flops_gate_up / (peak_f * 1e12) >= bytes_gate_up / (PEAK_HBM_GBS * 1e9)
-        if compute_bound:
-            achieved, peak, unit = flops_gate_up / t / 1e12, peak_f, "TFLOP/s"
+    if us("gate_up"):
+        bytes_gu, flops_gu, _ = roofs["gate_up"]
+        t = us("gate_up") * 1e-6
+        if flops_gu / (peak_f * 1e12) >= bytes_gu / (PEAK_HBM_GBS * 1e9):
+            achieved, peak, unit = flops_gu / t / 1e12, peak_f, "TFLOP/s"
             bound = "mfma" if cfg.dtype == "bf16" else "alu"
         else:
-            achieved, peak, unit, bound = bytes_gate_up / t / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
+            achieved, peak, unit, bound = bytes_gu / t / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
         roof = {"bound": bound, "kernel": "gate_up SwiGLU grouped GEMM",
                 "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(cfg.name),
                 "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                "algorithmic_flops_per_launch": flops_gate_up,
-                "algorithmic_bytes_per_launch": bytes_gate_up, "experts_with_rows": active,
-                "mfma_frac": round(flops_gate_up / t / 1e12 / peak_f, 4),
-                "hbm_frac": round(bytes_gate_up / t / 1e9 / PEAK_HBM_GBS, 4)}
-    # permute kernels against HBM (algorithmic bytes)
-    N, d, k, E = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts
-    hbm = {}
-    if "pack" in kernels:
-        b = N * d * es + N * k * d * es + 4 * N * k
-        hbm["pack"] = b / (kernels["pack"]["us_per_launch"] * 1e-6) / 1e9
-    if "combine" in kernels:
-        b = N * k * d * es + 8 * N * k + 2 * N * d * es
-        hbm["combine"] = b / (kernels["combine"]["us_per_launch"] * 1e-6) / 1e9
-    if "router" in kernels:
-        flops = 2.0 * N * d * E
-        kernels["router"]["tflops"] = flops / (kernels["router"]["us_per_launch"] * 1e-6) / 1e12
+                "algorithmic_flops_per_launch": flops_gu,
+                "algorithmic_bytes_per_launch": bytes_gu, "experts_with_rows": active,
+                "mfma_frac": round(flops_gu / t / 1e12 / peak_f, 4),
+                "hbm_frac": round(bytes_gu / t / 1e9 / PEAK_HBM_GBS, 4)}
+
+    # the whole FFNs (gate/up + down): routed and shared separately, against
+    # the MFMA peak (2 M 3 d F flops) and HBM (weights + activations; the
+    # decode metric)
+    ffn = {}
+    for name, gu_k, dn_k in (("routed", "gate_up", "down"), ("shared", "shared_gate_up", "shared_down")):
+        if us(gu_k) and us(dn_k):
+            t = (us(gu_k) + us(dn_k)) * 1e-6
+            b = roofs[gu_k][0] + roofs[dn_k][0]
+            f = roofs[gu_k][1] + roofs[dn_k][1]
+            ffn[name] = {"us": round(t * 1e6, 2), "tflops": round(f / t / 1e12, 2),
+                         "mfma_frac": round(f / t / 1e12 / peak_f, 4),
+                         "hbm_gbs": round(b / t / 1e9, 1), "hbm_frac": round(b / t / 1e9 / PEAK_HBM_GBS, 4)}
+    # permute kernels and the router against their roofs (algorithmic bytes;
+    # the router against max(bytes / HBM, flops / fp32 vector peak))
+    steps_frac = {}
+    for name in ("router", "topk", "pack", "combine"):
+        if us(name):
+            steps_frac[name] = round(roofs[name][2] / us(name), 4)
+    hbm = {name: roofs[name][0] / (us(name) * 1e-6) / 1e9 for name in ("pack", "combine") if us(name)}
+    # the block against the sum of its steps' roofs (the Dispatch copy is
+    # excluded: on a multi-GPU node it is network time, overlapped)
+    t_roof = sum(r[2] for r in roofs.values())
+    overlap = None
+    if args.overlap:
+        copy_bytes = cfg.cap * d * es
+        overlap = {"next_layer_us": us("next_layer"), "dispatch_copy_us": us("dispatch_copy"),
+                   "dispatch_bytes": copy_bytes,
+                   "xgmi_equivalent_us": round(copy_bytes / 8 / 153e9 * 1e6, 2),
+                   "note": "xgmi_equivalent_us: the same buffer spread over an 8-GPU node, 1/8 per "
+                           "peer at 153 GB/s per link, all links in parallel"}
+        if serial is not None:
+            ms_s, k_s = serial
+            overlap["ms_per_step_serial"] = ms_s
+            overlap["slowdown_under_copy"] = {
+                name: round(kernels[name]["us_per_launch"] / k_s[name]["us_per_launch"] - 1, 4)
+                for name in ("shared_gate_up", "shared_down", "next_layer", "gate_up")
+                if name in kernels and name in k_s}
     res = {
         "metric": METRIC,
         "value": N / (ms * 1e-3),
@@ -226,15 +300,22 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: FarSkip MoE block forward, {N} tokens, d {d}, {E} experts "
                                f"top-{k} {cfg.score}, FFN {cfg.ffn}, {cfg.n_shared} shared, EP rank "
-                               f"{cfg.ep_rank} of {cfg.ep_size}, {cfg.dtype}",
+                               f"{cfg.ep_rank} of {cfg.ep_size}, {cfg.dtype}"
+                               + (", with the next-layer stand-in between BEGIN and FINISH"
+                                  if args.overlap else ""),
                    "tokens": N, "hidden": d, "experts": E, "top_k": k, "ffn": cfg.ffn,
                    "shared": cfg.n_shared, "ep_size": cfg.ep_size, "rows_local_experts": M,
-                   "second_stream": comm is not None},
+                   "second_stream": comm is not None, "next_layer": bool(args.overlap)},
         "roofline": roof,
         "grouped_gemm_frac_bf16_peak": None if roof is None else roof["mfma_frac"],
+        "ffn": ffn,
         "permute_frac_hbm": {k2: round(v / PEAK_HBM_GBS, 4) for k2, v in hbm.items()},
+        "step_roofline_frac": steps_frac,
+        "block_roofline_frac": round(t_roof / (ms * 1e3), 4),
         "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in kernels.items()},
     }
+    if overlap is not None:
+        res["overlap"] = overlap
     if not args.no_cpu_baseline:
         try:
             res["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_sample)

@@ -287,7 +287,11 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
                           const void* w, void* out, fs_stream stream);
 
 /* Per-kernel timing with HIP events recorded on the launch stream around
- * selected kernels.  fs_profile_read synchronises those events. */
+ * selected kernels.  fs_profile_read synchronises those events.
+ * FS_K_GATE_UP / FS_K_DOWN time the routed experts' passes (and
+ * fs_grouped_expert_ffn); FS_K_SHARED_* the shared experts' passes inside
+ * fs_moe_block_forward; FS_K_DISPATCH_COPY the Dispatch stand-in copy on
+ * the comm stream; FS_K_DENSE fs_dense_linear. */
 typedef enum {
   FS_K_ROUTER = 0,
   FS_K_TOPK = 1,
@@ -296,7 +300,11 @@ typedef enum {
   FS_K_GATE_UP = 4,
   FS_K_DOWN = 5,
   FS_K_COMBINE = 6,
-  FS_K_COUNT = 7
+  FS_K_SHARED_GATE_UP = 7,
+  FS_K_SHARED_DOWN = 8,
+  FS_K_DISPATCH_COPY = 9,
+  FS_K_DENSE = 10,
+  FS_K_COUNT = 11
 } fs_kernel_id;
 fs_status fs_profile_enable(int32_t on);
 fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);

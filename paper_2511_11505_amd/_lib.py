@@ -18,7 +18,8 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH = 0, 1, 2
 FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK = range(4)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
- FS_K_COMBINE, FS_K_COUNT) = range(8)
+ FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
+ FS_K_COUNT) = range(12)
 FS_ABI_VERSION = 1
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t

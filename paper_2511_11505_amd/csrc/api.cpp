@@ -355,7 +355,7 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
   NEED(ws, "ws");
   FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, in_rows, group_rows,
                                 group_offsets, max_rows, w_gate_up, w_down, out_rows, ws,
-                                S(stream), true),
+                                S(stream), FS_K_GATE_UP),
          "grouped_ffn");
   return FS_OK;
 }
@@ -411,7 +411,9 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
   NEED(a, "a");
   NEED(w, "w");
   NEED(out, "out");
+  fs::prof_begin(FS_K_DENSE, S(stream));
   FS_HIP(fs::launch_dense_linear(dtype, m, n, kdim, a, w, out, S(stream)), "dense_linear");
+  fs::prof_end(FS_K_DENSE, S(stream));
   return FS_OK;
 }
 
@@ -532,8 +534,10 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     if (sm) {
       FS_HIP(hipEventRecord(sync->packed, sc), "hipEventRecord");
       FS_HIP(hipStreamWaitEvent(sm, sync->packed, 0), "hipStreamWaitEvent");
+      fs::prof_begin(FS_K_DISPATCH_COPY, sm);
       FS_HIP(hipMemcpyAsync(recv_slot, b->send, (size_t)cap * D * es, hipMemcpyDeviceToDevice, sm),
              "hipMemcpyAsync");
+      fs::prof_end(FS_K_DISPATCH_COPY, sm);
       FS_HIP(hipEventRecord(sync->dispatched, sm), "hipEventRecord");
       sync->have_dispatch = true;
     } else if (R > 1) {
@@ -544,7 +548,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     if (desc->n_shared > 0) {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, 1, desc->n_shared * desc->ffn_shared, D,
                                     residual_in, nullptr, nullptr, N, wt->ws_gate_up, wt->ws_down,
-                                    b->shared_out, ws_shared, sc, false),
+                                    b->shared_out, ws_shared, sc, FS_K_SHARED_GATE_UP),
              "shared_ffn");
     }
     FS_HIP(fs::launch_residual(desc->dtype, partial_out, residual_in,
@@ -573,7 +577,8 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
     }
     FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, goff,
-                                  max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc, true),
+                                  max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,
+                                  FS_K_GATE_UP),
            "grouped_ffn");
     const char* y_ret = reinterpret_cast<const char*>(b->y) + (size_t)r * cap * D * es;
     fs::prof_begin(FS_K_COMBINE, sc);

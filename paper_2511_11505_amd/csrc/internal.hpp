@@ -40,7 +40,7 @@ size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn);
 hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const void* in,
                               const int32_t* rows, const int32_t* goff, int64_t max_rows,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
-                              hipStream_t s, bool profile);
+                              hipStream_t s, int prof_gate_up);  // profile id of gate/up, down = +1; -1: none
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s);
 

@@ -13,6 +13,17 @@ are also reported scaled by the reading of the plain device copy kernel
 (__amd_rocclr_copyBuffer) of --copy-bytes bytes, which moves that many bytes
 each way; the copy dispatches taken are those reading the most.
 
+With --overlap, it instead reports, for every copy dispatched on the stream
+that carries the largest copies (the Dispatch stand-in), the fraction of the
+copy's interval during which a kernel of another stream runs:
+|copy ∩ (∪ compute kernels)| / |copy|.
+
+With --mfma PMC_DIR (a `rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES
+SQ_INSTS_VALU_MFMA_MOPS_BF16` run), it reports per kernel the fraction of
+cycles the MFMA units were busy, SQ_VALU_MFMA_BUSY_CYCLES summed over the
+1024 SIMDs / (GRBM_GUI_ACTIVE summed over the 8 XCDs * 128), and the clock
+the kernel ran at, GRBM_GUI_ACTIVE / 8 / its duration in the trace.
+
 With --traffic-json, the calibrated HBM bytes per launch (FETCH + WRITE) of
 the one kernel whose short name contains --kernel are written to OUT, with
 the sha256 of the kernel's source file, so that a reader of OUT can tell
@@ -51,6 +62,56 @@ def trace_table(trace_dir):
     return agg
 
 
+def overlap_report(trace_dir, min_us, skip):
+    rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
+    span = lambda r: (int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+    copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+    longest = max(span(r)[1] - span(r)[0] for r in copies)
+    streams = {r["Stream_Id"] for r in copies if span(r)[1] - span(r)[0] >= 0.5 * longest}
+    if len(streams) != 1:
+        raise SystemExit(f"the largest copies run on several streams: {sorted(streams)}")
+    cs = streams.pop()
+    copies = [span(r) for r in copies if r["Stream_Id"] == cs and span(r)[1] - span(r)[0] >= 1e3 * min_us]
+    copies = sorted(copies)[skip:]
+    compute = sorted(span(r) for r in rows if r["Stream_Id"] != cs)
+    # union of the compute intervals
+    merged = []
+    for a, b in compute:
+        if merged and a <= merged[-1][1]:
+            merged[-1][1] = max(merged[-1][1], b)
+        else:
+            merged.append([a, b])
+    fr, dur = [], []
+    for a, b in copies:
+        cov = sum(max(0, min(b, y) - max(a, x)) for x, y in merged if y > a and x < b)
+        fr.append(cov / (b - a))
+        dur.append((b - a) / 1e3)
+    n = len(fr)
+    print(f"copy stream {cs}: {n} copies of at least {min_us} us after the first {skip}")
+    print()
+    print("| copies | mean copy us | mean overlap | min overlap | max overlap | mean exposed us |")
+    print("|---|---|---|---|---|---|")
+    exposed = [d * (1 - f) for d, f in zip(dur, fr)]
+    print(f"| {n} | {sum(dur) / n:.1f} | {100 * sum(fr) / n:.1f}% | {100 * min(fr):.1f}% | "
+          f"{100 * max(fr):.1f}% | {sum(exposed) / n:.1f} |")
+
+
+def mfma_report(trace_dir, pmc_dir, min_us):
+    agg = trace_table(trace_dir)
+    cnt = {c: counter_table(pmc_dir, c) for c in ("GRBM_GUI_ACTIVE", "SQ_VALU_MFMA_BUSY_CYCLES")}
+    print("| kernel | grid | avg us (trace) | MFMA busy | clock GHz |")
+    print("|---|---|---|---|---|")
+    for key, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        avg = sum(v) / len(v)
+        grbm, busy = cnt["GRBM_GUI_ACTIVE"].get(key), cnt["SQ_VALU_MFMA_BUSY_CYCLES"].get(key)
+        if avg < min_us or not grbm or not busy:
+            continue
+        g, b = sum(grbm) / len(grbm), sum(busy) / len(busy)
+        if b == 0:
+            continue
+        print(f"| {key[0]} | {key[1]} | {avg:.2f} | {100 * b / (g * 128):.1f}% | {g / 8 / avg / 1e3:.2f} |")
+
+
 def counter_table(pmc_dir, counter):
     rows = list(csv.DictReader(open(one(os.path.join(pmc_dir, "*_counter_collection.csv")))))
     agg = collections.defaultdict(list)
@@ -67,6 +128,9 @@ def main():
     ap.add_argument("--write")
     ap.add_argument("--copy-bytes", type=float, default=None)
     ap.add_argument("--min-us", type=float, default=1.0)
+    ap.add_argument("--overlap", action="store_true")
+    ap.add_argument("--skip", type=int, default=0, help="--overlap: leading copies to skip (warm-up)")
+    ap.add_argument("--mfma")
     ap.add_argument("--traffic-json")
     ap.add_argument("--kernel")
     ap.add_argument("--workload")
@@ -75,6 +139,12 @@ def main():
     ap.add_argument("--command", action="append", default=[])
     a = ap.parse_args()
     scales, kib = {}, {}
+    if a.overlap:
+        overlap_report(a.trace_dir, a.min_us, a.skip)
+        return
+    if a.mfma:
+        mfma_report(a.trace_dir, a.mfma, a.min_us)
+        return
     agg = trace_table(a.trace_dir)
     print("| kernel | grid (threads) | launches | avg us | min us | max us |")
     print("|---|---|---|---|---|---|")

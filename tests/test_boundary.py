@@ -31,6 +31,18 @@ def test_library_loads_and_exports_every_declared_symbol():
     assert L.fs_abi_version() == L.FS_ABI_VERSION
 
 
+def test_binding_constants_match_the_header():
+    """Every enumerator the header defines has the same value in the binding."""
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    enums = re.findall(r"\b(FS_[A-Z0-9_]+)\s*=\s*(\d+)\s*[,}\n]", src)
+    assert len(enums) >= 20
+    for name, value in enums:
+        assert getattr(L, name) == int(value), name
+    assert L.fs_profile_read(L.FS_K_COUNT - 1) == (0.0, 0)
+    with pytest.raises(L.FsError):
+        L.fs_profile_read(L.FS_K_COUNT)
+
+
 def test_status_strings():
     lib = L.load()
     assert lib.fs_status_string(0) == b"FS_OK"

@@ -1,0 +1,72 @@
+"""Host logic of rocprof_summary.py on small synthetic rocprofv3 CSV files:
+the overlap fraction of the copy stream, and the calibrated traffic record."""
+
+import csv
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TOOL = os.path.join(ROOT, "rocprof_summary.py")
+
+TRACE_FIELDS = ["Kind", "Stream_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"]
+
+
+def write_trace(path, rows):
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "x_kernel_trace.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=TRACE_FIELDS)
+        w.writeheader()
+        for stream, name, a, b, grid in rows:
+            w.writerow({"Kind": "KERNEL_DISPATCH", "Stream_Id": stream, "Kernel_Name": name,
+                        "Start_Timestamp": a, "End_Timestamp": b, "Grid_Size_X": grid})
+
+
+def run(*args):
+    return subprocess.run([sys.executable, TOOL, *args], capture_output=True, text=True, check=True).stdout
+
+
+def test_overlap_fraction(tmp_path):
+    # copy 1 on stream 1: [0, 100 us], compute covers [20, 50] and [40, 90] -> 70%
+    # copy 2: [200, 300 us], compute [150, 400] -> 100%
+    us = 1000
+    write_trace(str(tmp_path), [
+        (1, "__amd_rocclr_copyBuffer", 0, 100 * us, 4096),
+        (0, "void fs::gemm<0>(int)", 20 * us, 50 * us, 65536),
+        (0, "void fs::gemm<1>(int)", 40 * us, 90 * us, 65536),
+        (1, "__amd_rocclr_copyBuffer", 200 * us, 300 * us, 4096),
+        (0, "void fs::combine(int)", 150 * us, 400 * us, 4096),
+        (0, "__amd_rocclr_copyBuffer", 500 * us, 502 * us, 512),   # small setup copy elsewhere
+    ])
+    out = run(str(tmp_path), "--overlap", "--min-us", "10")
+    assert "copy stream 1: 2 copies" in out
+    assert "| 2 | 100.0 | 85.0% | 70.0% | 100.0% | 15.0 |" in out
+    out = run(str(tmp_path), "--overlap", "--min-us", "10", "--skip", "1")
+    assert "| 1 | 100.0 | 100.0% | 100.0% | 100.0% | 0.0 |" in out
+
+
+def test_traffic_record(tmp_path):
+    trace, fetch, write = (str(tmp_path / n) for n in ("trace", "fetch", "write"))
+    write_trace(trace, [(0, "void fs::(anonymous namespace)::gemm_x<0, 128>(int)", 0, 10, 65536)])
+    for d, counter, gemm_kib, copy_kib in ((fetch, "FETCH_SIZE", 1000, 512), (write, "WRITE_SIZE", 300, 1024)):
+        os.makedirs(d)
+        with open(os.path.join(d, "x_counter_collection.csv"), "w", newline="") as f:
+            w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"])
+            w.writeheader()
+            w.writerow({"Kernel_Name": "void fs::(anonymous namespace)::gemm_x<0, 128>(int)",
+                        "Grid_Size": 65536, "Counter_Name": counter, "Counter_Value": gemm_kib})
+            w.writerow({"Kernel_Name": "__amd_rocclr_copyBuffer", "Grid_Size": 4096,
+                        "Counter_Name": counter, "Counter_Value": copy_kib})
+    src = tmp_path / "src.hip"
+    src.write_text("kernel source\n")
+    out_json = str(tmp_path / "rec.json")
+    run(trace, "--fetch", fetch, "--write", write, "--copy-bytes", str(1024 * 1024),
+        "--traffic-json", out_json, "--kernel", "gemm_x<0, 128>", "--workload", "w",
+        "--source", str(src), "--command", "cmd")
+    rec = json.load(open(out_json))
+    # the 1 MiB copy reads 512 KiB of FETCH (scale 2) and 1024 KiB of WRITE (scale 1)
+    assert rec["fetch_scale"] == 2.0 and rec["write_scale"] == 1.0
+    assert rec["hbm_bytes_per_launch"] == (1000 * 2 + 300) * 1024
+    assert rec["commands"] == ["cmd"] and rec["workload"] == "w"
+    assert len(rec["source_sha256"]) == 64
