@@ -193,13 +193,13 @@ fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_row
     case FS_OP_DISPATCH_PACK: *bytes = plan_bytes(desc); return FS_OK;
     case FS_OP_GROUPED_FFN:
       if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
-      *bytes = fs::ffn_ws_bytes(desc->dtype, max_rows, ffn);
+      *bytes = fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden);
       return FS_OK;
     case FS_OP_BLOCK: {
       size_t b = router_bytes(desc) + plan_bytes(desc);
-      b += fs::ffn_ws_bytes(desc->dtype, max_rows, desc->ffn);
+      b += fs::ffn_ws_bytes(desc->dtype, max_rows, desc->ffn, desc->hidden);
       if (desc->n_shared > 0)
-        b += fs::ffn_ws_bytes(desc->dtype, desc->n_tokens, desc->n_shared * desc->ffn_shared);
+        b += fs::ffn_ws_bytes(desc->dtype, desc->n_tokens, desc->n_shared * desc->ffn_shared, desc->hidden);
       *bytes = b;
       return FS_OK;
     }
@@ -350,7 +350,7 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
   NEED(w_gate_up, "w_gate_up");
   NEED(w_down, "w_down");
   NEED(out_rows, "out_rows");
-  if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn))
+  if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden))
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
   NEED(ws, "ws");
   FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, in_rows, group_rows,
@@ -514,9 +514,9 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   Carve c{reinterpret_cast<char*>(ws)};
   void* ws_router = c.take(router_bytes(desc));
   void* ws_plan = c.take(plan_bytes(desc));
-  void* ws_ffn = c.take(fs::ffn_ws_bytes(desc->dtype, max_recv_rows, desc->ffn));
+  void* ws_ffn = c.take(fs::ffn_ws_bytes(desc->dtype, max_recv_rows, desc->ffn, D));
   void* ws_shared = desc->n_shared > 0
-                        ? c.take(fs::ffn_ws_bytes(desc->dtype, N, desc->n_shared * desc->ffn_shared))
+                        ? c.take(fs::ffn_ws_bytes(desc->dtype, N, desc->n_shared * desc->ffn_shared, D))
                         : nullptr;
   int32_t* my_counts = b->src_counts + (size_t)r * E;
   int32_t* my_offsets = b->src_offsets + (size_t)r * (E + 1);

@@ -1047,6 +1047,168 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_rs_kernel(
   }
 }
 
+// ---------------------------------------------------------------- bf16 MFMA, weight streaming
+// For groups of few rows (decode), where the GEMM reads each weight once and
+// is bound by HBM: one wave per workgroup owns 64 weight rows of one group
+// (gate/up: 32 gate rows and the matching 32 up rows; down: 64 output
+// columns) over one slice of K, for 16 * MF activation rows at a time.
+// Operand fragments go straight from global memory into the registers of
+// v_mfma_f32_16x16x32_bf16 (lane l holds row l % 16, K elements
+// 8 * (l / 16) .. + 7 of a 32-wide step), so one load instruction reads 16
+// rows x 64 contiguous bytes: whole 64-byte L2 requests, nothing re-read.
+// The next 64-wide K block is always in flight.  Many small workgroups keep
+// many loads in flight per CU.  With one K slice the SwiGLU / scatter
+// epilogue runs here; with several, each slice stores fp32 partials
+// P[slice][row][col] and stream_reduce_kernel sums them in slice order.
+constexpr int kStreamWrows = 64;       // weight rows per workgroup
+constexpr int kStreamMaxRows = 4096;   // larger batches use the LDS-ring kernels
+constexpr int kStreamWgs = 2048;       // workgroups aimed for
+constexpr size_t kStreamPartialCap = size_t(64) << 20;
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+template <int MODE, int MF>
+__global__ __launch_bounds__(64, 2) void gemm_bf16_stream_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
+    int NOUT, bf16_t* __restrict__ C, int ldc, float* __restrict__ P, int splits, int kb_per_split) {
+  constexpr int NCOL = MODE == MODE_GATEUP ? kStreamWrows / 2 : kStreamWrows;
+  constexpr int NF = kStreamWrows / 16;   // 16-row weight fragments
+  constexpr int BMR = 16 * MF;            // activation rows per pass
+  const int lane = threadIdx.x;
+  const int n_tiles = NOUT / NCOL;
+  int64_t w = blockIdx.x;
+  const int sp = (int)(w % splits);
+  w /= splits;
+  const int nt = (int)(w % n_tiles);
+  const int g = (int)(w / n_tiles);
+  if (g >= G) return;
+  auto clampo = [&](int v) { return v < 0 ? 0 : (v > (int)m_total ? (int)m_total : v); };
+  const int row_base = clampo(goff ? goff[g] : 0);
+  const int rows_g = clampo(goff ? goff[g + 1] : (int)m_total) - row_base;
+  const int KT = K / 64;
+  const int kb0 = sp * kb_per_split;
+  const int kb1 = min(KT, kb0 + kb_per_split);
+  if (rows_g <= 0 || kb0 >= kb1) return;
+
+  const size_t bstride = (size_t)(MODE == MODE_GATEUP ? 2 * NOUT : NOUT) * K;
+  const bf16_t* Bg = B + (size_t)g * bstride;
+  const int q = lane >> 4, l16 = lane & 15;
+  // weight fragment f: gate/up f < 2 are gate rows, f >= 2 the matching up rows
+  const bf16_t* pb[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int wrow = MODE == MODE_GATEUP ? (f / 2) * NOUT + nt * NCOL + (f % 2) * 16 + l16
+                                         : nt * NCOL + f * 16 + l16;
+    pb[f] = Bg + (size_t)wrow * K + 8 * q;
+  }
+  for (int m0 = 0; m0 < rows_g; m0 += BMR) {
+    const bf16_t* pa[MF];
+#pragma unroll
+    for (int i = 0; i < MF; ++i) {
+      int m = m0 + i * 16 + l16;
+      if (m >= rows_g) m = rows_g - 1;   // padding rows read a valid row, never stored
+      const int grow = row_base + m;
+      const int64_t src = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      pa[i] = A + src * K + 8 * q;
+    }
+    floatx4 acc[MF][NF];
+#pragma unroll
+    for (int i = 0; i < MF; ++i)
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[i][f][v] = 0.f;
+    bf16x8 fa0[MF][2], fb0[NF][2], fa1[MF][2], fb1[NF][2];
+    auto load = [&](bf16x8 (&fa)[MF][2], bf16x8 (&fb)[NF][2], int kb) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+          fb[f][s2] = *reinterpret_cast<const bf16x8*>(pb[f] + (size_t)kb * 64 + s2 * 32);
+#pragma unroll
+        for (int i = 0; i < MF; ++i)
+          fa[i][s2] = *reinterpret_cast<const bf16x8*>(pa[i] + (size_t)kb * 64 + s2 * 32);
+      }
+    };
+    auto mma = [&](bf16x8 (&fa)[MF][2], bf16x8 (&fb)[NF][2]) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int i = 0; i < MF; ++i)
+#pragma unroll
+          for (int f = 0; f < NF; ++f)
+            acc[i][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i][s2], fb[f][s2], acc[i][f], 0, 0, 0);
+    };
+    load(fa0, fb0, kb0);
+    int kb = kb0;
+    for (; kb + 2 <= kb1; kb += 2) {
+      load(fa1, fb1, kb + 1);
+      mma(fa0, fb0);
+      if (kb + 2 < kb1) load(fa0, fb0, kb + 2);
+      mma(fa1, fb1);
+    }
+    if (kb < kb1) mma(fa0, fb0);
+
+    // element v of lane l: row 4 * (l / 16) + v, column l % 16 of its 16 x 16 tile
+#pragma unroll
+    for (int i = 0; i < MF; ++i) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + i * 16 + 4 * q + v;
+        if (m >= rows_g) continue;
+        const int grow = row_base + m;
+        if (splits > 1) {
+          float* pr = P + ((size_t)sp * m_total + grow) * (MODE == MODE_GATEUP ? 2 * NOUT : NOUT);
+#pragma unroll
+          for (int f = 0; f < NF; ++f) {
+            const int col = MODE == MODE_GATEUP ? (f / 2) * NOUT + nt * NCOL + (f % 2) * 16 + l16
+                                                : nt * NCOL + f * 16 + l16;
+            pr[col] = acc[i][f][v];
+          }
+        } else if (MODE == MODE_GATEUP) {
+#pragma unroll
+          for (int f = 0; f < 2; ++f)
+            C[(size_t)grow * ldc + nt * NCOL + f * 16 + l16] =
+                f2bf(swiglu_bf16_epi(acc[i][f][v], acc[i][f + 2][v]));
+        } else {
+          const int64_t orow = rows ? (int64_t)rows[grow] : (int64_t)grow;
+#pragma unroll
+          for (int f = 0; f < NF; ++f) C[orow * ldc + nt * NCOL + f * 16 + l16] = f2bf(acc[i][f][v]);
+        }
+      }
+    }
+  }
+}
+
+// Sum of the split-K partials in slice order, then the pass's epilogue:
+// gate/up H[r, c] = SiLU(sum gate) * (sum up); down out[row(r), c] = sum.
+// One thread per output element of the rows that exist (goff[G]).
+template <int MODE>
+__global__ __launch_bounds__(256) void stream_reduce_kernel(
+    const float* __restrict__ P, const int32_t* __restrict__ rows, const int32_t* __restrict__ goff,
+    int G, int64_t m_total, int NOUT, int splits, bf16_t* __restrict__ C, int ldc) {
+  int64_t m_rows = goff ? goff[G] : m_total;
+  m_rows = m_rows < 0 ? 0 : (m_rows > m_total ? m_total : m_rows);
+  const int W = MODE == MODE_GATEUP ? 2 * NOUT : NOUT;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < m_rows * NOUT;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t r = e / NOUT;
+    const int c = (int)(e % NOUT);
+    float a = 0.f, b = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      const float* pr = P + ((size_t)s * m_total + r) * W;
+      a += pr[c];
+      if (MODE == MODE_GATEUP) b += pr[NOUT + c];
+    }
+    if (MODE == MODE_GATEUP) {
+      C[r * ldc + c] = f2bf(swiglu_bf16_epi(a, b));
+    } else {
+      const int64_t orow = rows ? (int64_t)rows[r] : r;
+      C[orow * ldc + c] = f2bf(a);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- fp32 VALU
 // 64 x 64 tiles, 256 threads, 4 rows x 4 columns per thread.  For gate/up a
 // tile holds 32 gate and the matching 32 up columns; a thread owns 2 H
@@ -1262,9 +1424,54 @@ void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff,
 
 }  // namespace
 
-size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn) {
-  const size_t b = (size_t)max_rows * ffn * (dtype == 0 ? 4 : 2);
-  return (b + 255) / 256 * 256;
+// fp32 partials of the weight-streaming passes (shared by both passes): up
+// to 32 K slices of max_rows x max(2F, d), at most kStreamPartialCap.  It
+// grows with max_rows, so a workspace sized for a bound serves any smaller
+// bound.
+size_t stream_partial_bytes(int dtype, int64_t max_rows, int ffn, int d) {
+  if (dtype != 1) return 0;
+  const size_t want = (size_t)32 * max_rows * std::max(2 * ffn, d) * 4;
+  return std::min(want, kStreamPartialCap);
+}
+
+// K slices of one weight-streaming pass: enough workgroups (groups x 64-row
+// weight tiles x slices) to fill the chip, at least two K blocks per slice,
+// and partials that fit the buffer above.
+int stream_splits(int64_t max_rows, int G, int nw, int K, size_t partial_bytes) {
+  const int64_t tiles = (int64_t)G * (nw / kStreamWrows);
+  int64_t s = cdiv64(kStreamWgs, tiles);
+  const int64_t by_k = (K / 64) / 2;
+  if (s > by_k) s = by_k;
+  const int64_t by_mem = (int64_t)(partial_bytes / ((size_t)(max_rows > 0 ? max_rows : 1) * nw * 4));
+  if (s > by_mem) s = by_mem;
+  return s < 1 ? 1 : (int)s;
+}
+
+// FS_GEMM_STREAM=0 never takes the streaming kernel, =2 takes it whenever
+// the groups average at most 64 rows (tuning); unset or 1: the rule below.
+int stream_mode() {
+  static const int mode = [] {
+    const char* e = getenv("FS_GEMM_STREAM");
+    return e ? atoi(e) : 1;
+  }();
+  return mode;
+}
+
+// The streaming kernel takes a pass when its groups average at most 64 rows
+// and the LDS-ring kernel's 128 x 256 tiles would not give every CU one.
+bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
+  const int mode = stream_mode();
+  if (mode == 0 || dtype != 1 || max_rows > kStreamMaxRows || max_rows > (int64_t)64 * G ||
+      ffn % 64 != 0 || d % 64 != 0)
+    return false;
+  const int64_t ring_tiles =
+      (int64_t)G * std::max<int64_t>(1, cdiv64(max_rows, (int64_t)128 * G)) * std::max(1, ffn / 128);
+  return mode == 2 || ring_tiles < 256;
+}
+
+size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn, int d) {
+  const size_t h = (size_t)max_rows * ffn * (dtype == 0 ? 4 : 2);
+  return (h + 255) / 256 * 256 + (stream_partial_bytes(dtype, max_rows, ffn, d) + 255) / 256 * 256;
 }
 
 hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
@@ -1274,7 +1481,50 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
   const bool profile = prof_gate_up >= 0;
   const int pg = prof_gate_up, pd = prof_gate_up + 1;
   if (max_rows <= 0) return hipSuccess;
-  if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
+  if (use_stream(dtype, max_rows, G, ffn, d)) {
+    bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+    float* P = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                        ((size_t)max_rows * ffn * 2 + 255) / 256 * 256);
+    const size_t pbytes = stream_partial_bytes(dtype, max_rows, ffn, d);
+    // 64 activation rows per pass when the groups average more than 32
+    const bool wide = max_rows > (int64_t)32 * G;
+    // gate/up: 32 H columns per workgroup; down: 64 output columns
+    {
+      const int kt = d / 64, sp = stream_splits(max_rows, G, 2 * ffn, d, pbytes);
+      const int kps = (int)cdiv64(kt, sp), spe = (int)cdiv64(kt, kps);
+      if (profile) prof_begin(pg, s);
+      const unsigned grid = (unsigned)((int64_t)G * (ffn / 32) * spe);
+      if (wide)
+        gemm_bf16_stream_kernel<MODE_GATEUP, 4><<<grid, 64, 0, s>>>(
+            (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
+            P, spe, kps);
+      else
+        gemm_bf16_stream_kernel<MODE_GATEUP, 2><<<grid, 64, 0, s>>>(
+            (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
+            P, spe, kps);
+      if (spe > 1)
+        stream_reduce_kernel<MODE_GATEUP><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * ffn, 256), 8192),
+                                            256, 0, s>>>(P, rows, goff, G, max_rows, ffn, spe, H, ffn);
+      if (profile) prof_end(pg, s);
+    }
+    {
+      const int kt = ffn / 64, sp = stream_splits(max_rows, G, d, ffn, pbytes);
+      const int kps = (int)cdiv64(kt, sp), spe = (int)cdiv64(kt, kps);
+      if (profile) prof_begin(pd, s);
+      const unsigned grid = (unsigned)((int64_t)G * (d / 64) * spe);
+      if (wide)
+        gemm_bf16_stream_kernel<MODE_DOWN, 4><<<grid, 64, 0, s>>>(
+            H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+      else
+        gemm_bf16_stream_kernel<MODE_DOWN, 2><<<grid, 64, 0, s>>>(
+            H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+      if (spe > 1)
+        stream_reduce_kernel<MODE_DOWN><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * d, 256), 8192),
+                                          256, 0, s>>>(P, rows, goff, G, max_rows, d, spe,
+                                                       (bf16_t*)out, d);
+      if (profile) prof_end(pd, s);
+    }
+  } else if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     if (profile) prof_begin(pg, s);
     gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d), (const bf16_t*)in, rows, goff, G,

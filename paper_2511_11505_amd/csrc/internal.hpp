@@ -36,7 +36,7 @@ hipError_t launch_receive_rows(const int32_t* src_counts, const int32_t* src_off
                                int32_t* group_offsets, hipStream_t s);
 
 // ---- grouped SwiGLU FFN and dense linear (gemm.hip)
-size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn);
+size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn, int d);
 hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const void* in,
                               const int32_t* rows, const int32_t* goff, int64_t max_rows,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
