@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 1
+#define FS_ABI_VERSION 2
 
 typedef enum {
   FS_OK = 0,
@@ -70,7 +70,15 @@ typedef enum {
 
 typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
 typedef enum { FS_SOFTMAX = 0, FS_SIGMOID = 1 } fs_score;
-typedef enum { FS_PHASE_ALL = 0, FS_PHASE_BEGIN = 1, FS_PHASE_FINISH = 2 } fs_phase;
+typedef enum {
+  FS_PHASE_ALL = 0,      /* GATE, SHARED, EXPERTS, COMBINE */
+  FS_PHASE_BEGIN = 1,    /* GATE, SHARED */
+  FS_PHASE_FINISH = 2,   /* EXPERTS, COMBINE */
+  FS_PHASE_GATE = 3,     /* router + top-k, plan + pack, Dispatch started */
+  FS_PHASE_SHARED = 4,   /* shared experts, partial_out */
+  FS_PHASE_EXPERTS = 5,  /* Dispatch joined, routed experts, Combine started */
+  FS_PHASE_COMBINE = 6   /* Combine joined, weighted sum + deferred add */
+} fs_phase;
 typedef enum {
   FS_OP_ROUTER_TOPK = 0,
   FS_OP_DISPATCH_PACK = 1,
@@ -246,6 +254,9 @@ typedef struct {
                              slot r is this rank's Combine return y_ret, whose
                              rows for other ranks' experts the caller fills */
   void* shared_out;       /* [N, d] (S > 0) */
+  void* ret;              /* [N*k, d] or NULL: the Combine stand-in copies y's
+                             slot r here and the weighted sum reads it; NULL:
+                             no copy, the sum reads slot r of y */
 } fs_block_buffers;
 
 /* Events that order the two streams of one block. */
@@ -254,26 +265,39 @@ fs_status fs_block_sync_create(fs_block_sync** out);
 fs_status fs_block_sync_destroy(fs_block_sync* sync);
 
 /* One FarSkip MoE block forward (Section 3 connectivity, Section 4.1
- * schedule), split in two phases around the far-skipped next computation.
- *   FS_PHASE_BEGIN on `compute`: router + top-k, plan + pack; then the
+ * schedule), in phases that let the caller place other work between them.
+ *   FS_PHASE_GATE on `compute`: router + top-k, plan + pack; then the
  *     Dispatch stand-in: on `comm` (after an event), a device-to-device copy
- *     of the whole send buffer into receive slot r; then the shared experts
- *     on residual_in and partial_out = residual_in + shared_out (Eq. 8b:
- *     the next layer's input without the routed output).
- *   The caller then enqueues the next computation on `compute`, reading
- *     partial_out; it overlaps the copy.
- *   FS_PHASE_FINISH on `compute`: wait for the copy, receive rows (R > 1),
- *     grouped SwiGLU experts, Combine and the deferred add
+ *     of the whole send buffer into receive slot r.
+ *   FS_PHASE_SHARED on `compute`: the shared experts on residual_in and
+ *     partial_out = residual_in + shared_out (Eq. 8b: the next layer's input
+ *     without the routed output).
+ *   FS_PHASE_EXPERTS on `compute`: wait for the Dispatch copy, receive rows
+ *     (R > 1), grouped SwiGLU experts; then, if buffers->ret is given, the
+ *     Combine stand-in: on `comm` (after an event), a copy of y's slot r
+ *     (the rows this rank's tokens get back) into ret.
+ *   FS_PHASE_COMBINE on `compute`: wait for the Combine copy, then the
+ *     weighted sum over each token's k rows and the deferred add
  *     residual_io += routed (Eq. 7).
- *   FS_PHASE_ALL runs both with nothing in between.
- * With comm == NULL the copy runs on `compute` (R > 1) or is skipped and the
- * experts read `send` (R = 1).  residual_in [N, d] is o_{k-1}, the MoE input
- * (Eq. 8a); partial_out [N, d]; residual_io [N, d] is updated in place
- * (normally partial_out after the caller added its next-layer output).
- * max_recv_rows bounds the rows landing on local experts (N*k when R = 1).
- * sync may be NULL only with comm == NULL.  One sync object serves one block
- * at a time: FINISH of a block is enqueued before the next BEGIN that uses
- * the same object. */
+ *   FS_PHASE_BEGIN = GATE + SHARED, FS_PHASE_FINISH = EXPERTS + COMBINE,
+ *   FS_PHASE_ALL = all four.  Between BEGIN and FINISH the caller enqueues
+ *   the far-skipped next computation on `compute`, reading partial_out; it
+ *   overlaps the Dispatch copy.  In the two-window schedule of Section 4.1
+ *   the phases of consecutive layers interleave: GATE_k, attention,
+ *   EXPERTS_k, SHARED_k, the next layer's first attention part, COMBINE_k,
+ *   GATE_{k+1}, ...; the Combine copy of layer k then overlaps SHARED_k and
+ *   that attention part.
+ * With comm == NULL each copy runs on `compute` in order (blocking, as in
+ *   the regular schedule); the Dispatch copy is skipped when recv is NULL
+ *   (R = 1: the experts read `send`), the Combine copy when ret is NULL.
+ * residual_in [N, d] is o_{k-1}, the MoE input (Eq. 8a); partial_out [N, d];
+ * residual_io [N, d] is updated in place (normally partial_out after the
+ * caller added its next-layer output).  max_recv_rows bounds the rows
+ * landing on local experts (N*k when R = 1).  sync may be NULL only with
+ * comm == NULL.  Every phase of one block gets the same comm argument.  One
+ * sync object serves one block at a time: the phases of one block are
+ * enqueued in order (GATE before EXPERTS before COMBINE) before the next
+ * GATE that uses the same object. */
 fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                                const fs_moe_weights* weights, const void* residual_in,
                                void* partial_out, void* residual_io, fs_block_buffers* buffers,
@@ -290,8 +314,9 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
  * selected kernels.  fs_profile_read synchronises those events.
  * FS_K_GATE_UP / FS_K_DOWN time the routed experts' passes (and
  * fs_grouped_expert_ffn); FS_K_SHARED_* the shared experts' passes inside
- * fs_moe_block_forward; FS_K_DISPATCH_COPY the Dispatch stand-in copy on
- * the comm stream; FS_K_DENSE fs_dense_linear. */
+ * fs_moe_block_forward; FS_K_DISPATCH_COPY / FS_K_COMBINE_COPY the Dispatch
+ * and Combine stand-in copies on the stream they run on; FS_K_DENSE
+ * fs_dense_linear. */
 typedef enum {
   FS_K_ROUTER = 0,
   FS_K_TOPK = 1,
@@ -304,7 +329,8 @@ typedef enum {
   FS_K_SHARED_DOWN = 8,
   FS_K_DISPATCH_COPY = 9,
   FS_K_DENSE = 10,
-  FS_K_COUNT = 11
+  FS_K_COMBINE_COPY = 11,
+  FS_K_COUNT = 12
 } fs_kernel_id;
 fs_status fs_profile_enable(int32_t on);
 fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);

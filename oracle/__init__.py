@@ -28,6 +28,7 @@ from .moe import (  # noqa: F401
     logits_f64,
     logits_routing_f32,
     route,
+    route_given,
     dispatch_plan,
     pack,
     receive_rows,
@@ -41,4 +42,7 @@ from .moe import (  # noqa: F401
     regular_pair,
     residual_add,
     dense_linear,
+    attention_stand_in,
+    farskip_stack,
+    regular_stack,
 )

@@ -126,6 +126,23 @@ def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
     return ids.astype(np.int32), w, margin < tau, margin
 
 
+def route_given(z32, ids, score, norm_topk=False, routed_scale=1.0):
+    """Weights of a given selection (ids [N,k], slot order as given) from
+    fp32 logits: the softmax probability over all E or the sigmoid (no
+    bias), then the optional renormalisation and the scale, as route()
+    computes them for its own selection."""
+    z = np.asarray(z32, np.float64)
+    if score == "softmax":
+        ex = np.exp(z - z.max(axis=1, keepdims=True))
+        base = ex / ex.sum(axis=1, keepdims=True)
+    else:
+        base = 1.0 / (1.0 + np.exp(-z))
+    w = np.take_along_axis(base, np.asarray(ids, np.int64), axis=1)
+    if norm_topk:
+        w = w / w.sum(axis=1, keepdims=True)
+    return w * routed_scale
+
+
 # --------------------------------------------------------------------------
 # O7-O8: Dispatch plan and pack  (Section 2.1, Dispatch: permutation of A
 # followed by the all-to-all)
@@ -246,11 +263,14 @@ def dense_linear(a, w):
 # The whole block on rank r (packed formulation, O1-O13)
 # --------------------------------------------------------------------------
 def moe_block(cfg, x_all, w_router, bias, w_gate_up, w_down, sh_gate_up=None,
-              sh_down=None, y_remote=None):
+              sh_down=None, y_remote=None, ids_given=None):
     """Every step of the block on rank cfg.ep_rank, following the data flow
     router -> top-k -> plan -> pack -> all-to-all -> experts -> return ->
     combine.  For R > 1 the other ranks' routing and sends are computed here
-    too.  Returns a dict of every intermediate."""
+    too.  ids_given (optional, [N, k]) replaces this rank's own selection
+    (the weights still come from its logits): where rounding in an earlier
+    layer moved a near tie, a caller takes the selection the other side
+    made.  Returns a dict of every intermediate."""
     R, r, k, E = cfg.ep_size, cfg.ep_rank, cfg.top_k, cfg.n_experts
     E_loc, cap = cfg.n_local, cfg.cap
     src = []
@@ -259,6 +279,9 @@ def moe_block(cfg, x_all, w_router, bias, w_gate_up, w_down, sh_gate_up=None,
         z32 = logits_routing_f32(xs, w_router)
         ids, w, near, margin = route(z32, cfg.score, k, cfg.n_groups, cfg.topk_groups,
                                      cfg.norm_topk, cfg.routed_scale, bias)
+        if s == r and ids_given is not None:
+            ids = np.asarray(ids_given, np.int32)
+            w = route_given(z32, ids, cfg.score, cfg.norm_topk, cfg.routed_scale)
         plan = dispatch_plan(ids, E, R)
         send = pack(xs, plan["slot_to_row"], k)
         src.append(dict(z32=z32, ids=ids, w=w, near_tie=near, margin=margin, plan=plan, send=send))
@@ -327,3 +350,55 @@ def regular_pair(x, shared, routed, w_next):
     r1 = np.asarray(x, np.float64) + shared + routed
     nxt = dense_linear(r1, w_next)
     return r1 + nxt, r1, nxt
+
+
+# --------------------------------------------------------------------------
+# Stacked layers: the FarSkip connectivity of Section 3 (Eqs. 7-8) and the
+# regular one (Eq. 6), each layer an attention stand-in (a bias-free linear
+# for part (a), one for part (b), as Section 4.1 splits attention) and an
+# MoE block.  R = 1: every source token is this rank's.
+# --------------------------------------------------------------------------
+def _layer_moe(cfg, o, lw, ids_given=None):
+    """Shared and routed outputs of one layer's MoE block on input o, and
+    its routing (logits, ids, margin)."""
+    blk = moe_block(cfg, o[None], lw["w_router"], lw.get("bias"), lw["w_gate_up"], lw["w_down"],
+                    lw.get("sh_gate_up"), lw.get("sh_down"), ids_given=ids_given)
+    me = blk["me"]
+    return blk["shared"], blk["routed"], dict(z32=me["z32"], ids=me["ids"], margin=me["margin"])
+
+
+def attention_stand_in(p, lw):
+    """Part (a) then part (b) of the attention stand-in: (p Wa^T) Wb^T."""
+    return dense_linear(dense_linear(p, lw["w_a"]), lw["w_b"])
+
+
+def farskip_stack(cfg, x, layers, ids_given=None):
+    """L FarSkip layers.  Layer k's attention reads the partial output
+    p_{k-1} (everything but layer k-1's routed output, Eq. 8b); its shared
+    and routed experts read the outdated o_{k-1} (Eq. 8a);
+    p_k = o_{k-1} + attn_k + shared_k and o_k = p_k + routed_k (Eq. 7).
+    p_{-1} = o_{-1} = x.  ids_given[k] (optional) is layer k's selection
+    (see moe_block).  Returns the final o and the per-layer terms."""
+    o = p = np.asarray(x, np.float64)
+    terms = []
+    for k, lw in enumerate(layers):
+        attn = attention_stand_in(p, lw)
+        shared, routed, rt = _layer_moe(cfg, o, lw, None if ids_given is None else ids_given[k])
+        p = o + attn + shared
+        o = p + routed
+        terms.append(dict(attn=attn, shared=shared, routed=routed, p=p, o=o, **rt))
+    return o, terms
+
+
+def regular_stack(cfg, x, layers, ids_given=None):
+    """L regular layers (Eq. 6): o'_k = o_{k-1} + attn(o_{k-1}), then
+    o_k = o'_k + shared(o'_k) + routed(o'_k)."""
+    o = np.asarray(x, np.float64)
+    terms = []
+    for k, lw in enumerate(layers):
+        attn = attention_stand_in(o, lw)
+        o1 = o + attn
+        shared, routed, rt = _layer_moe(cfg, o1, lw, None if ids_given is None else ids_given[k])
+        o = o1 + shared + routed
+        terms.append(dict(attn=attn, shared=shared, routed=routed, o=o, **rt))
+    return o, terms

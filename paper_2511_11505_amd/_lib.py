@@ -15,12 +15,13 @@ LIB_PATH = os.path.join(HERE, "libfarskip.so")
 FS_OK, FS_ERR_INVALID, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE, FS_ERR_HIP = range(5)
 FS_F32, FS_BF16 = 0, 1
 FS_SOFTMAX, FS_SIGMOID = 0, 1
-FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH = 0, 1, 2
+(FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH, FS_PHASE_GATE, FS_PHASE_SHARED, FS_PHASE_EXPERTS,
+ FS_PHASE_COMBINE) = range(7)
 FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK = range(4)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
- FS_K_COUNT) = range(12)
-FS_ABI_VERSION = 1
+ FS_K_COMBINE_COPY, FS_K_COUNT) = range(13)
+FS_ABI_VERSION = 2
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -47,7 +48,7 @@ class fs_moe_weights(ctypes.Structure):
 class fs_block_buffers(ctypes.Structure):
     _fields_ = [(n, _vp) for n in ("logits", "topk_ids", "topk_w", "src_counts", "src_offsets",
                                    "rank_offsets", "slot_to_row", "row_to_slot", "send", "recv",
-                                   "group_rows", "group_offsets", "y", "shared_out")]
+                                   "group_rows", "group_offsets", "y", "shared_out", "ret")]
 
 
 _SIGS = {

@@ -21,7 +21,7 @@ def _dt(cfg):
 
 class MoEBlock:
     def __init__(self, cfg, w_router, sel_bias, w_gate_up, w_down, ws_gate_up=None, ws_down=None,
-                 max_recv_rows=None, device="cuda", with_comm=True):
+                 max_recv_rows=None, device="cuda", with_comm=True, with_return=False):
         self.cfg = cfg
         self.desc = make_desc(cfg)
         R, N, d, E, k = cfg.ep_size, cfg.n_tokens, cfg.hidden, cfg.n_experts, cfg.top_k
@@ -46,6 +46,7 @@ class MoEBlock:
             group_offsets=torch.empty((E // R + 1,), dtype=i32, device=dev) if R > 1 else None,
             y=torch.empty((R * cap, d), dtype=dt, device=dev),
             shared_out=torch.empty((N, d), dtype=dt, device=dev) if cfg.n_shared > 0 else None,
+            ret=torch.empty((cap, d), dtype=dt, device=dev) if with_return else None,
         )
         self.weights_keep = (w_router, sel_bias, w_gate_up, w_down, ws_gate_up, ws_down)
         self.weights = L.fs_moe_weights(L.ptr(w_router), L.ptr(sel_bias), L.ptr(w_gate_up),
@@ -79,6 +80,11 @@ class MoEBlock:
                                residual_io, self.buffers, self.max_recv_rows, self.ws,
                                sync=self.sync if comm is not None else None,
                                compute=compute, comm=comm)
+
+    def phase(self, phase, residual_in, partial_out=None, residual_io=None, compute=None,
+              comm=None):
+        """One of the finer phases (FS_PHASE_GATE / SHARED / EXPERTS / COMBINE)."""
+        self.run(phase, residual_in, partial_out, residual_io, compute, comm)
 
     def begin(self, residual_in, partial_out, compute=None, comm=None):
         self.run(L.FS_PHASE_BEGIN, residual_in, partial_out, None, compute, comm)

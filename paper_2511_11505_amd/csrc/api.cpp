@@ -419,9 +419,12 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
 
 // ---- block sync
 struct fs_block_sync {
-  hipEvent_t packed = nullptr;
-  hipEvent_t dispatched = nullptr;
+  hipEvent_t packed = nullptr;      // send buffer ready (compute)
+  hipEvent_t dispatched = nullptr;  // Dispatch copy done (comm)
+  hipEvent_t computed = nullptr;    // expert outputs ready (compute)
+  hipEvent_t returned = nullptr;    // Combine copy done (comm)
   bool have_dispatch = false;
+  bool have_return = false;
 };
 
 fs_status fs_block_sync_create(fs_block_sync** out) {
@@ -430,9 +433,10 @@ fs_status fs_block_sync_create(fs_block_sync** out) {
   if (!s) return fail(FS_ERR_INVALID, "out of host memory");
   hipError_t e = hipEventCreateWithFlags(&s->packed, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&s->dispatched, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->computed, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->returned, hipEventDisableTiming);
   if (e != hipSuccess) {
-    if (s->packed) (void)hipEventDestroy(s->packed);
-    delete s;
+    (void)fs_block_sync_destroy(s);
     return hip_fail(e, "hipEventCreate");
   }
   *out = s;
@@ -443,6 +447,8 @@ fs_status fs_block_sync_destroy(fs_block_sync* s) {
   if (!s) return FS_OK;
   if (s->packed) (void)hipEventDestroy(s->packed);
   if (s->dispatched) (void)hipEventDestroy(s->dispatched);
+  if (s->computed) (void)hipEventDestroy(s->computed);
+  if (s->returned) (void)hipEventDestroy(s->returned);
   delete s;
   return FS_OK;
 }
@@ -455,8 +461,8 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                                fs_block_sync* sync, fs_stream compute, fs_stream comm) {
   fs_status st = check_desc(desc);
   if (st != FS_OK) return st;
-  if (phase != FS_PHASE_ALL && phase != FS_PHASE_BEGIN && phase != FS_PHASE_FINISH)
-    return fail(FS_ERR_INVALID, "phase must be FS_PHASE_ALL, BEGIN or FINISH");
+  if (phase < FS_PHASE_ALL || phase > FS_PHASE_COMBINE)
+    return fail(FS_ERR_INVALID, "phase must be one of FS_PHASE_ALL .. FS_PHASE_COMBINE");
   if (!wt) return fail(FS_ERR_INVALID, "weights must not be NULL");
   if (!b) return fail(FS_ERR_INVALID, "buffers must not be NULL");
   if (comm && !sync) return fail(FS_ERR_INVALID, "a comm stream needs a sync object");
@@ -468,7 +474,10 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     return fail(FS_ERR_INVALID, "max_recv_rows must be >= n_tokens * top_k when ep_size == 1");
   if (max_recv_rows > (int64_t)R * cap)
     return fail(FS_ERR_INVALID, "max_recv_rows must be <= ep_size * n_tokens * top_k");
-  const bool begin = phase != FS_PHASE_FINISH, finish = phase != FS_PHASE_BEGIN;
+  const bool do_gate = phase == FS_PHASE_ALL || phase == FS_PHASE_BEGIN || phase == FS_PHASE_GATE;
+  const bool do_shared = phase == FS_PHASE_ALL || phase == FS_PHASE_BEGIN || phase == FS_PHASE_SHARED;
+  const bool do_experts = phase == FS_PHASE_ALL || phase == FS_PHASE_FINISH || phase == FS_PHASE_EXPERTS;
+  const bool do_combine = phase == FS_PHASE_ALL || phase == FS_PHASE_FINISH || phase == FS_PHASE_COMBINE;
   size_t need = 0;
   st = fs_workspace_size(desc, FS_OP_BLOCK, max_recv_rows, 0, &need);
   if (st != FS_OK) return st;
@@ -476,31 +485,38 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   if (N == 0) return FS_OK;
   NEED(ws, "ws");
   NEED(residual_in, "residual_in");
-  if (begin) {
+  if (do_gate) {
     NEED(wt->w_router, "weights->w_router");
     OPT4(wt->sel_bias, "weights->sel_bias");
     if (wt->sel_bias && desc->score == FS_SOFTMAX)
       return fail(FS_ERR_UNSUPPORTED, "a selection bias is defined for sigmoid scoring only");
-    NEED(partial_out, "partial_out");
     NEED(b->send, "buffers->send");
     NEED4(b->row_to_slot, "buffers->row_to_slot");
+    OPT4(b->logits, "buffers->logits");
+  }
+  if (do_shared) {
+    NEED(partial_out, "partial_out");
     if (desc->n_shared > 0) {
       NEED(wt->ws_gate_up, "weights->ws_gate_up");
       NEED(wt->ws_down, "weights->ws_down");
       NEED(b->shared_out, "buffers->shared_out");
     }
-    OPT4(b->logits, "buffers->logits");
   }
-  if (finish) {
+  if (do_experts) {
     NEED(wt->w_gate_up, "weights->w_gate_up");
     NEED(wt->w_down, "weights->w_down");
-    NEED(residual_io, "residual_io");
     NEED(b->y, "buffers->y");
     if (R > 1) {
       NEED4(b->group_rows, "buffers->group_rows");
       NEED4(b->group_offsets, "buffers->group_offsets");
     }
+    if (!b->recv) NEED(b->send, "buffers->send");
   }
+  if (do_combine) {
+    NEED(residual_io, "residual_io");
+    if (!b->ret) NEED(b->y, "buffers->y");
+  }
+  OPT(b->ret, "buffers->ret");
   NEED4(b->topk_ids, "buffers->topk_ids");
   NEED4(b->topk_w, "buffers->topk_w");
   NEED4(b->src_counts, "buffers->src_counts");
@@ -511,6 +527,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
 
   hipStream_t sc = S(compute), sm = S(comm);
   const size_t es = elem(desc->dtype);
+  const size_t slot_bytes = (size_t)cap * D * es;
   Carve c{reinterpret_cast<char*>(ws)};
   void* ws_router = c.take(router_bytes(desc));
   void* ws_plan = c.take(plan_bytes(desc));
@@ -520,9 +537,10 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                         : nullptr;
   int32_t* my_counts = b->src_counts + (size_t)r * E;
   int32_t* my_offsets = b->src_offsets + (size_t)r * (E + 1);
-  char* recv_slot = b->recv ? reinterpret_cast<char*>(b->recv) + (size_t)r * cap * D * es : nullptr;
+  char* recv_slot = b->recv ? reinterpret_cast<char*>(b->recv) + (size_t)r * slot_bytes : nullptr;
+  char* y_slot = b->y ? reinterpret_cast<char*>(b->y) + (size_t)r * slot_bytes : nullptr;
 
-  if (begin) {
+  if (do_gate) {
     // gate: router + top-k (not overlappable, Eq. 9), then plan + pack
     st = router_impl(desc, residual_in, wt->w_router, wt->sel_bias, nullptr, b->logits,
                      b->topk_ids, b->topk_w, ws_router, sc);
@@ -530,20 +548,25 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     st = plan_pack_impl(desc, b->topk_ids, residual_in, my_counts, my_offsets, b->rank_offsets,
                         b->slot_to_row, b->row_to_slot, b->send, ws_plan, sc);
     if (st != FS_OK) return st;
-    // Dispatch stand-in: the whole send buffer leaves on the comm stream.
+    // Dispatch stand-in: the whole send buffer into receive slot r, on the
+    // comm stream, else in order on compute
     if (sm) {
       FS_HIP(hipEventRecord(sync->packed, sc), "hipEventRecord");
       FS_HIP(hipStreamWaitEvent(sm, sync->packed, 0), "hipStreamWaitEvent");
       fs::prof_begin(FS_K_DISPATCH_COPY, sm);
-      FS_HIP(hipMemcpyAsync(recv_slot, b->send, (size_t)cap * D * es, hipMemcpyDeviceToDevice, sm),
+      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, sm),
              "hipMemcpyAsync");
       fs::prof_end(FS_K_DISPATCH_COPY, sm);
       FS_HIP(hipEventRecord(sync->dispatched, sm), "hipEventRecord");
       sync->have_dispatch = true;
-    } else if (R > 1) {
-      FS_HIP(hipMemcpyAsync(recv_slot, b->send, (size_t)cap * D * es, hipMemcpyDeviceToDevice, sc),
+    } else if (recv_slot) {
+      fs::prof_begin(FS_K_DISPATCH_COPY, sc);
+      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, sc),
              "hipMemcpyAsync");
+      fs::prof_end(FS_K_DISPATCH_COPY, sc);
     }
+  }
+  if (do_shared) {
     // shared experts on o_{k-1}, then the next layer's partial input
     if (desc->n_shared > 0) {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, 1, desc->n_shared * desc->ffn_shared, D,
@@ -556,8 +579,8 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                                (int64_t)N * D, sc),
            "partial");
   }
-  if (finish) {
-    if (sm && sync && sync->have_dispatch) {
+  if (do_experts) {
+    if (sm && sync->have_dispatch) {
       FS_HIP(hipStreamWaitEvent(sc, sync->dispatched, 0), "hipStreamWaitEvent");
       sync->have_dispatch = false;
     }
@@ -572,7 +595,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       rows = b->group_rows;
       goff = b->group_offsets;
     } else {
-      in_rows = sm ? b->recv : b->send;
+      in_rows = recv_slot ? recv_slot : b->send;
       rows = nullptr;
       goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
     }
@@ -580,7 +603,32 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                                   max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,
                                   FS_K_GATE_UP),
            "grouped_ffn");
-    const char* y_ret = reinterpret_cast<const char*>(b->y) + (size_t)r * cap * D * es;
+    // Combine stand-in: slot r of y (the rows this rank's tokens get back)
+    // into ret, on the comm stream, else in order on compute
+    if (b->ret) {
+      if (sm) {
+        FS_HIP(hipEventRecord(sync->computed, sc), "hipEventRecord");
+        FS_HIP(hipStreamWaitEvent(sm, sync->computed, 0), "hipStreamWaitEvent");
+        fs::prof_begin(FS_K_COMBINE_COPY, sm);
+        FS_HIP(hipMemcpyAsync(b->ret, y_slot, slot_bytes, hipMemcpyDeviceToDevice, sm),
+               "hipMemcpyAsync");
+        fs::prof_end(FS_K_COMBINE_COPY, sm);
+        FS_HIP(hipEventRecord(sync->returned, sm), "hipEventRecord");
+        sync->have_return = true;
+      } else {
+        fs::prof_begin(FS_K_COMBINE_COPY, sc);
+        FS_HIP(hipMemcpyAsync(b->ret, y_slot, slot_bytes, hipMemcpyDeviceToDevice, sc),
+               "hipMemcpyAsync");
+        fs::prof_end(FS_K_COMBINE_COPY, sc);
+      }
+    }
+  }
+  if (do_combine) {
+    if (sm && sync->have_return) {
+      FS_HIP(hipStreamWaitEvent(sc, sync->returned, 0), "hipStreamWaitEvent");
+      sync->have_return = false;
+    }
+    const void* y_ret = b->ret ? b->ret : y_slot;
     fs::prof_begin(FS_K_COMBINE, sc);
     FS_HIP(fs::launch_combine(desc->dtype, y_ret, b->slot_to_row, b->topk_w, nullptr, nullptr,
                               residual_io, N, K, D, sc),

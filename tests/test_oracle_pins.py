@@ -373,3 +373,104 @@ def test_farskip_conservation_and_dropped_input():
         pending = rol
     o = o + pending
     assert np.allclose(o, total, rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------- stacked layers
+def _stack_layers(cfg, g, L, zero_down=False, zero_attention=False, shared=True):
+    d, F = cfg.hidden, cfg.ffn
+    layers = []
+    for _ in range(L):
+        _, wr, bias, gu, dn, _ = _tiny_inputs(cfg, g)
+        if zero_down:
+            dn[:] = 0
+        lw = dict(w_router=wr, bias=bias, w_gate_up=gu, w_down=dn,
+                  w_a=0.4 * g.standard_normal((d, d)), w_b=0.4 * g.standard_normal((d, d)))
+        if zero_attention:
+            lw["w_a"][:] = 0
+        if shared and cfg.n_shared:
+            lw["sh_gate_up"] = 0.3 * g.standard_normal((cfg.n_shared, 2 * cfg.ffn_shared, d))
+            lw["sh_down"] = 0.3 * g.standard_normal((cfg.n_shared, d, cfg.ffn_shared))
+        layers.append(lw)
+    return layers
+
+
+def test_stack_zero_moe_output_equals_regular():
+    # With zero MoE output (zero down projections, no shared experts) the
+    # FarSkip and the regular stacks are the same computation (Eq. 6 vs
+    # Eq. 7 with f = 0), bit for bit in fp64.
+    cfg = _tiny_cfg()
+    g = rng(20)
+    x = g.standard_normal((cfg.n_tokens, cfg.hidden))
+    layers = _stack_layers(cfg, g, 3, zero_down=True)
+    fs, _ = oracle.farskip_stack(cfg, x, layers)
+    rg, _ = oracle.regular_stack(cfg, x, layers)
+    assert np.array_equal(fs, rg)
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(n_shared=2, ffn_shared=3, score="sigmoid", norm_topk=True)])
+def test_stack_conservation(kw):
+    # Eq. 7 over L layers: the final residual minus the input is the sum of
+    # every layer's attention, shared and routed outputs, each once.
+    cfg = _tiny_cfg(**kw)
+    g = rng(21)
+    x = g.standard_normal((cfg.n_tokens, cfg.hidden))
+    layers = _stack_layers(cfg, g, 4)
+    o, terms = oracle.farskip_stack(cfg, x, layers)
+    total = sum(t["attn"] + t["shared"] + t["routed"] for t in terms)
+    assert np.allclose(o - x, total, rtol=1e-12, atol=1e-12)
+    assert any(t["routed"].any() for t in terms)
+
+
+def test_stack_one_layer_is_the_block():
+    # One layer with a zero attention stand-in is the MoE block on x:
+    # o = x + shared + routed, with both from the block computed directly.
+    cfg = _tiny_cfg(n_shared=1, ffn_shared=4)
+    g = rng(22)
+    x = g.standard_normal((cfg.n_tokens, cfg.hidden)).astype(np.float32)
+    layers = _stack_layers(cfg, g, 1, zero_attention=True)
+    lw = layers[0]
+    o, terms = oracle.farskip_stack(cfg, x, layers)
+    blk = oracle.moe_block(cfg, x[None], lw["w_router"], lw["bias"], lw["w_gate_up"], lw["w_down"],
+                           lw["sh_gate_up"], lw["sh_down"])
+    assert np.array_equal(o, (x.astype(np.float64) + 0 + blk["shared"]) + blk["routed"])
+    rg, _ = oracle.regular_stack(cfg, x, layers)
+    assert np.array_equal(o, rg)
+
+
+def test_stack_attention_does_not_see_the_previous_routed_output():
+    # The one dependency FarSkip drops (Section 3): layer k's attention reads
+    # p_{k-1}, which lacks layer k-1's routed output.  Changing layer 0's
+    # experts leaves layer 1's attention unchanged in the FarSkip stack and
+    # changes it in the regular stack; layer 1's experts see it in both.
+    cfg = _tiny_cfg()
+    g = rng(23)
+    x = g.standard_normal((cfg.n_tokens, cfg.hidden))
+    layers = _stack_layers(cfg, g, 2)
+    other = [dict(lw) for lw in layers]
+    other[0]["w_down"] = 2.0 * layers[0]["w_down"]
+    _, t1 = oracle.farskip_stack(cfg, x, layers)
+    _, t2 = oracle.farskip_stack(cfg, x, other)
+    assert np.array_equal(t1[1]["attn"], t2[1]["attn"])
+    assert not np.allclose(t1[1]["routed"], t2[1]["routed"])
+    _, r1 = oracle.regular_stack(cfg, x, layers)
+    _, r2 = oracle.regular_stack(cfg, x, other)
+    assert not np.allclose(r1[1]["attn"], r2[1]["attn"])
+
+
+def test_route_given_matches_route_on_its_own_selection():
+    # The weights of a given selection are route()'s weights when the given
+    # selection is route()'s own, for every scoring mode.
+    g = rng(24)
+    z = g.standard_normal((9, 12)).astype(np.float32)
+    for score, norm in (("softmax", False), ("softmax", True), ("sigmoid", True), ("sigmoid", False)):
+        ids, w, _, _ = oracle.route(z, score, 3, norm_topk=norm, routed_scale=2.5)
+        assert np.allclose(oracle.route_given(z, ids, score, norm, 2.5), w, rtol=1e-15, atol=0)
+    # and a given selection changes the block output only through the routing
+    cfg = _tiny_cfg()
+    x_all, wr, bias, gu, dn, _ = _tiny_inputs(cfg, rng(25))
+    own = oracle.moe_block(cfg, x_all, wr, bias, gu, dn)
+    same = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, ids_given=own["me"]["ids"])
+    assert np.array_equal(own["routed"], same["routed"])
+    flipped = own["me"]["ids"][:, ::-1].copy()   # same experts, other slot order
+    other = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, ids_given=flipped)
+    assert np.allclose(own["routed"], other["routed"], rtol=1e-12, atol=1e-12)

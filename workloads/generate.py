@@ -24,6 +24,7 @@ import torch
 # tensor tags
 TAG_X, TAG_ROUTER, TAG_BIAS, TAG_GATE_UP, TAG_DOWN = 0, 1, 2, 3, 4
 TAG_SH_GATE_UP, TAG_SH_DOWN, TAG_NEXT, TAG_Y_REMOTE = 5, 6, 7, 8
+TAG_ATT_A, TAG_ATT_B, TAG_LAYER = 9, 10, 11
 
 WEIGHT_STD = 0.02
 Y_REMOTE_STD = 1.8   # close to the rms of one expert's output at d=7168, F=2048
@@ -158,3 +159,23 @@ def synthetic_topk_ids(n_tokens, n_experts, top_k, seed, device="cpu", skew=0.0)
     w = w.expand(n_tokens, n_experts).contiguous()
     ids = torch.multinomial(w, top_k, replacement=False, generator=g)
     return ids.to(torch.int32)
+
+
+def layer_seed(seed, layer):
+    """Seed of layer `layer` of a stack built on a workload of seed `seed`."""
+    return int(np.random.SeedSequence([int(seed), TAG_LAYER, int(layer)]).generate_state(1, np.uint32)[0])
+
+
+def stack_layers(cfg, n_layers, device):
+    """Weights of n_layers stacked layers: each an MoE block drawn like a
+    workload of its own seed, plus two d x d attention stand-in linears
+    (part (a), part (b)) ~ N(0, 0.02^2).  Returns a list of
+    (layer config, Workload, w_a, w_b)."""
+    out = []
+    for k in range(n_layers):
+        lc = cfg.scaled(seed=layer_seed(cfg.seed, k))
+        wl = make_workload(lc, device)
+        w_a = normal((cfg.hidden, cfg.hidden), WEIGHT_STD, cfg.dtype, device, lc.seed, TAG_ATT_A)
+        w_b = normal((cfg.hidden, cfg.hidden), WEIGHT_STD, cfg.dtype, device, lc.seed, TAG_ATT_B)
+        out.append((lc, wl, w_a, w_b))
+    return out
