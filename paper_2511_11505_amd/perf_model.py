@@ -1,0 +1,179 @@
+"""Analytic performance model of FarSkip prefill (App. B, Tab. 5, Fig. 9).
+
+One MoE transformer layer of a DeepSeek-V3-like model serving a prefill
+batch on an 8-accelerator node, attention and shared experts tensor-parallel
+over the 8, routed experts expert-parallel over the 8 with perfect load
+balance, activations replicated (the inference variant of Section 4.2):
+after attention and after the MLP the activations are all-reduced.
+
+Component runtimes are FLOPs / rate (GEMMs and attention at their own
+rates) and message bytes / all-reduce bandwidth.  The exposed communication
+of each all-reduce follows Tab. 5, with max(0, .) where the table prints
+min(0, .) (an exposed time is never negative):
+  regular:  attention all-reduce attn.comm, MLP all-reduce mlp.comm, both
+            fully exposed;
+  FarSkip:  attention + shared all-reduce (one message)
+            max(0, as.comm - routed.runtime); routed all-reduce
+            max(0, routed.comm - attn.runtime).
+Sparsity s = routed experts / active routed experts; a model s/32 times
+sparser than DeepSeek-V3 (s = 32) has s/32 times the experts, each
+32/s times narrower, with the same 8 + 1 active experts: same parameters,
+fewer routed FLOPs.
+
+Pure arithmetic on the host; no GPU and no data.
+"""
+
+from dataclasses import dataclass, replace
+
+
+@dataclass(frozen=True)
+class Arch:
+    """DeepSeek-V3 dimensions (the attention is multi-head latent)."""
+    d: int = 7168
+    heads: int = 128
+    q_lora: int = 1536
+    kv_lora: int = 512
+    qk_nope: int = 128
+    qk_rope: int = 64
+    v_head: int = 128
+    experts: int = 256
+    active: int = 8
+    ffn: int = 2048
+    shared_ffn: int = 2048
+    n_shared: int = 1
+
+    def sparser(self, s):
+        """The same parameter count at sparsity s (s = experts / active)."""
+        ratio = s * self.active / self.experts
+        return replace(self, experts=int(round(self.experts * ratio)),
+                       ffn=int(round(self.ffn / ratio)))
+
+
+@dataclass(frozen=True)
+class Machine:
+    """Sustained rates: FLOP/s for GEMMs and for attention, all-reduce bus
+    bandwidth in bytes/s, node size.  The default is the hypothetical
+    accelerator of App. B."""
+    gemm_flops: float = 600e12
+    attn_flops: float = 500e12
+    allreduce_bw: float = 400e9
+    gpus: int = 8
+
+    def scaled(self, compute=1.0, attention=1.0, comm=1.0):
+        return replace(self, gemm_flops=self.gemm_flops * compute,
+                       attn_flops=self.attn_flops * compute * attention,
+                       allreduce_bw=self.allreduce_bw * comm)
+
+
+@dataclass(frozen=True)
+class Batch:
+    """Prefill batch: sequences x context, activations of `act_bytes`."""
+    seqs: int = 32
+    context: int = 2048
+    act_bytes: int = 2
+
+    @property
+    def tokens(self):
+        return self.seqs * self.context
+
+
+def gemm_flops(m, k, n):
+    return 2.0 * m * k * n
+
+
+def attention_flops(a, b):
+    """Whole-node FLOPs of one MLA attention layer on a causal prefill
+    batch: the projections plus QK^T and PV over the lower triangle."""
+    t = b.tokens
+    proj = (gemm_flops(t, a.d, a.q_lora)
+            + gemm_flops(t, a.q_lora, a.heads * (a.qk_nope + a.qk_rope))
+            + gemm_flops(t, a.d, a.kv_lora + a.qk_rope)
+            + gemm_flops(t, a.kv_lora, a.heads * (a.qk_nope + a.v_head))
+            + gemm_flops(t, a.heads * a.v_head, a.d))
+    pairs = b.seqs * b.context * (b.context + 1) / 2.0       # causal (query, key) pairs
+    core = 2.0 * pairs * a.heads * (a.qk_nope + a.qk_rope) + 2.0 * pairs * a.heads * a.v_head
+    return proj, core
+
+
+def swiglu_flops(tokens, d, f):
+    """Gate, up and down projections of one SwiGLU MLP."""
+    return gemm_flops(tokens, d, 2 * f) + gemm_flops(tokens, f, d)
+
+
+def allreduce_time(nbytes, m):
+    """Ring all-reduce of nbytes over m.gpus at bus bandwidth m.allreduce_bw
+    (bus bandwidth = algorithm bandwidth x 2 (n - 1) / n)."""
+    n = m.gpus
+    return nbytes * 2.0 * (n - 1) / n / m.allreduce_bw
+
+
+def layer_times(a, m, b):
+    """Per-accelerator runtimes of one layer's parts (seconds)."""
+    t = b.tokens
+    proj, core = attention_flops(a, b)
+    attn = proj / m.gpus / m.gemm_flops + core / m.gpus / m.attn_flops
+    shared = a.n_shared * swiglu_flops(t, a.d, a.shared_ffn) / m.gpus / m.gemm_flops
+    routed = a.active * swiglu_flops(t, a.d, a.ffn) / m.gpus / m.gemm_flops
+    gate = gemm_flops(t, a.d, a.experts) / m.gpus / m.gemm_flops
+    msg = allreduce_time(t * a.d * b.act_bytes, m)            # one [tokens, d] all-reduce
+    return dict(attn=attn, shared=shared, routed=routed, gate=gate, attn_comm=msg, mlp_comm=msg)
+
+
+def exposed(comm, overlapped_compute):
+    """Communication left exposed after overlapping it with a computation."""
+    return max(0.0, comm - overlapped_compute)
+
+
+def layer_runtime(parts, farskip):
+    """Layer time (seconds): compute plus exposed communication (Tab. 5)."""
+    compute = parts["attn"] + parts["shared"] + parts["routed"] + parts["gate"]
+    if farskip:
+        comm = (exposed(parts["attn_comm"], parts["routed"])     # attention + shared, one message
+                + exposed(parts["mlp_comm"], parts["attn"]))     # routed experts
+    else:
+        comm = parts["attn_comm"] + parts["mlp_comm"]
+    return compute + comm
+
+
+def speedup(a, m, b):
+    parts = layer_times(a, m, b)
+    return layer_runtime(parts, False) / layer_runtime(parts, True)
+
+
+SPARSITIES = (4, 8, 16, 32, 64, 128, 256, 512)
+
+SCENARIOS = {
+    "baseline": dict(),
+    "2x compute": dict(compute=2.0),
+    "2x attention": dict(attention=2.0),
+    "2x communication": dict(comm=2.0),
+    "2x compute + 2x communication": dict(compute=2.0, comm=2.0),
+}
+
+
+def sweep(machine=Machine(), batch=Batch(), arch=Arch(), sparsities=SPARSITIES):
+    """{scenario: [(sparsity, speedup)]} (Fig. 9 and its scenarios)."""
+    out = {}
+    for name, kw in SCENARIOS.items():
+        m = machine.scaled(**kw)
+        out[name] = [(s, speedup(arch.sparser(s), m, batch)) for s in sparsities]
+    return out
+
+
+def main():
+    import argparse
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gemm-tflops", type=float, default=600.0)
+    ap.add_argument("--attn-tflops", type=float, default=500.0)
+    ap.add_argument("--allreduce-gbs", type=float, default=400.0)
+    a = ap.parse_args()
+    m = Machine(a.gemm_tflops * 1e12, a.attn_tflops * 1e12, a.allreduce_gbs * 1e9)
+    res = sweep(m)
+    print("| scenario | " + " | ".join(f"{s}x" for s in SPARSITIES) + " |")
+    print("|---|" + "---|" * len(SPARSITIES))
+    for name, row in res.items():
+        print(f"| {name} | " + " | ".join(f"{v:.3f}" for _, v in row) + " |")
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,66 @@
+"""Pins of the analytic prefill model (App. B, Tab. 5, Fig. 9): closed-form
+FLOP and all-reduce counts, the exposure rules of Tab. 5, and the properties
+the paper states for its model."""
+
+import math
+
+import pytest
+
+from paper_2511_11505_amd import perf_model as pm
+
+
+def test_flop_counts():
+    assert pm.gemm_flops(3, 5, 7) == 210.0
+    assert pm.swiglu_flops(4, 8, 16) == 2 * 4 * 8 * 32 + 2 * 4 * 16 * 8
+    # causal attention: context 2 has 3 (query, key) pairs per sequence
+    a = pm.Arch(d=4, heads=1, q_lora=2, kv_lora=2, qk_nope=2, qk_rope=1, v_head=2)
+    _, core = pm.attention_flops(a, pm.Batch(seqs=5, context=2))
+    assert core == 2 * 15 * 1 * 3 + 2 * 15 * 1 * 2
+
+
+def test_allreduce_is_a_ring():
+    m = pm.Machine(allreduce_bw=100.0, gpus=8)
+    assert math.isclose(pm.allreduce_time(800.0, m), 800.0 * 2 * 7 / 8 / 100.0)
+
+
+def test_sparser_keeps_parameters_and_scales_routed_flops():
+    a = pm.Arch()
+    for s in pm.SPARSITIES:
+        b = a.sparser(s)
+        assert b.experts * b.ffn == a.experts * a.ffn
+        assert b.experts == s * b.active
+        assert math.isclose(pm.swiglu_flops(10, b.d, b.ffn), pm.swiglu_flops(10, a.d, a.ffn) * 32 / s)
+
+
+def test_exposure_rules_of_table_5():
+    parts = dict(attn=3.0, shared=1.0, routed=2.0, gate=0.5, attn_comm=2.5, mlp_comm=4.0)
+    # regular: every all-reduce exposed
+    assert pm.layer_runtime(parts, farskip=False) == 6.5 + 2.5 + 4.0
+    # FarSkip: attention + shared all-reduce under the routed experts (2.5 - 2.0),
+    # routed all-reduce under the next attention (4.0 - 3.0)
+    assert pm.layer_runtime(parts, farskip=True) == 6.5 + 0.5 + 1.0
+    # an exposed time is never negative (max(0, .))
+    small = dict(parts, attn_comm=0.1, mlp_comm=0.2)
+    assert pm.layer_runtime(small, farskip=True) == 6.5
+
+
+@pytest.mark.parametrize("s", pm.SPARSITIES)
+def test_farskip_never_slower_and_free_communication_gives_no_gain(s):
+    a = pm.Arch().sparser(s)
+    assert pm.speedup(a, pm.Machine(), pm.Batch()) >= 1.0
+    assert math.isclose(pm.speedup(a, pm.Machine(allreduce_bw=1e30), pm.Batch()), 1.0)
+
+
+def test_properties_stated_for_the_model():
+    res = pm.sweep()
+    base = dict(res["baseline"])
+    # doubling compute and communication speeds scales every time by 1/2:
+    # that scenario coincides with the baseline
+    for (s, v), (_, w) in zip(res["baseline"], res["2x compute + 2x communication"]):
+        assert math.isclose(v, w, rel_tol=1e-12)
+    # the speedup grows past DeepSeek-V3's sparsity (32) and drops off at 128
+    assert base[64] > base[32] > base[16] > base[8] > base[4] > 1.0
+    assert base[128] < base[64]
+    # faster communication leaves less to hide
+    for (s, v), (_, w) in zip(res["baseline"], res["2x communication"]):
+        assert w <= v + 1e-12
