@@ -224,6 +224,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serial", action="store_true", help="no second stream")
     ap.add_argument("--rotate", type=int, default=4, help="input sets rotated across steps")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured as a HIP graph and replayed")
     ap.add_argument("--layers", type=int, default=0,
                     help="run this many stacked layers in the two-window schedule and the regular one")
     ap.add_argument("--overlap", action="store_true",
@@ -302,6 +304,42 @@ def main():
 
     ms, kernels = timed(comm)
     serial = timed(None) if (args.overlap and comm is not None) else None
+    graph = None
+    if args.graph:
+        # one HIP graph per input set, captured on a side stream (the comm
+        # stream joins the capture through the library's events), replayed
+        # in rotation; the per-kernel table stays the eager run's
+        graphs = []
+        side = torch.cuda.Stream(device=dev)
+        for j in range(len(xs)):
+            gr = torch.cuda.CUDAGraph()
+            side.wait_stream(compute)
+            with torch.cuda.stream(side):
+                with torch.cuda.graph(gr):
+                    cur = torch.cuda.current_stream()
+                    blk.begin(xs[j], partials[j], compute=cur, comm=comm)
+                    if args.overlap:
+                        L.fs_dense_linear(dt_id, cfg.n_tokens, cfg.hidden, cfg.hidden, partials[j],
+                                          wl.w_next, nxts[j], stream=cur)
+                        L.fs_farskip_residual(blk.desc, outs[j], partials[j], nxts[j], stream=cur)
+                        blk.finish(xs[j], outs[j], compute=cur, comm=comm)
+                    else:
+                        blk.finish(xs[j], partials[j], compute=cur, comm=comm)
+            compute.wait_stream(side)
+            graphs.append(gr)
+        torch.cuda.synchronize()
+        for i in range(args.warmup):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(compute)
+        for i in range(args.steps):
+            graphs[i % len(graphs)].replay()
+        b.record(compute)
+        torch.cuda.synchronize()
+        gms = a.elapsed_time(b) / args.steps
+        graph = {"ms_per_step": gms, "tokens_per_s": cfg.n_tokens / (gms * 1e-3),
+                 "note": "the same step captured as one HIP graph per input set and replayed"}
 
     es = cfg.elem_bytes
     N, d, k, E = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts
@@ -402,6 +440,8 @@ def main():
     }
     if overlap is not None:
         res["overlap"] = overlap
+    if graph is not None:
+        res["graph"] = graph
     if not args.no_cpu_baseline:
         try:
             res["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_sample)
