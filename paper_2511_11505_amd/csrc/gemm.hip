@@ -277,17 +277,23 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
 // One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
-// lds_wave_base + 16 * l.  Issued as inline assembly so that the compiler
-// does not add a conservative wait for every outstanding DMA before each LDS
-// read; the kernel orders them itself with explicit vmcnt waits and
-// barriers.  M0 carries the LDS base and has no other user in this kernel.
-__device__ __forceinline__ void dma16(const void* g, void* lds_wave_base) {
-  const unsigned lds = __builtin_amdgcn_readfirstlane(
-      (unsigned)(uintptr_t)(lds_void_t*)lds_wave_base);
+// LDS address lds + 16 * l, where lds is the wave's destination as a
+// wave-uniform 32-bit LDS address (kept in SGPRs by the caller, so a copy
+// needs no address-space conversion or lane broadcast).  Issued as inline
+// assembly so that the compiler does not add a conservative wait for every
+// outstanding DMA before each LDS read; the kernels order them themselves
+// with explicit vmcnt waits and barriers.  M0 carries the LDS address and has
+// no other user in these kernels.
+__device__ __forceinline__ void dma16_at(const void* g, unsigned lds) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                :
                : "s"(lds), "v"(g)
                : "memory");
+}
+
+// LDS address of a __shared__ location as a wave-uniform 32-bit value.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(const lds_void_t*)p);
 }
 
 // s_waitcnt with only vmcnt constrained (gfx9 encoding).
@@ -463,13 +469,15 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
         wrow = n0 + r;
       pb[i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
     }
+    const unsigned ring_lds = lds_addr(ring);
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
     auto issue = [&](int kt) {
-      unsigned char* slot = ring + (kt % STAGES) * STAGE;
+      const unsigned slot = ring_lds + (unsigned)((kt % STAGES) * STAGE);
 #pragma unroll
-      for (int i = 0; i < A_LD; ++i) dma16(pa[i] + kt * BK, slot + (wave * A_LD + i) * 1024);
+      for (int i = 0; i < A_LD; ++i) dma16_at(pa[i] + kt * BK, slot + (wave_u * A_LD + i) * 1024u);
 #pragma unroll
       for (int i = 0; i < B_LD; ++i)
-        dma16(pb[i] + kt * BK, slot + BM * ROWB + (wave * B_LD + i) * 1024);
+        dma16_at(pb[i] + kt * BK, slot + (unsigned)(BM * ROWB) + (wave_u * B_LD + i) * 1024u);
     };
 
     floatx16 acc[TM][TN];
@@ -699,11 +707,15 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         wrow = n0 + r;
       src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
     }
+    // wave-uniform LDS destinations: ring base + slot + this wave's blocks
+    const unsigned ring_lds = lds_addr(ring);
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
     auto dst_of = [&](int i) {
-      return i < A_LD ? (wave * A_LD + i) * 1024 : BM * ROWB + (wave * B_LD + (i - A_LD)) * 1024;
+      return i < A_LD ? (wave_u * A_LD + i) * 1024u
+                      : (unsigned)(BM * ROWB) + (wave_u * B_LD + (i - A_LD)) * 1024u;
     };
     auto dma_one = [&](int i, int kt) {
-      dma16(src[i] + kt * BK, ring + (kt % STAGES) * STAGE + dst_of(i));
+      dma16_at(src[i] + kt * BK, ring_lds + (unsigned)((kt % STAGES) * STAGE) + dst_of(i));
     };
 
     floatx16 acc[TM][TN];
