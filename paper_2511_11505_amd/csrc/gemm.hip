@@ -1347,8 +1347,9 @@ constexpr int kBM = 128, kBN = 128, kBK = 64;
 // shapes: gate/up takes the register-staged 256 x 256 x 64 kernel (8) when
 // the groups average at least 2048 rows (dense, shared-expert-like) and the
 // interleaved 128 x 256 x 64 ring (5) otherwise, where half-empty 256-row
-// tail tiles would waste MFMA work; down takes the interleaved ring (5) for
-// K >= 2816 and the eight-wave 256 x 256 x 32 DMA ring (2) below that.
+// tail tiles would waste MFMA work; down takes the interleaved 256 x 256 x 64
+// ring (7) when K < 2816 and the groups average at least 1024 rows, and the
+// 128-row interleaved ring (5) otherwise.
 // FS_GEMM_TILE / FS_GEMM_TILE_DOWN (0-9) force a variant, for tuning.
 int tile_choice(bool down, int64_t max_rows, int G, int K) {
   static const int gu_env = [] {
@@ -1359,7 +1360,8 @@ int tile_choice(bool down, int64_t max_rows, int G, int K) {
     const char* e = getenv("FS_GEMM_TILE_DOWN");
     return e ? atoi(e) : -1;
   }();
-  if (down) return dn_env >= 0 ? dn_env : (K >= 2816 ? 5 : 2);
+  if (down)
+    return dn_env >= 0 ? dn_env : (K < 2816 && max_rows >= 1024 * (int64_t)G ? 7 : 5);
   return gu_env >= 0 ? gu_env : (max_rows >= 2048 * (int64_t)G ? 8 : 5);
 }
 

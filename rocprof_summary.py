@@ -137,7 +137,10 @@ def main():
     ap.add_argument("--source")
     ap.add_argument("--tile", default="")
     ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--all-kernels", action="store_true",
+                    help="also list torch's kernels (input generation during setup)")
     a = ap.parse_args()
+    keep = (lambda k: True) if a.all_kernels else (lambda k: not k.startswith("torch:"))
     scales, kib = {}, {}
     if a.overlap:
         overlap_report(a.trace_dir, a.min_us, a.skip)
@@ -150,7 +153,7 @@ def main():
     print("|---|---|---|---|---|---|")
     for (k, g), v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
         avg = sum(v) / len(v)
-        if avg < a.min_us:
+        if avg < a.min_us or not keep(k):
             continue
         print(f"| {k} | {g} | {len(v)} | {avg:.2f} | {min(v):.2f} | {max(v):.2f} |")
     for label, d, ctr in (("FETCH_SIZE", a.fetch, "FETCH_SIZE"), ("WRITE_SIZE", a.write, "WRITE_SIZE")):
@@ -175,6 +178,8 @@ def main():
             avg = sum(v) / len(v)
             if a.kernel and a.kernel in k:
                 kib.setdefault(label, []).append((k, g, avg))
+            if not keep(k):
+                continue
             cal = f"{avg * scale * 1024 / 1e6:.1f}" if scale else "-"
             print(f"| {k} | {g} | {len(v)} | {avg:.0f} | {cal} |")
     if a.traffic_json:
