@@ -21,8 +21,21 @@ Parity status per function (what pins it is in tests/test_oracle_pins.py):
   swiglu ........................... pinned (closed forms)
   combine, moe_block ............... pinned (dense masked brute force)
   farskip_pair, regular_pair ....... pinned (zero-output equality, conservation)
+  farskip_stack, regular_stack ..... pinned (zero-output equality, conservation,
+                                     one layer = the block, the dropped dependency)
+
+oracle.allreduce holds the replicated-activation inference variant (each
+rank runs its own experts on every token; partial sums are all-reduced):
+  local_rows ....................... pinned (the plan's rank blocks)
+  routed_partial, combine_partial .. pinned (partials over R ranks sum to the
+                                     all-to-all block; zero rows; two forms)
+  shared_partial, attention_partial  pinned (partials sum to the full terms)
+  farskip_ar_stack, regular_ar_stack pinned (R = 1 equals the all-to-all
+                                     stacks; conservation; dropped dependency)
+tests/test_oracle_allreduce.py holds those pins.
 """
 
+from . import allreduce  # noqa: F401
 from .moe import (  # noqa: F401
     ROUTER_SLICE,
     logits_f64,

@@ -32,6 +32,11 @@ class MoEConfig:
     zipf_beta: float = 0.0
     seed: int = 0
     next_linear: bool = True   # a dense d x d linear stands in for the next layer
+    # "a2a": each rank routes its own tokens and exchanges rows with
+    # Dispatch / Combine; "allreduce": every rank holds all n_tokens tokens
+    # (replicated activations), runs its own experts and the per-rank
+    # partial sums are all-reduced (the inference variant)
+    ep_mode: str = "a2a"
 
     @property
     def n_local(self):
@@ -44,7 +49,12 @@ class MoEConfig:
 
     @property
     def n_global_tokens(self):
-        return self.n_tokens * self.ep_size
+        return self.n_tokens if self.ep_mode == "allreduce" else self.n_tokens * self.ep_size
+
+    @property
+    def n_sources(self):
+        """Token sets this rank sees: its own (replicated) or one per rank."""
+        return 1 if self.ep_mode == "allreduce" else self.ep_size
 
     @property
     def elem_bytes(self):
