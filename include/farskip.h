@@ -17,6 +17,13 @@
  *                routed output is added into the residual afterwards.
  *   Section 4.1  Dispatch overlaps the next computation; the gate and the
  *                routed experts are the parts that cannot overlap (Eq. 9).
+ *   Section 4.2  The inference variant with replicated activations: every
+ *                rank holds all N tokens and routes them, runs only its
+ *                own experts (fs_local_rows, fs_grouped_expert_ffn_gathered,
+ *                fs_combine_partial) and the per-rank partial sums are
+ *                all-reduced; FarSkip defers the routed all-reduce to the
+ *                next MoE and merges the attention and shared-expert
+ *                partials into one all-reduce (Tab. 5).
  *
  * Conventions shared by every entry point
  *   Memory      Every array argument is DEVICE memory owned by the caller,
@@ -58,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 2
+#define FS_ABI_VERSION 3
 
 typedef enum {
   FS_OK = 0,
@@ -158,7 +165,8 @@ fs_status fs_router_topk(const fs_moe_desc* desc, const void* x, const void* w_r
  *   rank_offsets   [R+1] int32 out: expert_offsets[r * E/R]
  *   slot_to_row    [N*k] int32 out: send row of slot t*k+j
  *   row_to_slot    [N*k] int32 out: its inverse
- *   send           [N*k, d] dtype out: send[slot_to_row[t*k+j]] = x[t] */
+ *   send           [N*k, d] dtype out: send[slot_to_row[t*k+j]] = x[t];
+ *                  NULL computes the plan only (x is then not read) */
 fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
                            int32_t* expert_counts, int32_t* expert_offsets,
                            int32_t* rank_offsets, int32_t* slot_to_row, int32_t* row_to_slot,
@@ -176,6 +184,23 @@ fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, con
 fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
                           const int32_t* src_offsets, int32_t* group_rows,
                           int32_t* group_offsets, fs_stream stream);
+
+/* Rows of this rank's experts with replicated activations (Section 4.2:
+ * every rank holds all N tokens; Section 2.1: rank r owns experts
+ * [r*E/R, (r+1)*E/R)).  These are the plan rows [rank_offsets[r],
+ * rank_offsets[r+1]) of fs_dispatch_pack (expert-major, tokens ascending),
+ * read back to token indices so the expert GEMM gathers them from x.
+ *   expert_offsets [E+1], rank_offsets [R+1], row_to_slot [N*k]: int32 in,
+ *                  as written by fs_dispatch_pack for the same topk_ids
+ *   local_tokens   [min(k, E/R) * N] int32 out: entry i < M_r is the token of
+ *                  local row i, M_r = rank_offsets[r+1] - rank_offsets[r];
+ *                  later entries are not written
+ *   local_offsets  [E/R + 1] int32 out: expert_offsets[r*E/R + e] -
+ *                  rank_offsets[r], the start of local expert e's rows
+ * With N == 0 nothing is written (no rows). */
+fs_status fs_local_rows(const fs_moe_desc* desc, const int32_t* expert_offsets,
+                        const int32_t* rank_offsets, const int32_t* row_to_slot,
+                        int32_t* local_tokens, int32_t* local_offsets, fs_stream stream);
 
 /* Grouped SwiGLU expert FFN (Section 2.1, MLP^j read as SwiGLU): for each
  * group g and its rows X_g, Y_g = (SiLU(X_g Wg^T) * (X_g Wu^T)) Wd^T.
@@ -201,6 +226,22 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
                                 const void* w_gate_up, const void* w_down, void* out_rows,
                                 void* ws, size_t ws_bytes, fs_stream stream);
 
+/* The grouped SwiGLU FFN of fs_grouped_expert_ffn with the input gathered
+ * and the output in grouped order: row i of the grouped order reads
+ * x[gather_rows[i]] and writes y[i].  Used with replicated activations,
+ * where the GEMM reads this rank's rows straight from the token matrix.
+ *   x            [*, d] dtype
+ *   gather_rows  [max_rows] int32: token of each row (local_tokens of
+ *                fs_local_rows)
+ *   y            [max_rows, d] dtype out
+ * Other arguments, the workspace (FS_OP_GROUPED_FFN) and the arithmetic are
+ * those of fs_grouped_expert_ffn. */
+fs_status fs_grouped_expert_ffn_gathered(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                         const void* x, const int32_t* gather_rows,
+                                         const int32_t* group_offsets, int64_t max_rows,
+                                         const void* w_gate_up, const void* w_down, void* y,
+                                         void* ws, size_t ws_bytes, fs_stream stream);
+
 /* Combine and unpack (Section 2.1, Combine: weighted sum of the returned
  * expert outputs), fused with the deferred residual add of Eq. 7.
  *   acc[t] = sum_{j<k} topk_w[t,j] * y_ret[slot_to_row[t*k+j]]  (fp32, j
@@ -214,6 +255,30 @@ fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
                             const int32_t* slot_to_row, const float* topk_w,
                             const void* shared_out, void* routed_out, void* residual,
                             fs_stream stream);
+
+/* Partial Combine of rank r with replicated activations (Section 4.2):
+ *   partial[t] = sum over j < k with lo <= slot_to_row[t*k+j] < hi of
+ *                topk_w[t,j] * y_local[slot_to_row[t*k+j] - lo]
+ * in fp32, j ascending, rounded once to dtype; lo = rank_offsets[r],
+ * hi = rank_offsets[r+1] (device).  A token whose selections are all on
+ * other ranks gets a zero row.  Summed over the R ranks (the all-reduce)
+ * the partials are the routed MoE output.
+ *   y_local      [M_r, d] dtype: fs_grouped_expert_ffn_gathered's y
+ *   slot_to_row  [N*k], rank_offsets [R+1]: int32, from fs_dispatch_pack
+ *   topk_w       [N, k] fp32
+ *   partial_out  [N, d] dtype out */
+fs_status fs_combine_partial(const fs_moe_desc* desc, const void* y_local,
+                             const int32_t* slot_to_row, const int32_t* rank_offsets,
+                             const float* topk_w, void* partial_out, fs_stream stream);
+
+/* One-GPU stand-in for the all-reduce of an [N, d] dtype partial sum over
+ * the R ranks (Section 4.2): with one participant the sum is the partial
+ * itself, so out = partial as a device-to-device copy on `stream` (the
+ * traffic and the stream placement of the collective; on a node RCCL's
+ * all-reduce takes its place).  out == partial is an in-place no-op; other
+ * overlaps are FS_ERR_INVALID. */
+fs_status fs_allreduce_standin(const fs_moe_desc* desc, void* out, const void* partial,
+                               fs_stream stream);
 
 /* FarSkip residual add (Eq. 7): out = residual + deferred (+ extra), in
  * fp32 with one rounding.  out may equal residual (in place).  [N, d]
@@ -313,10 +378,12 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
 /* Per-kernel timing with HIP events recorded on the launch stream around
  * selected kernels.  fs_profile_read synchronises those events.
  * FS_K_GATE_UP / FS_K_DOWN time the routed experts' passes (and
- * fs_grouped_expert_ffn); FS_K_SHARED_* the shared experts' passes inside
- * fs_moe_block_forward; FS_K_DISPATCH_COPY / FS_K_COMBINE_COPY the Dispatch
- * and Combine stand-in copies on the stream they run on; FS_K_DENSE
- * fs_dense_linear. */
+ * fs_grouped_expert_ffn and fs_grouped_expert_ffn_gathered); FS_K_COMBINE
+ * fs_combine_unpack, fs_combine_partial and the block's Combine;
+ * FS_K_SHARED_* the shared experts' passes inside fs_moe_block_forward;
+ * FS_K_DISPATCH_COPY / FS_K_COMBINE_COPY the Dispatch and Combine stand-in
+ * copies on the stream they run on; FS_K_DENSE fs_dense_linear;
+ * FS_K_ALLREDUCE_COPY fs_allreduce_standin. */
 typedef enum {
   FS_K_ROUTER = 0,
   FS_K_TOPK = 1,
@@ -330,7 +397,8 @@ typedef enum {
   FS_K_DISPATCH_COPY = 9,
   FS_K_DENSE = 10,
   FS_K_COMBINE_COPY = 11,
-  FS_K_COUNT = 12
+  FS_K_ALLREDUCE_COPY = 12,
+  FS_K_COUNT = 13
 } fs_kernel_id;
 fs_status fs_profile_enable(int32_t on);
 fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);

@@ -20,8 +20,8 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK = range(4)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
- FS_K_COMBINE_COPY, FS_K_COUNT) = range(13)
-FS_ABI_VERSION = 2
+ FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_COUNT) = range(14)
+FS_ABI_VERSION = 3
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -59,9 +59,14 @@ _SIGS = {
     "fs_router_topk": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_dispatch_pack": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_receive_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
+    "fs_local_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
+    "fs_grouped_expert_ffn_gathered": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp,
+                                              _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_grouped_expert_ffn": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp, _i64,
                                      _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_combine_unpack": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "fs_combine_partial": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
+    "fs_allreduce_standin": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp]),
     "fs_farskip_residual": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
     "fs_block_sync_create": (_i32, [ctypes.POINTER(_vp)]),
     "fs_block_sync_destroy": (_i32, [_vp]),
@@ -174,6 +179,22 @@ def fs_receive_rows(desc, src_counts, src_offsets, group_rows, group_offsets, st
                                   ptr(group_rows), ptr(group_offsets), stream_handle(stream)))
 
 
+def fs_local_rows(desc, expert_offsets, rank_offsets, row_to_slot, local_tokens, local_offsets,
+                  stream=None):
+    _check(load().fs_local_rows(ctypes.byref(desc), ptr(expert_offsets), ptr(rank_offsets),
+                                ptr(row_to_slot), ptr(local_tokens), ptr(local_offsets),
+                                stream_handle(stream)))
+
+
+def fs_grouped_expert_ffn_gathered(desc, n_groups, ffn, x, gather_rows, group_offsets, max_rows,
+                                   w_gate_up, w_down, y, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(load().fs_grouped_expert_ffn_gathered(ctypes.byref(desc), n_groups, ffn, ptr(x),
+                                                 ptr(gather_rows), ptr(group_offsets), max_rows,
+                                                 ptr(w_gate_up), ptr(w_down), ptr(y), wp, wb,
+                                                 stream_handle(stream)))
+
+
 def fs_grouped_expert_ffn(desc, n_groups, ffn, in_rows, group_rows, group_offsets, max_rows,
                           w_gate_up, w_down, out_rows, ws, stream=None):
     wp, wb = _ws(ws)
@@ -188,6 +209,17 @@ def fs_combine_unpack(desc, y_ret, slot_to_row, topk_w, shared_out, routed_out, 
     _check(load().fs_combine_unpack(ctypes.byref(desc), ptr(y_ret), ptr(slot_to_row), ptr(topk_w),
                                     ptr(shared_out), ptr(routed_out), ptr(residual),
                                     stream_handle(stream)))
+
+
+def fs_combine_partial(desc, y_local, slot_to_row, rank_offsets, topk_w, partial_out, stream=None):
+    _check(load().fs_combine_partial(ctypes.byref(desc), ptr(y_local), ptr(slot_to_row),
+                                     ptr(rank_offsets), ptr(topk_w), ptr(partial_out),
+                                     stream_handle(stream)))
+
+
+def fs_allreduce_standin(desc, out, partial, stream=None):
+    _check(load().fs_allreduce_standin(ctypes.byref(desc), ptr(out), ptr(partial),
+                                       stream_handle(stream)))
 
 
 def fs_farskip_residual(desc, out, residual, deferred, extra=None, stream=None):

@@ -297,13 +297,13 @@ fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, con
   if (st != FS_OK) return st;
   if (desc->n_tokens == 0) return FS_OK;
   NEED4(topk_ids, "topk_ids");
-  NEED(x, "x");
   NEED4(expert_counts, "expert_counts");
   NEED4(expert_offsets, "expert_offsets");
   NEED4(rank_offsets, "rank_offsets");
   NEED4(slot_to_row, "slot_to_row");
   NEED4(row_to_slot, "row_to_slot");
-  NEED(send, "send");
+  OPT(send, "send");
+  if (send) NEED(x, "x");
   if (ws_bytes < plan_bytes(desc))
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_DISPATCH_PACK)");
   NEED(ws, "ws");
@@ -327,12 +327,27 @@ fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
   return FS_OK;
 }
 
+fs_status fs_local_rows(const fs_moe_desc* desc, const int32_t* expert_offsets,
+                        const int32_t* rank_offsets, const int32_t* row_to_slot,
+                        int32_t* local_tokens, int32_t* local_offsets, fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED4(expert_offsets, "expert_offsets");
+  NEED4(rank_offsets, "rank_offsets");
+  NEED4(row_to_slot, "row_to_slot");
+  NEED4(local_tokens, "local_tokens");
+  NEED4(local_offsets, "local_offsets");
+  FS_HIP(fs::launch_local_rows(expert_offsets, rank_offsets, row_to_slot, desc->n_tokens,
+                               desc->top_k, desc->n_experts, desc->ep_size, desc->ep_rank,
+                               local_tokens, local_offsets, S(stream)),
+         "local_rows");
+  return FS_OK;
+}
+
 // ---- grouped FFN
-fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
-                                const void* in_rows, const int32_t* group_rows,
-                                const int32_t* group_offsets, int64_t max_rows,
-                                const void* w_gate_up, const void* w_down, void* out_rows,
-                                void* ws, size_t ws_bytes, fs_stream stream) {
+static fs_status ffn_checks(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                            const int32_t* group_offsets, int64_t max_rows) {
   fs_status st = check_desc(desc);
   if (st != FS_OK) return st;
   if (n_groups < 1) return fail(FS_ERR_INVALID, "n_groups must be >= 1");
@@ -343,6 +358,40 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
   if (max_rows >= ((int64_t)1 << 31)) return fail(FS_ERR_UNSUPPORTED, "max_rows must be < 2^31");
   if (!group_offsets && n_groups != 1)
     return fail(FS_ERR_INVALID, "group_offsets may be NULL only with n_groups == 1");
+  return FS_OK;
+}
+
+fs_status fs_grouped_expert_ffn_gathered(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                         const void* x, const int32_t* gather_rows,
+                                         const int32_t* group_offsets, int64_t max_rows,
+                                         const void* w_gate_up, const void* w_down, void* y,
+                                         void* ws, size_t ws_bytes, fs_stream stream) {
+  fs_status st = ffn_checks(desc, n_groups, ffn, group_offsets, max_rows);
+  if (st != FS_OK) return st;
+  if (max_rows == 0) return FS_OK;
+  NEED(x, "x");
+  NEED4(gather_rows, "gather_rows");
+  OPT4(group_offsets, "group_offsets");
+  NEED(w_gate_up, "w_gate_up");
+  NEED(w_down, "w_down");
+  NEED(y, "y");
+  if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
+  NEED(ws, "ws");
+  FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, x, gather_rows,
+                                nullptr, group_offsets, max_rows, w_gate_up, w_down, y, ws,
+                                S(stream), FS_K_GATE_UP),
+         "grouped_ffn_gathered");
+  return FS_OK;
+}
+
+fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                const void* in_rows, const int32_t* group_rows,
+                                const int32_t* group_offsets, int64_t max_rows,
+                                const void* w_gate_up, const void* w_down, void* out_rows,
+                                void* ws, size_t ws_bytes, fs_stream stream) {
+  fs_status st = ffn_checks(desc, n_groups, ffn, group_offsets, max_rows);
+  if (st != FS_OK) return st;
   if (max_rows == 0) return FS_OK;
   NEED(in_rows, "in_rows");
   OPT4(group_rows, "group_rows");
@@ -354,7 +403,7 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
   NEED(ws, "ws");
   FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, in_rows, group_rows,
-                                group_offsets, max_rows, w_gate_up, w_down, out_rows, ws,
+                                group_rows, group_offsets, max_rows, w_gate_up, w_down, out_rows, ws,
                                 S(stream), FS_K_GATE_UP),
          "grouped_ffn");
   return FS_OK;
@@ -378,9 +427,50 @@ fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
   hipStream_t s = S(stream);
   fs::prof_begin(FS_K_COMBINE, s);
   FS_HIP(fs::launch_combine(desc->dtype, y_ret, slot_to_row, topk_w, shared_out, routed_out,
-                            residual, desc->n_tokens, desc->top_k, desc->hidden, s),
+                            residual, nullptr, desc->n_tokens, desc->top_k, desc->hidden, s),
          "combine");
   fs::prof_end(FS_K_COMBINE, s);
+  return FS_OK;
+}
+
+fs_status fs_combine_partial(const fs_moe_desc* desc, const void* y_local,
+                             const int32_t* slot_to_row, const int32_t* rank_offsets,
+                             const float* topk_w, void* partial_out, fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED(y_local, "y_local");
+  NEED4(slot_to_row, "slot_to_row");
+  NEED4(rank_offsets, "rank_offsets");
+  NEED4(topk_w, "topk_w");
+  NEED(partial_out, "partial_out");
+  hipStream_t s = S(stream);
+  fs::prof_begin(FS_K_COMBINE, s);
+  FS_HIP(fs::launch_combine(desc->dtype, y_local, slot_to_row, topk_w, nullptr, partial_out,
+                            nullptr, rank_offsets + desc->ep_rank, desc->n_tokens, desc->top_k,
+                            desc->hidden, s),
+         "combine_partial");
+  fs::prof_end(FS_K_COMBINE, s);
+  return FS_OK;
+}
+
+fs_status fs_allreduce_standin(const fs_moe_desc* desc, void* out, const void* partial,
+                               fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED(out, "out");
+  NEED(partial, "partial");
+  const size_t bytes = (size_t)desc->n_tokens * desc->hidden * elem(desc->dtype);
+  const char* o = static_cast<const char*>(out);
+  const char* p = static_cast<const char*>(partial);
+  if (o < p + bytes && p < o + bytes && o != p)
+    return fail(FS_ERR_INVALID, "out and partial overlap");
+  hipStream_t s = S(stream);
+  if (o == p) return FS_OK;
+  fs::prof_begin(FS_K_ALLREDUCE_COPY, s);
+  FS_HIP(hipMemcpyAsync(out, partial, bytes, hipMemcpyDeviceToDevice, s), "hipMemcpyAsync");
+  fs::prof_end(FS_K_ALLREDUCE_COPY, s);
   return FS_OK;
 }
 
@@ -570,7 +660,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     // shared experts on o_{k-1}, then the next layer's partial input
     if (desc->n_shared > 0) {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, 1, desc->n_shared * desc->ffn_shared, D,
-                                    residual_in, nullptr, nullptr, N, wt->ws_gate_up, wt->ws_down,
+                                    residual_in, nullptr, nullptr, nullptr, N, wt->ws_gate_up, wt->ws_down,
                                     b->shared_out, ws_shared, sc, FS_K_SHARED_GATE_UP),
              "shared_ffn");
     }
@@ -599,7 +689,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       rows = nullptr;
       goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
     }
-    FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, goff,
+    FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, rows, goff,
                                   max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,
                                   FS_K_GATE_UP),
            "grouped_ffn");
@@ -631,7 +721,7 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     const void* y_ret = b->ret ? b->ret : y_slot;
     fs::prof_begin(FS_K_COMBINE, sc);
     FS_HIP(fs::launch_combine(desc->dtype, y_ret, b->slot_to_row, b->topk_w, nullptr, nullptr,
-                              residual_io, N, K, D, sc),
+                              residual_io, nullptr, N, K, D, sc),
            "combine");
     fs::prof_end(FS_K_COMBINE, sc);
   }

@@ -11,6 +11,10 @@
 //      below the token's lane).
 // Pack copies each token row once from HBM and writes it to its k rows with
 // 16-byte vector accesses.
+//
+// With replicated activations (the inference variant) a rank keeps only the
+// rows of its own experts: a contiguous block of the plan's rows, read back
+// to token indices so the expert GEMM gathers them straight from x.
 
 #include "common.hpp"
 #include "internal.hpp"
@@ -166,6 +170,21 @@ __global__ __launch_bounds__(256) void receive_rows_kernel(const int32_t* __rest
   if (e == E_loc - 1 && tid == 0) goff[E_loc] = base;
 }
 
+// Rows [rank_offsets[r], rank_offsets[r+1]) of the plan belong to rank r's
+// experts.  Thread i < that count writes the token of row lo + i; threads
+// 0..E_loc write the local group offsets.
+__global__ __launch_bounds__(256) void local_rows_kernel(const int32_t* __restrict__ offsets,
+                                                         const int32_t* __restrict__ rank_offsets,
+                                                         const int32_t* __restrict__ row_to_slot,
+                                                         int k, int E_loc, int r,
+                                                         int32_t* __restrict__ local_tokens,
+                                                         int32_t* __restrict__ local_offsets) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int lo = rank_offsets[r], hi = rank_offsets[r + 1];
+  if (i < hi - lo) local_tokens[i] = row_to_slot[lo + i] / k;
+  if (i <= E_loc) local_offsets[i] = offsets[(size_t)r * E_loc + i] - lo;
+}
+
 }  // namespace
 
 size_t plan_ws_bytes(int N, int E) {
@@ -197,6 +216,16 @@ hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int
   else
     pack_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)x, slot_to_row, N, k, d,
                                              (bf16_t*)send);
+  return hipGetLastError();
+}
+
+hipError_t launch_local_rows(const int32_t* offsets, const int32_t* rank_offsets,
+                             const int32_t* row_to_slot, int N, int k, int E, int R, int r,
+                             int32_t* local_tokens, int32_t* local_offsets, hipStream_t s) {
+  const int E_loc = E / R;
+  const int64_t rows = (int64_t)N * k, n = rows > E_loc + 1 ? rows : E_loc + 1;
+  local_rows_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+      offsets, rank_offsets, row_to_slot, k, E_loc, r, local_tokens, local_offsets);
   return hipGetLastError();
 }
 

@@ -4,6 +4,10 @@
 // Combine is a gather: token t reads its k expert-output rows through
 // slot_to_row, so no atomics are needed and the fp32 sum runs in slot order
 // j = 0..k-1.  All adds run in fp32 and round once at the store.
+//
+// The partial Combine of the replicated-activation variant is the same
+// gather restricted to the plan rows [lo, hi) of this rank's experts, read
+// from y at row - lo; other slots contribute nothing.
 
 #include "common.hpp"
 #include "internal.hpp"
@@ -13,14 +17,15 @@ namespace {
 
 // Each lane handles one 16-byte chunk of one token row; waves are laid out
 // (token, 64-chunk block) so that short batches still fill the machine.
-template <typename T>
+template <typename T, bool LOCAL>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
                                                       const int32_t* __restrict__ slot_to_row,
                                                       const float* __restrict__ topk_w,
                                                       const T* __restrict__ shared_out,
                                                       T* __restrict__ routed_out,
-                                                      T* __restrict__ residual, int N, int k,
-                                                      int d) {
+                                                      T* __restrict__ residual,
+                                                      const int32_t* __restrict__ row_range,
+                                                      int N, int k, int d) {
   constexpr int V = 16 / sizeof(T);
   const int nch = d / V;
   const int nb = (nch + 63) / 64;
@@ -32,9 +37,18 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
   float acc[V];
 #pragma unroll
   for (int i = 0; i < V; ++i) acc[i] = 0.f;
+  int lo = 0, hi = 0;
+  if (LOCAL) {
+    lo = row_range[0];
+    hi = row_range[1];
+  }
   for (int j = 0; j < k; ++j) {
-    const int row = slot_to_row[(size_t)t * k + j];
+    int row = slot_to_row[(size_t)t * k + j];
     if (row < 0) continue;
+    if (LOCAL) {
+      if (row < lo || row >= hi) continue;
+      row -= lo;
+    }
     const float wj = topk_w[(size_t)t * k + j];
     Vec16<T> v;
     v.raw = ld16(y + (size_t)row * d + (size_t)c * V);
@@ -87,17 +101,22 @@ __global__ __launch_bounds__(256) void residual_kernel(T* out, const T* a, const
 
 hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_row,
                           const float* topk_w, const void* shared_out, void* routed_out,
-                          void* residual, int N, int k, int d, hipStream_t s) {
+                          void* residual, const int32_t* row_range, int N, int k, int d,
+                          hipStream_t s) {
   const int64_t nb = ((int64_t)d / (dtype == 0 ? 4 : 8) + 63) / 64;
   dim3 grid((unsigned)((N * nb + 3) / 4));
-  if (dtype == 0)
-    combine_kernel<float><<<grid, 256, 0, s>>>((const float*)y_ret, slot_to_row, topk_w,
-                                               (const float*)shared_out, (float*)routed_out,
-                                               (float*)residual, N, k, d);
-  else
-    combine_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)y_ret, slot_to_row, topk_w,
-                                                (const bf16_t*)shared_out, (bf16_t*)routed_out,
-                                                (bf16_t*)residual, N, k, d);
+#define FS_COMBINE(T, L)                                                                    \
+  combine_kernel<T, L><<<grid, 256, 0, s>>>((const T*)y_ret, slot_to_row, topk_w,          \
+                                            (const T*)shared_out, (T*)routed_out,          \
+                                            (T*)residual, row_range, N, k, d)
+  if (dtype == 0) {
+    if (row_range) FS_COMBINE(float, true);
+    else FS_COMBINE(float, false);
+  } else {
+    if (row_range) FS_COMBINE(bf16_t, true);
+    else FS_COMBINE(bf16_t, false);
+  }
+#undef FS_COMBINE
   return hipGetLastError();
 }
 

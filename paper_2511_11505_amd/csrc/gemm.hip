@@ -1489,7 +1489,8 @@ size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn, int d) {
 }
 
 hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
-                              const int32_t* rows, const int32_t* goff, int64_t max_rows,
+                              const int32_t* rows_in, const int32_t* rows_out,
+                              const int32_t* goff, int64_t max_rows,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
                               hipStream_t s, int prof_gate_up) {
   const bool profile = prof_gate_up >= 0;
@@ -1510,15 +1511,15 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
       const unsigned grid = (unsigned)((int64_t)G * (ffn / 32) * spe);
       if (wide)
         gemm_bf16_stream_kernel<MODE_GATEUP, 4><<<grid, 64, 0, s>>>(
-            (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
+            (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
             P, spe, kps);
       else
         gemm_bf16_stream_kernel<MODE_GATEUP, 2><<<grid, 64, 0, s>>>(
-            (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
+            (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
             P, spe, kps);
       if (spe > 1)
         stream_reduce_kernel<MODE_GATEUP><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * ffn, 256), 8192),
-                                            256, 0, s>>>(P, rows, goff, G, max_rows, ffn, spe, H, ffn);
+                                            256, 0, s>>>(P, rows_in, goff, G, max_rows, ffn, spe, H, ffn);
       if (profile) prof_end(pg, s);
     }
     {
@@ -1528,24 +1529,24 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
       const unsigned grid = (unsigned)((int64_t)G * (d / 64) * spe);
       if (wide)
         gemm_bf16_stream_kernel<MODE_DOWN, 4><<<grid, 64, 0, s>>>(
-            H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+            H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
       else
         gemm_bf16_stream_kernel<MODE_DOWN, 2><<<grid, 64, 0, s>>>(
-            H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+            H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
       if (spe > 1)
         stream_reduce_kernel<MODE_DOWN><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * d, 256), 8192),
-                                          256, 0, s>>>(P, rows, goff, G, max_rows, d, spe,
+                                          256, 0, s>>>(P, rows_out, goff, G, max_rows, d, spe,
                                                        (bf16_t*)out, d);
       if (profile) prof_end(pd, s);
     }
   } else if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     if (profile) prof_begin(pg, s);
-    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d), (const bf16_t*)in, rows, goff, G,
+    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d), (const bf16_t*)in, rows_in, goff, G,
                            max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn, s);
     if (profile) prof_end(pg, s);
     if (profile) prof_begin(pd, s);
-    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn), H, rows, goff, G, max_rows,
+    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn), H, rows_out, goff, G, max_rows,
                          (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, s);
     if (profile) prof_end(pd, s);
   } else if (dtype == 1) {
@@ -1553,24 +1554,24 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
     const int64_t g1 = grid_for(max_rows, G, kBM, ffn / (kBN / 2));
     if (profile) prof_begin(pg, s);
     gemm_bf16_kernel<MODE_GATEUP, kBM, kBN, kBK, 2, 2><<<(unsigned)g1, 256, 0, s>>>(
-        (const bf16_t*)in, rows, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn);
+        (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn);
     if (profile) prof_end(pg, s);
     const int64_t g2 = grid_for(max_rows, G, kBM, d / kBN);
     if (profile) prof_begin(pd, s);
     gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g2, 256, 0, s>>>(
-        H, rows, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);
+        H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);
     if (profile) prof_end(pd, s);
   } else {
     float* H = reinterpret_cast<float*>(ws);
     const int64_t g1 = grid_for(max_rows, G, 64, ffn / 32);
     if (profile) prof_begin(pg, s);
     gemm_f32_kernel<MODE_GATEUP><<<(unsigned)g1, 256, 0, s>>>(
-        (const float*)in, rows, goff, G, max_rows, (const float*)w_gate_up, d, ffn, H, ffn);
+        (const float*)in, rows_in, goff, G, max_rows, (const float*)w_gate_up, d, ffn, H, ffn);
     if (profile) prof_end(pg, s);
     const int64_t g2 = grid_for(max_rows, G, 64, d / 64);
     if (profile) prof_begin(pd, s);
     gemm_f32_kernel<MODE_DOWN><<<(unsigned)g2, 256, 0, s>>>(
-        H, rows, goff, G, max_rows, (const float*)w_down, ffn, d, (float*)out, d);
+        H, rows_out, goff, G, max_rows, (const float*)w_down, ffn, d, (float*)out, d);
     if (profile) prof_end(pd, s);
   }
   return hipGetLastError();

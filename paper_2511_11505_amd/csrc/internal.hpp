@@ -31,23 +31,32 @@ hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* 
                        int32_t* row_to_slot, void* ws, hipStream_t s);
 hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int N, int k, int d,
                        void* send, hipStream_t s);
+hipError_t launch_local_rows(const int32_t* offsets, const int32_t* rank_offsets,
+                             const int32_t* row_to_slot, int N, int k, int E, int R, int r,
+                             int32_t* local_tokens, int32_t* local_offsets, hipStream_t s);
 hipError_t launch_receive_rows(const int32_t* src_counts, const int32_t* src_offsets, int R,
                                int E, int r, int64_t cap, int32_t* group_rows,
                                int32_t* group_offsets, hipStream_t s);
 
 // ---- grouped SwiGLU FFN and dense linear (gemm.hip)
 size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn, int d);
+// rows_in: gate/up reads input row rows_in[i] (NULL: row i); rows_out: down
+// writes output row rows_out[i] (NULL: row i).
 hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const void* in,
-                              const int32_t* rows, const int32_t* goff, int64_t max_rows,
+                              const int32_t* rows_in, const int32_t* rows_out,
+                              const int32_t* goff, int64_t max_rows,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
                               hipStream_t s, int prof_gate_up);  // profile id of gate/up, down = +1; -1: none
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s);
 
 // ---- combine and residual (elementwise.hip)
+// row_range (device, 2 ints) or NULL: only plan rows in [row_range[0],
+// row_range[1]) contribute, read from y_ret at row - row_range[0].
 hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_row,
                           const float* topk_w, const void* shared_out, void* routed_out,
-                          void* residual, int N, int k, int d, hipStream_t s);
+                          void* residual, const int32_t* row_range, int N, int k, int d,
+                          hipStream_t s);
 hipError_t launch_residual(int dtype, void* out, const void* a, const void* b, const void* c,
                            int64_t n_elems, hipStream_t s);
 

@@ -95,6 +95,21 @@ CONFIGS = {
         top_k=8, ffn=2048, score="sigmoid", norm_topk=True, n_shared=1,
         ffn_shared=2048, n_groups=8, topk_groups=4, ep_size=8, ep_rank=0,
         dtype="bf16", bias="zipf", zipf_s=1.2, zipf_beta=0.05, seed=5),
+    # Replicated-activation inference (all-reduce variant), one rank of
+    # EP = TP = 8: a DeepSeek-V2-shaped layer (160 experts top-6 softmax of
+    # 8 groups / top-3, 2 shared experts, routed scale 16) on a prefill of
+    # 2 sequences x 2048 tokens held by every rank.
+    "dsv2_ar": MoEConfig(
+        name="dsv2_ar", n_tokens=4096, hidden=5120, n_experts=160, top_k=6,
+        ffn=1536, score="softmax", norm_topk=False, n_shared=2, ffn_shared=1536,
+        n_groups=8, topk_groups=3, routed_scale=16.0, ep_size=8, ep_rank=0,
+        dtype="bf16", seed=6, ep_mode="allreduce"),
+    # The same variant on a Llama-4-Scout-shaped layer: 16 experts top-1
+    # sigmoid with a uniform selection bias, one shared expert.
+    "scout_ar": MoEConfig(
+        name="scout_ar", n_tokens=4096, hidden=5120, n_experts=16, top_k=1,
+        ffn=8192, score="sigmoid", norm_topk=False, n_shared=1, ffn_shared=8192,
+        ep_size=8, ep_rank=0, dtype="bf16", bias="uniform", seed=7, ep_mode="allreduce"),
 }
 
 ORDER = ["tiny", "dsv2lite", "scout", "dsv3_prefill", "dsv3_decode"]

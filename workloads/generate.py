@@ -90,8 +90,9 @@ class Workload:
 
     @property
     def x(self):
-        """This rank's own tokens: the MoE input o_{k-1}."""
-        return self.x_all[self.cfg.ep_rank]
+        """This rank's tokens, the MoE input o_{k-1}: its own (all-to-all) or
+        the replicated token set (all-reduce)."""
+        return self.x_all[0 if self.cfg.ep_mode == "allreduce" else self.cfg.ep_rank]
 
 
 def expert_weights(cfg, device, e_local):
@@ -108,8 +109,8 @@ def source_tokens(cfg, device, src):
 def make_workload(cfg, device="cpu", with_experts=True):
     R, N, d, E, F = cfg.ep_size, cfg.n_tokens, cfg.hidden, cfg.n_experts, cfg.ffn
     dt = torch_dtype(cfg.dtype)
-    x_all = torch.empty((R, N, d), dtype=dt, device=device)
-    for s in range(R):
+    x_all = torch.empty((cfg.n_sources, N, d), dtype=dt, device=device)
+    for s in range(cfg.n_sources):
         x_all[s] = source_tokens(cfg, device, s)
     w_router = normal((E, d), WEIGHT_STD, cfg.dtype, device, cfg.seed, TAG_ROUTER)
     bias = selection_bias(cfg, device)
@@ -130,7 +131,7 @@ def make_workload(cfg, device="cpu", with_experts=True):
                              for s in range(cfg.n_shared)])
     w_next = normal((d, d), WEIGHT_STD, cfg.dtype, device, cfg.seed, TAG_NEXT) if cfg.next_linear else None
     y_remote = None
-    if R > 1:
+    if R > 1 and cfg.ep_mode == "a2a":
         y_remote = normal((cfg.cap, d), Y_REMOTE_STD, cfg.dtype, device, cfg.seed, TAG_Y_REMOTE)
     return Workload(cfg, device, x_all, w_router, bias, w_gate_up, w_down, sh_gu, sh_dn, w_next, y_remote)
 
@@ -146,6 +147,25 @@ def merge_shared(sh_gate_up, sh_down):
     gu = torch.cat([gate, up], dim=0).contiguous()
     dn = sh_down.permute(1, 0, 2).reshape(d, S * Fs).contiguous()
     return gu, dn
+
+
+def tp_shared_slice(gate_up, down, ep_size, ep_rank):
+    """Rank r's tensor-parallel block of a merged shared-expert SwiGLU of
+    width W (gate_up [2W, d], down [d, W]): hidden units
+    [r W/R, (r+1) W/R), as (gate_up [2W/R, d], down [d, W/R]), contiguous
+    (a weight-layout transform)."""
+    W = down.shape[1]
+    lo, hi = ep_rank * W // ep_size, (ep_rank + 1) * W // ep_size
+    gu = torch.cat([gate_up[lo:hi], gate_up[W + lo:W + hi]], dim=0).contiguous()
+    return gu, down[:, lo:hi].contiguous()
+
+
+def tp_attention_slice(w_a, w_b, ep_size, ep_rank):
+    """Rank r's tensor-parallel block of the attention stand-in: rows
+    [r d/R, (r+1) d/R) of w_a, the same columns of w_b (contiguous)."""
+    d = w_a.shape[0]
+    lo, hi = ep_rank * d // ep_size, (ep_rank + 1) * d // ep_size
+    return w_a[lo:hi].contiguous(), w_b[:, lo:hi].contiguous()
 
 
 def synthetic_topk_ids(n_tokens, n_experts, top_k, seed, device="cpu", skew=0.0):
