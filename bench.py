@@ -50,7 +50,7 @@ def measured_traffic(cfg_name):
 
 
 KERNEL_NAMES = ("router", "topk", "plan", "pack", "gate_up", "down", "combine", "shared_gate_up",
-                "shared_down", "dispatch_copy", "next_layer", "combine_copy")
+                "shared_down", "dispatch_copy", "next_layer", "combine_copy", "allreduce_copy")
 
 
 def kernel_table(L):
@@ -213,6 +213,145 @@ def bench_layers(args, cfg, torch, L):
     print(json.dumps(res), flush=True)
 
 
+def bench_replicated(args, cfg, torch, L):
+    """L stacked layers of the replicated-activation (all-reduce) variant on
+    one rank: the FarSkip schedule with the all-reduce stand-in copies on a
+    second stream, the same order on one stream, and the regular schedule;
+    one JSON line with the times, Tab. 5's two overlap windows and the
+    roofline of the gathered routed gate/up GEMM."""
+    import numpy as np
+
+    from paper_2511_11505_amd.replicated import ReplicatedStack
+    from workloads.generate import merge_shared, stack_layers, tp_attention_slice, tp_shared_slice
+
+    dev = "cuda:0"
+    t0 = time.perf_counter()
+    R, r = cfg.ep_size, cfg.ep_rank
+    layers = stack_layers(cfg, args.layers, dev)
+    gl = []
+    for _, wl, w_a, w_b in layers:
+        sh_gu = sh_dn = None
+        if cfg.n_shared:
+            sh_gu, sh_dn = tp_shared_slice(*merge_shared(wl.sh_gate_up, wl.sh_down), R, r)
+        wa_r, wb_r = tp_attention_slice(w_a, w_b, R, r)
+        gl.append(dict(w_router=wl.w_router, bias=wl.bias, w_gate_up=wl.w_gate_up,
+                       w_down=wl.w_down, sh_gate_up=sh_gu, sh_down=sh_dn, w_a=wa_r, w_b=wb_r))
+    x = layers[0][1].x
+    del layers
+    st = ReplicatedStack(cfg, gl, device=dev)
+    comm = torch.cuda.Stream(device=dev)
+    compute = torch.cuda.current_stream()
+    # rows this rank's experts receive, per layer (untimed pass)
+    st.farskip(x, compute=compute, comm=comm, keep_ids=True)
+    torch.cuda.synchronize()
+    lo, hi = r * cfg.n_local, (r + 1) * cfg.n_local
+    rows, active = [], []
+    for ids in st.kept_ids:
+        ids = ids.cpu().numpy()
+        local = ids[(ids >= lo) & (ids < hi)]
+        rows.append(local.size)
+        active.append(np.unique(local).size)
+    st.kept_ids = []
+    log(f"setup {time.perf_counter() - t0:.1f}s: {args.layers} replicated layers of {cfg.name}, "
+        f"local rows per layer {rows}")
+
+    def timed(run):
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        L.fs_profile_reset()
+        L.fs_profile_enable(True)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(compute)
+        for _ in range(args.steps):
+            run()
+        b.record(compute)
+        torch.cuda.synchronize()
+        L.fs_profile_enable(False)
+        return a.elapsed_time(b) / args.steps, kernel_table(L)
+
+    ms_fs, k_fs = timed(lambda: st.farskip(x, compute=compute, comm=comm))
+    if args.farskip_only:
+        print(json.dumps({"schedule": "farskip", "ms_per_step": ms_fs,
+                          "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()}}),
+              flush=True)
+        return
+    ms_serial, _ = timed(lambda: st.farskip(x, compute=compute, comm=None))
+    ms_rg, k_rg = timed(lambda: st.regular(x, compute=compute))
+    us = lambda k, name: k[name]["us_per_launch"] if name in k else 0.0
+    N, d, F, es = cfg.n_tokens, cfg.hidden, cfg.ffn, cfg.elem_bytes
+    per_layer = ms_fs * 1e3 / args.layers
+    attention = 2 * us(k_fs, "next_layer")
+    routed = sum(us(k_fs, n) for n in ("router", "topk", "plan", "gate_up", "down", "combine"))
+    shared = us(k_fs, "shared_gate_up") + us(k_fs, "shared_down")
+    copy = us(k_fs, "allreduce_copy")
+    msg_bytes = N * d * es
+    # ring all-reduce of one [N, d] message over R ranks moves 2 (R-1)/R of
+    # it through each rank: at the bus bandwidth of App. B's accelerator
+    # (400 GB/s) and at the rate of 7 xGMI links of 153 GB/s
+    ring = 2.0 * (R - 1) / R * msg_bytes
+    ar_400 = ring / 400e9 * 1e6
+    ar_links = ring / (7 * 153e9) * 1e6
+    M = float(np.mean(rows))
+    act = float(np.mean(active))
+    bytes_gu = (act * 2 * F * d + M * d + M * F) * es
+    flops_gu = 2.0 * M * d * 2 * F
+    t_gu = us(k_fs, "gate_up") * 1e-6
+    hbm_gbs, tflops = bytes_gu / t_gu / 1e9, flops_gu / t_gu / 1e12
+    mfma_bound = flops_gu / (PEAK_BF16_TFLOPS * 1e12) >= bytes_gu / (PEAK_HBM_GBS * 1e9)
+    roof = ({"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+             "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4)} if mfma_bound else
+            {"bound": "hbm", "achieved": round(hbm_gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+             "frac": round(hbm_gbs / PEAK_HBM_GBS, 4)})
+    roof.update({"kernel": "gathered routed gate/up SwiGLU GEMM", "traffic": None,
+                 "algorithmic_bytes_per_launch": int(bytes_gu),
+                 "algorithmic_flops_per_launch": flops_gu, "local_rows": round(M, 1),
+                 "experts_with_rows": round(act, 2),
+                 "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                 "hbm_frac": round(hbm_gbs / PEAK_HBM_GBS, 4)})
+    rg_copies_ms = args.layers * 2 * us(k_rg, "allreduce_copy") / 1e3
+    model = lambda t_ar: {
+        "allreduce_us": round(t_ar, 2),
+        "regular_ms_per_step": round(ms_rg - rg_copies_ms + args.layers * 2 * t_ar / 1e3, 4),
+        "farskip_ms_per_step": round(ms_fs + args.layers * (max(0.0, t_ar - routed)
+                                                            + max(0.0, t_ar - attention)) / 1e3, 4),
+        "attention_shared_ar_hidden": t_ar <= routed,
+        "routed_ar_hidden": t_ar <= attention}
+    m400, mlinks = model(ar_400), model(ar_links)
+    for m in (m400, mlinks):
+        m["speedup_vs_regular"] = round(m["regular_ms_per_step"] / m["farskip_ms_per_step"], 4)
+    res = {
+        "metric": "replicated-activation FarSkip stacked-layer tokens/sec per GPU "
+                  "(one EP/TP rank: attention and shared-expert blocks, own routed experts)",
+        "value": N / (ms_fs * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_fs, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {args.layers} stacked layers, replicated activations, "
+                               f"rank {r} of EP = TP = {R}; all-reduce stand-in copies on a second "
+                               f"stream", "layers": args.layers, "tokens": N, "hidden": d,
+                   "experts": cfg.n_experts, "top_k": cfg.top_k, "ep_size": R,
+                   "local_rows_per_layer": rows},
+        "serial_ms_per_step": ms_serial,
+        "regular_ms_per_step": ms_rg,
+        "speedup_vs_regular": ms_rg / ms_fs,
+        "roofline": roof,
+        "tab5_windows_per_layer_us": {
+            "layer": round(per_layer, 2), "attention": round(attention, 2),
+            "shared": round(shared, 2), "routed_experts": round(routed, 2),
+            "allreduce_copy": round(copy, 2),
+            "note": "the attention + shared all-reduce hides behind the routed experts, "
+                    "the routed all-reduce behind the next attention"},
+        "allreduce_model": {"message_bytes": msg_bytes, "at_400GBs_bus": m400,
+                            "at_7_xgmi_links": mlinks,
+                            "note": "measured times with each stand-in copy replaced by a ring "
+                                    "all-reduce of the message over R ranks (model, not a "
+                                    "measurement); FarSkip pays only what exceeds its window"},
+        "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()},
+        "kernels_us_regular": {k2: round(v["us_per_launch"], 2) for k2, v in k_rg.items()},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -227,7 +366,11 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="also time the step captured as a HIP graph and replayed")
     ap.add_argument("--layers", type=int, default=0,
-                    help="run this many stacked layers in the two-window schedule and the regular one")
+                    help="run this many stacked layers in the two-window schedule and the regular one "
+                         "(replicated-activation workloads always run stacked layers, 4 by default)")
+    ap.add_argument("--farskip-only", action="store_true",
+                    help="replicated-activation workloads: time only the two-stream FarSkip schedule "
+                         "(for kernel traces)")
     ap.add_argument("--overlap", action="store_true",
                     help="run the next-layer stand-in (d x d linear) between BEGIN and FINISH and "
                          "compare with a serial run")
@@ -247,6 +390,9 @@ def main():
     cfg = CONFIGS[args.config]
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if cfg.ep_mode == "allreduce":
+        args.layers = args.layers or 4
+        return bench_replicated(args, cfg, torch, L)
     if args.layers > 0:
         return bench_layers(args, cfg, torch, L)
     t_setup = time.perf_counter()

@@ -378,9 +378,11 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
 /* Per-kernel timing with HIP events recorded on the launch stream around
  * selected kernels.  fs_profile_read synchronises those events.
  * FS_K_GATE_UP / FS_K_DOWN time the routed experts' passes (and
- * fs_grouped_expert_ffn and fs_grouped_expert_ffn_gathered); FS_K_COMBINE
- * fs_combine_unpack, fs_combine_partial and the block's Combine;
- * FS_K_SHARED_* the shared experts' passes inside fs_moe_block_forward;
+ * fs_grouped_expert_ffn with group_offsets, and
+ * fs_grouped_expert_ffn_gathered); FS_K_COMBINE fs_combine_unpack,
+ * fs_combine_partial and the block's Combine; FS_K_SHARED_* the shared
+ * experts' passes inside fs_moe_block_forward and fs_grouped_expert_ffn
+ * without group_offsets (one group of max_rows rows);
  * FS_K_DISPATCH_COPY / FS_K_COMBINE_COPY the Dispatch and Combine stand-in
  * copies on the stream they run on; FS_K_DENSE fs_dense_linear;
  * FS_K_ALLREDUCE_COPY fs_allreduce_standin. */

@@ -402,9 +402,11 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
   if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden))
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
   NEED(ws, "ws");
+  // one group of max_rows rows (the shared-expert / dense form) is timed
+  // apart from the grouped routed-expert form
   FS_HIP(fs::launch_grouped_ffn(desc->dtype, n_groups, ffn, desc->hidden, in_rows, group_rows,
                                 group_rows, group_offsets, max_rows, w_gate_up, w_down, out_rows, ws,
-                                S(stream), FS_K_GATE_UP),
+                                S(stream), group_offsets ? FS_K_GATE_UP : FS_K_SHARED_GATE_UP),
          "grouped_ffn");
   return FS_OK;
 }

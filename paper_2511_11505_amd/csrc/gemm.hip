@@ -1345,13 +1345,16 @@ constexpr int kBM = 128, kBN = 128, kBK = 64;
 
 // Tile variant of the LDS-ring GEMMs, per pass, from the measured expert
 // shapes: gate/up takes the register-staged 256 x 256 x 64 kernel (8) when
-// the groups average at least 2048 rows (dense, shared-expert-like) and the
-// interleaved 128 x 256 x 64 ring (5) otherwise, where half-empty 256-row
-// tail tiles would waste MFMA work; down takes the interleaved 256 x 256 x 64
-// ring (7) when K < 2816 and the groups average at least 1024 rows, and the
-// 128-row interleaved ring (5) otherwise.
+// the groups average at least 2048 rows (dense, shared-expert-like) and its
+// tiles fill the 256 compute units, and the interleaved 128 x 256 x 64 ring
+// (5) otherwise, where half-empty 256-row tail tiles would waste MFMA work
+// or too few tiles would leave CUs idle (narrow tensor-parallel slices);
+// down takes the interleaved 256 x 256 x 64 ring (7) when K < 2816, the
+// groups average at least 1024 rows and its tiles fill the 256 compute
+// units, and the 128-row interleaved ring (5) otherwise.  nout: output
+// columns of the pass (F for gate/up, d for down).
 // FS_GEMM_TILE / FS_GEMM_TILE_DOWN (0-9) force a variant, for tuning.
-int tile_choice(bool down, int64_t max_rows, int G, int K) {
+int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
   static const int gu_env = [] {
     const char* e = getenv("FS_GEMM_TILE");
     return e ? atoi(e) : -1;
@@ -1360,9 +1363,14 @@ int tile_choice(bool down, int64_t max_rows, int G, int K) {
     const char* e = getenv("FS_GEMM_TILE_DOWN");
     return e ? atoi(e) : -1;
   }();
-  if (down)
-    return dn_env >= 0 ? dn_env : (K < 2816 && max_rows >= 1024 * (int64_t)G ? 7 : 5);
-  return gu_env >= 0 ? gu_env : (max_rows >= 2048 * (int64_t)G ? 8 : 5);
+  if (down) {
+    if (dn_env >= 0) return dn_env;
+    const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 256);
+    return K < 2816 && max_rows >= 1024 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
+  }
+  if (gu_env >= 0) return gu_env;
+  const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 128);
+  return max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 8 : 5;
 }
 
 int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
@@ -1542,11 +1550,11 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
   } else if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     if (profile) prof_begin(pg, s);
-    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d), (const bf16_t*)in, rows_in, goff, G,
+    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d, ffn), (const bf16_t*)in, rows_in, goff, G,
                            max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn, s);
     if (profile) prof_end(pg, s);
     if (profile) prof_begin(pd, s);
-    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn), H, rows_out, goff, G, max_rows,
+    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn, d), H, rows_out, goff, G, max_rows,
                          (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, s);
     if (profile) prof_end(pd, s);
   } else if (dtype == 1) {
@@ -1580,7 +1588,11 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s) {
   if (m <= 0) return hipSuccess;
-  if (dtype == 1) {
+  if (dtype == 1 && n % 256 == 0) {
+    // the LDS-ring kernels as one group of m rows
+    gemm_pass<MODE_DOWN>(tile_choice(true, m, 1, kdim, n), (const bf16_t*)a, nullptr, nullptr, 1,
+                         m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n, s);
+  } else if (dtype == 1) {
     const int64_t g = grid_for(m, 1, kBM, n / kBN);
     gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g, 256, 0, s>>>(
         (const bf16_t*)a, nullptr, nullptr, 1, m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n);

@@ -228,7 +228,8 @@ def test_grouped_ffn_streaming(counts, d, F, gather):
     assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
 
 
-@pytest.mark.parametrize("dtype,m,n,kd", [("f32", 70, 128, 256), ("bf16", 300, 256, 512), ("bf16", 1, 128, 64)])
+@pytest.mark.parametrize("dtype,m,n,kd", [("f32", 70, 128, 256), ("bf16", 300, 256, 512), ("bf16", 1, 128, 64),
+                                         ("bf16", 2049, 768, 640), ("bf16", 333, 640, 512)])
 def test_dense_linear(dtype, m, n, kd):
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     gen = torch.Generator(device=DEV).manual_seed(m)
