@@ -33,9 +33,19 @@ rank runs its own experts on every token; partial sums are all-reduced):
   farskip_ar_stack, regular_ar_stack pinned (R = 1 equals the all-to-all
                                      stacks; conservation; dropped dependency)
 tests/test_oracle_allreduce.py holds those pins.
+
+oracle.fp8 holds the FP8 (E4M3) experts: row quantisation, scaled GEMMs and
+the FP8 SwiGLU expert:
+  e4m3_decode / e4m3_encode ........ pinned (format constants, round trip,
+                                     brute-force nearest with ties to even)
+  quantize_rows, scaled_gemm ....... pinned (amax code, zero rows, error
+                                     bound, hand value)
+  swiglu_fp8 ....................... pinned (lossless quantisation reduces to
+                                     the bf16-rounded SwiGLU)
+tests/test_oracle_fp8.py holds those pins.
 """
 
-from . import allreduce  # noqa: F401
+from . import allreduce, fp8  # noqa: F401
 from .moe import (  # noqa: F401
     ROUTER_SLICE,
     logits_f64,
