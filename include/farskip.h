@@ -90,7 +90,8 @@ typedef enum {
   FS_OP_ROUTER_TOPK = 0,
   FS_OP_DISPATCH_PACK = 1,
   FS_OP_GROUPED_FFN = 2,
-  FS_OP_BLOCK = 3
+  FS_OP_BLOCK = 3,
+  FS_OP_GROUPED_FFN_FP8 = 4
 } fs_op;
 
 /* One MoE block on one EP rank (Section 2.1).  A plain host struct, read
@@ -126,7 +127,9 @@ int32_t fs_abi_version(void);
  *   op = FS_OP_GROUPED_FFN:   fs_grouped_expert_ffn with up to max_rows rows
  *                             and width ffn
  *   op = FS_OP_BLOCK:         fs_moe_block_forward with up to max_rows rows
- *                             landing on local experts (ffn ignored) */
+ *                             landing on local experts (ffn ignored)
+ *   op = FS_OP_GROUPED_FFN_FP8: fs_grouped_expert_ffn_fp8 with up to
+ *                             max_rows rows and width ffn */
 fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_rows,
                             int32_t ffn, size_t* bytes);
 
@@ -241,6 +244,48 @@ fs_status fs_grouped_expert_ffn_gathered(const fs_moe_desc* desc, int32_t n_grou
                                          const int32_t* group_offsets, int64_t max_rows,
                                          const void* w_gate_up, const void* w_down, void* y,
                                          void* ws, size_t ws_bytes, fs_stream stream);
+
+/* FP8 experts (the paper's inference runs use FP8 experts, Section 5.2).
+ * Row-wise OCP FP8 E4M3 quantisation of rows x [rows, cols] (activations:
+ * one row per token or expert row; weights: one row per output channel):
+ * amax = max |x_i|; scale = amax / 448 and inv = 448 / amax, each a
+ * correctly rounded fp32 division; code_i = E4M3(clamp(x_i * inv, +-448))
+ * rounded to nearest, ties to even (x_i * inv one fp32 rounding).  An
+ * all-zero row gets scale 1 and zero codes.  The row stands for
+ * dec(code_i) * scale.
+ *   dtype   FS_F32 or FS_BF16: the type of src
+ *   src     [rows, cols], cols % 16 == 0, 16-byte aligned
+ *   codes   [rows, cols] uint8 out, 16-byte aligned
+ *   scales  [rows] fp32 out */
+fs_status fs_quantize_fp8(int32_t dtype, int64_t rows, int32_t cols, const void* src,
+                          uint8_t* codes, float* scales, fs_stream stream);
+
+/* Grouped SwiGLU expert FFN on FP8 operands: the data flow of
+ * fs_grouped_expert_ffn with x and the weights as E4M3 codes and row
+ * scales (fs_quantize_fp8).  gate and up are
+ *   sum_k dec(x_mk) dec(w_nk) * x_scale[m] * s_gate_up[g][n]
+ * (MFMA with fp32 accumulation); H = SiLU(gate) * up rounded to bf16; H is
+ * quantised per row (as fs_quantize_fp8) inside the workspace; down is the
+ * same scaled product of H and w_down; out rows are bf16.
+ *   x_codes [*, d] uint8, x_scales [*] fp32: rows as in_rows of
+ *           fs_grouped_expert_ffn (gathered through group_rows)
+ *   w_gate_up [n_groups, 2F, d] uint8, s_gate_up [n_groups, 2F] fp32
+ *   w_down [n_groups, d, F] uint8, s_down [n_groups, d] fp32
+ *   out_rows [*, d] bf16 out (scattered through group_rows)
+ * desc->dtype must be FS_BF16; F % 128 == 0 and d % 256 == 0
+ * (FS_ERR_UNSUPPORTED otherwise).  Workspace: FS_OP_GROUPED_FFN_FP8; after
+ * the call it holds, for the M = group_offsets[n_groups] rows in grouped
+ * order, H as bf16 [max_rows, F] at byte 0, its codes [max_rows, F] at
+ * byte a(2 max_rows F) and its scales [max_rows] fp32 at byte
+ * a(2 max_rows F) + a(max_rows F), where a(n) rounds n up to a multiple
+ * of 256. */
+fs_status fs_grouped_expert_ffn_fp8(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                    const uint8_t* x_codes, const float* x_scales,
+                                    const int32_t* group_rows, const int32_t* group_offsets,
+                                    int64_t max_rows, const uint8_t* w_gate_up,
+                                    const float* s_gate_up, const uint8_t* w_down,
+                                    const float* s_down, void* out_rows, void* ws, size_t ws_bytes,
+                                    fs_stream stream);
 
 /* Combine and unpack (Section 2.1, Combine: weighted sum of the returned
  * expert outputs), fused with the deferred residual add of Eq. 7.
@@ -378,8 +423,9 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
 /* Per-kernel timing with HIP events recorded on the launch stream around
  * selected kernels.  fs_profile_read synchronises those events.
  * FS_K_GATE_UP / FS_K_DOWN time the routed experts' passes (and
- * fs_grouped_expert_ffn with group_offsets, and
- * fs_grouped_expert_ffn_gathered); FS_K_COMBINE fs_combine_unpack,
+ * fs_grouped_expert_ffn and fs_grouped_expert_ffn_fp8 with group_offsets,
+ * and fs_grouped_expert_ffn_gathered; for FP8, FS_K_DOWN includes the
+ * quantisation of H); FS_K_COMBINE fs_combine_unpack,
  * fs_combine_partial and the block's Combine; FS_K_SHARED_* the shared
  * experts' passes inside fs_moe_block_forward and fs_grouped_expert_ffn
  * without group_offsets (one group of max_rows rows);

@@ -17,7 +17,7 @@ FS_F32, FS_BF16 = 0, 1
 FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH, FS_PHASE_GATE, FS_PHASE_SHARED, FS_PHASE_EXPERTS,
  FS_PHASE_COMBINE) = range(7)
-FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK = range(4)
+FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK, FS_OP_GROUPED_FFN_FP8 = range(5)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
  FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_COUNT) = range(14)
@@ -65,6 +65,9 @@ _SIGS = {
     "fs_grouped_expert_ffn": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp, _i64,
                                      _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_combine_unpack": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "fs_quantize_fp8": (_i32, [_i32, _i64, _i32, _vp, _vp, _vp, _vp]),
+    "fs_grouped_expert_ffn_fp8": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp, _vp,
+                                         _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_combine_partial": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
     "fs_allreduce_standin": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp]),
     "fs_farskip_residual": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
@@ -209,6 +212,22 @@ def fs_combine_unpack(desc, y_ret, slot_to_row, topk_w, shared_out, routed_out, 
     _check(load().fs_combine_unpack(ctypes.byref(desc), ptr(y_ret), ptr(slot_to_row), ptr(topk_w),
                                     ptr(shared_out), ptr(routed_out), ptr(residual),
                                     stream_handle(stream)))
+
+
+def fs_quantize_fp8(dtype, rows, cols, src, codes, scales, stream=None):
+    _check(load().fs_quantize_fp8(dtype, rows, cols, ptr(src), ptr(codes), ptr(scales),
+                                  stream_handle(stream)))
+
+
+def fs_grouped_expert_ffn_fp8(desc, n_groups, ffn, x_codes, x_scales, group_rows, group_offsets,
+                              max_rows, w_gate_up, s_gate_up, w_down, s_down, out_rows, ws,
+                              stream=None):
+    wp, wb = _ws(ws)
+    _check(load().fs_grouped_expert_ffn_fp8(ctypes.byref(desc), n_groups, ffn, ptr(x_codes),
+                                            ptr(x_scales), ptr(group_rows), ptr(group_offsets),
+                                            max_rows, ptr(w_gate_up), ptr(s_gate_up), ptr(w_down),
+                                            ptr(s_down), ptr(out_rows), wp, wb,
+                                            stream_handle(stream)))
 
 
 def fs_combine_partial(desc, y_local, slot_to_row, rank_offsets, topk_w, partial_out, stream=None):

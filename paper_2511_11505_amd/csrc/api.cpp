@@ -195,6 +195,10 @@ fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_row
       if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
       *bytes = fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden);
       return FS_OK;
+    case FS_OP_GROUPED_FFN_FP8:
+      if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
+      *bytes = fs::ffn_fp8_ws_bytes(max_rows, ffn);
+      return FS_OK;
     case FS_OP_BLOCK: {
       size_t b = router_bytes(desc) + plan_bytes(desc);
       b += fs::ffn_ws_bytes(desc->dtype, max_rows, desc->ffn, desc->hidden);
@@ -382,6 +386,54 @@ fs_status fs_grouped_expert_ffn_gathered(const fs_moe_desc* desc, int32_t n_grou
                                 nullptr, group_offsets, max_rows, w_gate_up, w_down, y, ws,
                                 S(stream), FS_K_GATE_UP),
          "grouped_ffn_gathered");
+  return FS_OK;
+}
+
+fs_status fs_quantize_fp8(int32_t dtype, int64_t rows, int32_t cols, const void* src,
+                          uint8_t* codes, float* scales, fs_stream stream) {
+  if (dtype != FS_F32 && dtype != FS_BF16) return fail(FS_ERR_INVALID, "dtype must be FS_F32 or FS_BF16");
+  if (rows < 0 || cols <= 0) return fail(FS_ERR_INVALID, "rows >= 0 and cols > 0 required");
+  if (cols % 16 != 0) return fail(FS_ERR_UNSUPPORTED, "cols must be a multiple of 16");
+  if (rows == 0) return FS_OK;
+  NEED(src, "src");
+  NEED(codes, "codes");
+  NEED4(scales, "scales");
+  FS_HIP(fs::launch_quantize_fp8(dtype == FS_F32 ? 0 : 1, src, rows, cols, nullptr, codes, scales,
+                                 S(stream)),
+         "quantize_fp8");
+  return FS_OK;
+}
+
+fs_status fs_grouped_expert_ffn_fp8(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                    const uint8_t* x_codes, const float* x_scales,
+                                    const int32_t* group_rows, const int32_t* group_offsets,
+                                    int64_t max_rows, const uint8_t* w_gate_up,
+                                    const float* s_gate_up, const uint8_t* w_down,
+                                    const float* s_down, void* out_rows, void* ws, size_t ws_bytes,
+                                    fs_stream stream) {
+  fs_status st = ffn_checks(desc, n_groups, ffn, group_offsets, max_rows);
+  if (st != FS_OK) return st;
+  if (desc->dtype != FS_BF16) return fail(FS_ERR_UNSUPPORTED, "FP8 experts write bf16 rows (dtype FS_BF16)");
+  if (ffn % 128 != 0 || desc->hidden % 256 != 0)
+    return fail(FS_ERR_UNSUPPORTED, "FP8 experts need ffn % 128 == 0 and hidden % 256 == 0");
+  if (max_rows == 0) return FS_OK;
+  NEED(x_codes, "x_codes");
+  NEED4(x_scales, "x_scales");
+  OPT4(group_rows, "group_rows");
+  OPT4(group_offsets, "group_offsets");
+  NEED(w_gate_up, "w_gate_up");
+  NEED4(s_gate_up, "s_gate_up");
+  NEED(w_down, "w_down");
+  NEED4(s_down, "s_down");
+  NEED(out_rows, "out_rows");
+  if (ws_bytes < fs::ffn_fp8_ws_bytes(max_rows, ffn))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN_FP8)");
+  NEED(ws, "ws");
+  FS_HIP(fs::launch_grouped_ffn_fp8(n_groups, ffn, desc->hidden, x_codes, x_scales, group_rows,
+                                    group_rows, group_offsets, max_rows, w_gate_up, s_gate_up,
+                                    w_down, s_down, out_rows, ws, S(stream),
+                                    group_offsets ? FS_K_GATE_UP : FS_K_SHARED_GATE_UP),
+         "grouped_ffn_fp8");
   return FS_OK;
 }
 

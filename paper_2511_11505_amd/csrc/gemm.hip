@@ -591,22 +591,40 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
 // next block has landed.  A wave issues memory instructions in the shadow of
 // an executing MFMA, so with one wave per SIMD the MFMA pipe stays busy.
 // The grid is persistent (one workgroup per CU).
+//
+// F8: the same kernel on FP8 E4M3 operands with BK = 128 elements, so a
+// staged row is still 128 bytes and the ring, swizzle and DMAs are
+// unchanged.  A K step is one v_mfma_scale_f32_32x32x64_f8f6f4 per tile
+// (unit scales): lane l supplies row l % 32 and the 32 bytes
+// [32 (l / 32), 32 (l / 32) + 32) of the step's 64, read as two 16-byte
+// chunks (any split works as long as A and B use the same one).  A block has
+// two steps of half as many, twice as long MFMAs, so the MFMA time per block
+// equals bf16's for twice the K.  The epilogue multiplies each accumulator by
+// its row's scale sA (indexed like the A rows) and its column's scale sB
+// (per group: 2 NOUT gate/up columns or NOUT down columns).
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
   __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
 }
 
-template <int MODE, int BM, int BN, int BK, int STAGES, int OCC>
+typedef int int32x8 __attribute__((ext_vector_type(8)));
+
+template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false>
 __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
-    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
-    int NOUT, bf16_t* __restrict__ C, int ldc) {
+    const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
+    const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ B, int K, int NOUT,
+    bf16_t* __restrict__ C, int ldc, const float* __restrict__ sA, const float* __restrict__ sB) {
+  using TE = typename std::conditional<F8, uint8_t, bf16_t>::type;
+  using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
   constexpr int NT = 256;
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int ROWB = BK * 2;
-  constexpr int CPR = BK / 8;
+  constexpr int ES = F8 ? 1 : 2;                   // element bytes
+  constexpr int CE = 16 / ES;                      // elements per 16-byte chunk
+  constexpr int ROWB = BK * ES;
+  constexpr int CPR = ROWB / 16;
   constexpr int RPB = 1024 / ROWB;
   constexpr int SWD = 16 / CPR;
   constexpr int STAGE = (BM + BN) * ROWB;
@@ -615,7 +633,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
   constexpr int ECOL = 128;
   constexpr int CST = ECOL + 8;
-  constexpr int KS = BK / 16;                      // K steps per block
+  constexpr int KS = ROWB / (F8 ? 64 : 32);        // K steps per block
   constexpr int NF = TM + TN;                      // fragments per K step
   constexpr int MPS = TM * TN;                     // MFMAs per K step
   // read r of the next step goes out after MFMA read_slot(r) of this one
@@ -625,10 +643,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   // land before the block's last step).
   constexpr int DSTEPS = (STAGES == 2) ? 1 : KS - 1;
   constexpr int DPS = (NLD + DSTEPS - 1) / DSTEPS;  // DMAs per step
+  constexpr int DPQ = (DPS + MPS - 1) / MPS;        // DMAs after one MFMA
   static_assert(STAGES >= 2 && STAGES <= 6, "ring of two to six slots");
   static_assert(NLD * (STAGES - 2) < 64, "vmcnt range");
   static_assert(KS >= 2, "at least two K steps per block");
-  static_assert(DPS <= MPS, "one DMA per MFMA at most");
+  static_assert(DPQ <= 2, "two DMAs per MFMA at most");
+  static_assert(!F8 || BK == 128, "FP8 rows are 128 elements");
   static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
   static_assert(NCOL % ECOL == 0, "epilogue passes");
   static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
@@ -638,6 +658,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   __shared__ int s_goff[kMaxGroups + 1];
   __shared__ int s_tpre[kMaxGroups + 1];
   __shared__ int s_wtot[NT / 64];
+  __shared__ float s_sa[F8 ? BM : 1];              // F8: the tile's row scales
   __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -683,10 +704,10 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     const int nt = (int)(local / Tg), mt = (int)(local % Tg);
     const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
     const int m0 = mt * BM, n0 = nt * NCOL;
-    const bf16_t* Bg = B + (size_t)g * bstride;
+    const TE* Bg = B + (size_t)g * bstride;
 
     // DMA sources: NLD 16-byte chunks per lane per K block
-    const bf16_t* src[NLD];
+    const TE* src[NLD];
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
       const int blk = wave * A_LD + i;
@@ -694,7 +715,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
       if (m >= rows_g) m = rows_g - 1;
       const int grow = row_base + m;
       const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      src[i] = A + sr * K + dchunk(blk) * 8;
+      src[i] = A + sr * K + dchunk(blk) * CE;
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
@@ -705,7 +726,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
       else
         wrow = n0 + r;
-      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
+      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * CE;
     }
     // wave-uniform LDS destinations: ring base + slot + this wave's blocks
     const unsigned ring_lds = lds_addr(ring);
@@ -726,17 +747,26 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
 
-    bf16x8 Fa[NF], Fb[NF];
+    FragT Fa[NF], Fb[NF];
     // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
     // A1..A(TM-1); read r is issued after MFMA read_slot(r) of the step before
-    auto read_one = [&](bf16x8 (&F)[NF], int kt, int ks, int r) {
+    auto read_one = [&](FragT (&F)[NF], int kt, int ks, int r) {
       const unsigned char* slot = ring + (kt % STAGES) * STAGE;
-      const int c = ks * 2 + (lane >> 5);
       const int f = r == 0 ? 0 : (r <= TN ? TM + r - 1 : r - TN);
-      const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
-      F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
+      if constexpr (F8) {
+        const int c = ks * 4 + 2 * (lane >> 5);
+        const int base = f < TM ? aoff[f] : boff[f - TM];
+        const int sw = f < TM ? asw[f] : bsw[f - TM];
+        const int4 lo = *reinterpret_cast<const int4*>(slot + base + ((c ^ sw) << 4));
+        const int4 hi = *reinterpret_cast<const int4*>(slot + base + (((c + 1) ^ sw) << 4));
+        F[f] = int32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      } else {
+        const int c = ks * 2 + (lane >> 5);
+        const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
+        F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
+      }
     };
-    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
+    auto read_step = [&](FragT (&F)[NF], int kt, int ks) {
 #pragma unroll
       for (int r = 0; r < NF; ++r) read_one(F, kt, ks, r);
     };
@@ -751,14 +781,18 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     // MFMA pipe is busy during the barrier.  PF (a compile-time flag) says
     // whether block kt + STAGES - 1 exists, so the main loop carries no
     // per-DMA branch.
-    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks, auto PF) {
+    auto step = [&](FragT (&Fc)[NF], FragT (&Fn)[NF], int kt, int ks, auto PF) {
       constexpr bool pf = decltype(PF)::value;
       const bool more = ks < KS - 1 || kt + 1 < KT;
       const int rkt = ks < KS - 1 ? kt : kt + 1, rks = ks < KS - 1 ? ks + 1 : 0;
 #pragma unroll
       for (int q = 0; q < MPS; ++q) {
         const int i = q / TN, jn = q % TN;
-        acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
+        if constexpr (F8)
+          acc[i][jn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Fc[i], Fc[TM + jn], acc[i][jn],
+                                                                       0, 0, 0, 127, 0, 127);
+        else
+          acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
         if (q == 0 && ks == KS - 1 && (pf || kt + 1 < KT)) {
           // block kt+1 has landed once at most the DMAs of the blocks issued
@@ -775,10 +809,14 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
         for (int r = 0; r < NF; ++r)
           if (q == read_slot(r) && more) read_one(Fn, rkt, rks, r);
-        if (ks < DSTEPS && q < DPS) {
-          const int d = ks * DPS + q;
-          if (d < NLD) {
-            if constexpr (pf) dma_one(d, kt + STAGES - 1);
+        if (ks < DSTEPS) {
+#pragma unroll
+          for (int u = 0; u < DPQ; ++u) {
+            const int dl = q * DPQ + u;
+            const int d = ks * DPS + dl;
+            if (dl < DPS && d < NLD) {
+              if constexpr (pf) dma_one(d, kt + STAGES - 1);
+            }
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -813,7 +851,28 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     for (int kt = 0; kt < kt_pf; ++kt) run_block(kt, std::true_type{});
     for (int kt = kt_pf < 0 ? 0 : kt_pf; kt < KT; ++kt) run_block(kt, std::false_type{});
 
-    // Epilogue (as in the kernel above).
+    // Epilogue (as in the kernel above); F8 applies the row and column scales.
+    float sbg[F8 ? TN : 1];
+    if constexpr (F8) {
+      for (int r = tid; r < BM; r += NT) {
+        int m = m0 + r;
+        if (m >= rows_g) m = rows_g - 1;
+        const int grow = row_base + m;
+        const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+        s_sa[r] = sA[sr];
+      }
+      const float* sBg = sB + (size_t)g * ((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT);
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn) {
+        int col;
+        if (MODE == MODE_GATEUP)
+          col = (jn < TN / 2) ? n0 + wn * (WTN / 2) + jn * 32
+                              : NOUT + n0 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+        else
+          col = n0 + wn * WTN + jn * 32;
+        sbg[jn] = sBg[col + (lane & 31)];
+      }
+    }
     bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
     constexpr int PASSES = NCOL / ECOL;
 #pragma unroll
@@ -825,10 +884,15 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const float sa = F8 ? s_sa[r] : 1.f;
             if (MODE == MODE_GATEUP) {
 #pragma unroll
               for (int jn = 0; jn < TN / 2; ++jn) {
-                const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+                float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+                if constexpr (F8) {
+                  gt = gt * sa * sbg[jn];
+                  up = up * sa * sbg[jn + TN / 2];
+                }
                 const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
                 Cs[r * CST + col] = f2bf(swiglu_bf16_epi(gt, up));
               }
@@ -836,7 +900,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
               for (int jn = 0; jn < TN; ++jn) {
                 const int col = jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(acc[i][jn][v]);
+                float y = acc[i][jn][v];
+                if constexpr (F8) y = y * sa * sbg[jn];
+                Cs[r * CST + col] = f2bf(y);
               }
             }
           }
@@ -1412,7 +1478,16 @@ void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, OCC);
   gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>
-      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr);
+}
+template <int MODE, int BM, int BN, int ST>
+void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
+               const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc, const float* sA,
+               const float* sB, hipStream_t s) {
+  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
+  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
+  gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>
+      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB);
 }
 template <int MODE, int BM, int BN, int BK>
 void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
@@ -1489,6 +1564,48 @@ bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
   const int64_t ring_tiles =
       (int64_t)G * std::max<int64_t>(1, cdiv64(max_rows, (int64_t)128 * G)) * std::max(1, ffn / 128);
   return mode == 2 || ring_tiles < 256;
+}
+
+// One FP8 GEMM pass: the bf16 variant rule picks the tile height (the
+// 256-row tiles of variants 7 and 8 -> 256 x 256, otherwise 128 x 256).
+template <int MODE>
+void gemm_pass_f8(int v, const uint8_t* A, const int32_t* rows, const int32_t* goff, int G,
+                  int64_t m_total, const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc,
+                  const float* sA, const float* sB, hipStream_t s) {
+  if (v == 7 || v == 8)
+    run_il_f8<MODE, 256, 256, 2>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
+  else
+    run_il_f8<MODE, 128, 256, 3>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
+}
+
+size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn) {
+  const size_t h = (size_t)max_rows * ffn;
+  return (h * 2 + 255) / 256 * 256 + (h + 255) / 256 * 256 + ((size_t)max_rows * 4 + 255) / 256 * 256;
+}
+
+hipError_t launch_grouped_ffn_fp8(int G, int ffn, int d, const uint8_t* x, const float* x_scale,
+                                  const int32_t* rows_in, const int32_t* rows_out,
+                                  const int32_t* goff, int64_t max_rows, const uint8_t* w_gate_up,
+                                  const float* s_gate_up, const uint8_t* w_down,
+                                  const float* s_down, void* out, void* ws, hipStream_t s,
+                                  int prof_gate_up) {
+  if (max_rows <= 0) return hipSuccess;
+  const bool profile = prof_gate_up >= 0;
+  const size_t h = (size_t)max_rows * ffn;
+  bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+  uint8_t* Hq = reinterpret_cast<uint8_t*>(ws) + (h * 2 + 255) / 256 * 256;
+  float* Hs = reinterpret_cast<float*>(Hq + (h + 255) / 256 * 256);
+  if (profile) prof_begin(prof_gate_up, s);
+  gemm_pass_f8<MODE_GATEUP>(tile_choice(false, max_rows, G, d, ffn), x, rows_in, goff, G,
+                            max_rows, w_gate_up, d, ffn, H, ffn, x_scale, s_gate_up, s);
+  if (profile) prof_end(prof_gate_up, s);
+  if (profile) prof_begin(prof_gate_up + 1, s);
+  hipError_t e = launch_quantize_fp8(1, H, max_rows, ffn, goff ? goff + G : nullptr, Hq, Hs, s);
+  if (e != hipSuccess) return e;
+  gemm_pass_f8<MODE_DOWN>(tile_choice(true, max_rows, G, ffn, d), Hq, rows_out, goff, G, max_rows,
+                          w_down, ffn, d, static_cast<bf16_t*>(out), d, Hs, s_down, s);
+  if (profile) prof_end(prof_gate_up + 1, s);
+  return hipGetLastError();
 }
 
 size_t ffn_ws_bytes(int dtype, int64_t max_rows, int ffn, int d) {

@@ -47,6 +47,19 @@ hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const voi
                               const int32_t* goff, int64_t max_rows,
                               const void* w_gate_up, const void* w_down, void* out, void* ws,
                               hipStream_t s, int prof_gate_up);  // profile id of gate/up, down = +1; -1: none
+// FP8 (E4M3) experts: row quantisation, and the grouped SwiGLU FFN on
+// quantised operands (x and the weights by row scales; H is quantised per
+// row between the passes, inside the workspace).
+hipError_t launch_quantize_fp8(int dtype, const void* src, int64_t rows, int cols,
+                               const int32_t* row_count, uint8_t* codes, float* scales,
+                               hipStream_t s);
+size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn);
+hipError_t launch_grouped_ffn_fp8(int n_groups, int ffn, int d, const uint8_t* x,
+                                  const float* x_scale, const int32_t* rows_in,
+                                  const int32_t* rows_out, const int32_t* goff, int64_t max_rows,
+                                  const uint8_t* w_gate_up, const float* s_gate_up,
+                                  const uint8_t* w_down, const float* s_down, void* out,
+                                  void* ws, hipStream_t s, int prof_gate_up);
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s);
 

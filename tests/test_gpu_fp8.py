@@ -1,0 +1,133 @@
+"""GPU parity of the FP8 (E4M3) experts against oracle.fp8.
+
+Row quantisation is compared bit for bit (codes and scales).  The FP8
+SwiGLU FFN is compared step by step on the same quantised operands:
+  * H (bf16) against the oracle's fp64 gate/up product of the same x and
+    weight codes, then rounded like the kernel: only fp32 accumulation and
+    the bf16 rounding of H separate them;
+  * the codes and scales of H, bit for bit against the oracle's quantiser
+    applied to the GPU's H (H is the quantiser's input, so the decision is
+    taken on the same value);
+  * the output against the oracle's fp64 down product of those H codes;
+and end to end against the unquantised SwiGLU, within the error FP8
+brings (3 mantissa bits on both operands of both GEMMs).
+
+Tolerance for the step comparisons: max relative error (floored at the
+rms) 1e-2, between the bf16 output rounding (2^-9 relative) and the block
+tolerance; measured values are printed."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import fp8 as of8
+from paper_2511_11505_amd import _lib as L
+from tests._util import f64, rel_err
+from workloads import CONFIGS
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+DEV = "cuda"
+STEP_TOL = 1e-2
+
+
+def quantize(t):
+    rows, cols = t.shape
+    codes = torch.empty((rows, cols), dtype=torch.uint8, device=DEV)
+    scales = torch.empty((rows,), dtype=torch.float32, device=DEV)
+    L.fs_quantize_fp8(L.FS_F32 if t.dtype == torch.float32 else L.FS_BF16, rows, cols, t, codes, scales)
+    return codes, scales
+
+
+def np_u8(t):
+    return t.cpu().numpy().astype(np.uint8)
+
+
+@pytest.mark.parametrize("dtype,rows,cols", [("bf16", 37, 512), ("f32", 21, 256), ("bf16", 1, 7168),
+                                             ("bf16", 300, 2048)])
+def test_quantize_rows_bit_exact(dtype, rows, cols):
+    g = torch.Generator(device=DEV).manual_seed(rows * 7 + cols)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    x = torch.randn((rows, cols), generator=g, device=DEV)
+    # rows of very different magnitudes, an all-zero row, negative zeros,
+    # exact fp8 midpoints after scaling, and a row whose amax is negative
+    x *= torch.exp(torch.linspace(-8, 8, rows, device=DEV))[:, None]
+    if rows > 3:
+        x[1] = 0
+        x[2, : cols // 2] = -0.0
+        x[3] = torch.tensor([448.0, -232.0, 240.0, 13.0, -0.5], device=DEV).repeat(cols // 5 + 1)[:cols]
+        x[3, 5] = -448.0
+    x = x.to(tdt)
+    codes, scales = quantize(x)
+    torch.cuda.synchronize()
+    want_c, want_s = of8.quantize_rows(x.float().cpu().numpy())
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), want_s.view(np.uint32))
+    assert np.array_equal(np_u8(codes), want_c)
+
+
+def ffn_case(G, F, d, counts, gather, seed):
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    M = int(sum(counts))
+    n_src = max(M, 1) + 5
+    x = torch.randn((n_src, d), generator=g, device=DEV).to(torch.bfloat16)
+    wgu = (0.02 * torch.randn((G, 2 * F, d), generator=g, device=DEV)).to(torch.bfloat16)
+    wdn = (0.02 * torch.randn((G, d, F), generator=g, device=DEV)).to(torch.bfloat16)
+    goff = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32, device=DEV)
+    rows = None
+    if gather:
+        rows = torch.randperm(n_src, generator=g, device=DEV)[:M].to(torch.int32)
+    return x, wgu, wdn, goff, rows, M
+
+
+@pytest.mark.parametrize("counts,F,d,gather", [([0, 1, 64, 65, 130], 256, 512, True),
+                                               ([37], 128, 256, False),
+                                               ([3, 0, 5, 300, 1, 0, 2, 7], 384, 768, True),
+                                               ([513, 700], 512, 1024, False)])
+def test_grouped_ffn_fp8_steps(counts, F, d, gather):
+    G = len(counts)
+    x, wgu, wdn, goff, rows, M = ffn_case(G, F, d, counts, gather, seed=sum(counts) + F)
+    cfg = CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16")
+    desc = L.make_desc(cfg)
+    xq, xs = quantize(x)
+    gq, gs = quantize(wgu.reshape(G * 2 * F, d))
+    dq, ds = quantize(wdn.reshape(G * d, F))
+    out = torch.full((x.shape[0], d), float("nan"), dtype=torch.bfloat16, device=DEV)
+    ws_bytes = L.fs_workspace_size(desc, L.FS_OP_GROUPED_FFN_FP8, M, F)
+    ws = torch.empty((ws_bytes,), dtype=torch.uint8, device=DEV)
+    L.fs_grouped_expert_ffn_fp8(desc, G, F, xq, xs, rows, goff, M, gq.reshape(G, 2 * F, d), gs,
+                                dq.reshape(G, d, F), ds, out, ws)
+    torch.cuda.synchronize()
+    a = lambda n: (n + 255) // 256 * 256
+    H = ws[: M * F * 2].view(torch.bfloat16).reshape(M, F)
+    Hq = ws[a(2 * M * F): a(2 * M * F) + M * F].reshape(M, F)
+    Hs = ws[a(2 * M * F) + a(M * F): a(2 * M * F) + a(M * F) + 4 * M].view(torch.float32)
+    xq_n, xs_n = np_u8(xq), xs.cpu().numpy()
+    gq_n, gs_n = np_u8(gq).reshape(G, 2 * F, d), gs.cpu().numpy().reshape(G, 2 * F)
+    dq_n, ds_n = np_u8(dq).reshape(G, d, F), ds.cpu().numpy().reshape(G, d)
+    src = np.arange(M) if rows is None else rows.cpu().numpy()
+    goff_n = goff.cpu().numpy()
+    H_n, Hq_n, Hs_n, out_n = f64(H), np_u8(Hq), Hs.cpu().numpy(), f64(out)
+    errs = []
+    for e in range(G):
+        r0, r1 = goff_n[e], goff_n[e + 1]
+        if r1 == r0:
+            continue
+        sel = src[r0:r1]
+        h_want = of8.swiglu_fp8_hidden(xq_n[sel], xs_n[sel], gq_n[e], gs_n[e])
+        errs.append(rel_err(H_n[r0:r1], h_want))
+        c_want, s_want = of8.quantize_rows(H_n[r0:r1])
+        assert np.array_equal(Hq_n[r0:r1], c_want)
+        assert np.array_equal(Hs_n[r0:r1].view(np.uint32), s_want.view(np.uint32))
+        y_want = of8.scaled_gemm(Hq_n[r0:r1], Hs_n[r0:r1], dq_n[e], ds_n[e])
+        errs.append(rel_err(out_n[sel], y_want))
+        # end to end against the unquantised expert: the FP8 error
+        ref = oracle.swiglu(f64(x[torch.from_numpy(sel).to(DEV)]), f64(wgu[e]), f64(wdn[e]))
+        d_rms = np.sqrt(np.mean((out_n[sel] - ref) ** 2)) / np.sqrt(np.mean(ref ** 2))
+        assert d_rms <= 0.08, d_rms
+    print("max step errors", max(errs))
+    assert max(errs) <= STEP_TOL
+    # rows of x that no group reads keep their NaN fill only where out is not written
+    if rows is not None:
+        untouched = np.setdiff1d(np.arange(x.shape[0]), src)
+        assert np.all(np.isnan(out_n[untouched]))
