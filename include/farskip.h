@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 3
+#define FS_ABI_VERSION 4
 
 typedef enum {
   FS_OK = 0,
@@ -91,7 +91,8 @@ typedef enum {
   FS_OP_DISPATCH_PACK = 1,
   FS_OP_GROUPED_FFN = 2,
   FS_OP_BLOCK = 3,
-  FS_OP_GROUPED_FFN_FP8 = 4
+  FS_OP_GROUPED_FFN_FP8 = 4,
+  FS_OP_BLOCK_FP8 = 5
 } fs_op;
 
 /* One MoE block on one EP rank (Section 2.1).  A plain host struct, read
@@ -129,7 +130,9 @@ int32_t fs_abi_version(void);
  *   op = FS_OP_BLOCK:         fs_moe_block_forward with up to max_rows rows
  *                             landing on local experts (ffn ignored)
  *   op = FS_OP_GROUPED_FFN_FP8: fs_grouped_expert_ffn_fp8 with up to
- *                             max_rows rows and width ffn */
+ *                             max_rows rows and width ffn
+ *   op = FS_OP_BLOCK_FP8:     fs_moe_block_forward with FP8 routed and
+ *                             shared experts (enough for either alone) */
 fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_rows,
                             int32_t ffn, size_t* bytes);
 
@@ -341,6 +344,19 @@ typedef struct {
   const void* w_down;     /* [E/R, d, F] */
   const void* ws_gate_up; /* NULL when S = 0 */
   const void* ws_down;
+  /* FP8 experts (fs_quantize_fp8 codes and row scales; bf16 blocks only).
+   * When w_gate_up_fp8 is given the routed experts run in FP8
+   * (fs_grouped_expert_ffn_fp8 on the received rows, quantised per row
+   * first) and w_gate_up / w_down are not read; likewise ws_gate_up_fp8
+   * for the shared experts.  Dispatch and Combine stay bf16. */
+  const uint8_t* w_gate_up_fp8;  /* [E/R, 2F, d] or NULL */
+  const float* s_gate_up;        /* [E/R, 2F] */
+  const uint8_t* w_down_fp8;     /* [E/R, d, F] */
+  const float* s_down;           /* [E/R, d] */
+  const uint8_t* ws_gate_up_fp8; /* [2 S F_s, d] or NULL */
+  const float* ss_gate_up;       /* [2 S F_s] */
+  const uint8_t* ws_down_fp8;    /* [d, S F_s] */
+  const float* ss_down;          /* [d] */
 } fs_moe_weights;
 
 /* Caller-owned buffers of one block (device memory). */
@@ -431,7 +447,8 @@ fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, con
  * without group_offsets (one group of max_rows rows);
  * FS_K_DISPATCH_COPY / FS_K_COMBINE_COPY the Dispatch and Combine stand-in
  * copies on the stream they run on; FS_K_DENSE fs_dense_linear;
- * FS_K_ALLREDUCE_COPY fs_allreduce_standin. */
+ * FS_K_ALLREDUCE_COPY fs_allreduce_standin; FS_K_QUANTIZE the activation
+ * quantisation of the block's FP8 experts. */
 typedef enum {
   FS_K_ROUTER = 0,
   FS_K_TOPK = 1,
@@ -446,7 +463,8 @@ typedef enum {
   FS_K_DENSE = 10,
   FS_K_COMBINE_COPY = 11,
   FS_K_ALLREDUCE_COPY = 12,
-  FS_K_COUNT = 13
+  FS_K_QUANTIZE = 13,
+  FS_K_COUNT = 14
 } fs_kernel_id;
 fs_status fs_profile_enable(int32_t on);
 fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);

@@ -17,11 +17,12 @@ FS_F32, FS_BF16 = 0, 1
 FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH, FS_PHASE_GATE, FS_PHASE_SHARED, FS_PHASE_EXPERTS,
  FS_PHASE_COMBINE) = range(7)
-FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK, FS_OP_GROUPED_FFN_FP8 = range(5)
+(FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK, FS_OP_GROUPED_FFN_FP8,
+ FS_OP_BLOCK_FP8) = range(6)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
- FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_COUNT) = range(14)
-FS_ABI_VERSION = 3
+ FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_QUANTIZE, FS_K_COUNT) = range(15)
+FS_ABI_VERSION = 4
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -42,7 +43,10 @@ class fs_moe_desc(ctypes.Structure):
 
 class fs_moe_weights(ctypes.Structure):
     _fields_ = [("w_router", _vp), ("sel_bias", _vp), ("w_gate_up", _vp), ("w_down", _vp),
-                ("ws_gate_up", _vp), ("ws_down", _vp)]
+                ("ws_gate_up", _vp), ("ws_down", _vp),
+                ("w_gate_up_fp8", _vp), ("s_gate_up", _vp), ("w_down_fp8", _vp), ("s_down", _vp),
+                ("ws_gate_up_fp8", _vp), ("ss_gate_up", _vp), ("ws_down_fp8", _vp),
+                ("ss_down", _vp)]
 
 
 class fs_block_buffers(ctypes.Structure):

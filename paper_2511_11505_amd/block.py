@@ -6,6 +6,8 @@
 other EP ranks would have sent: their routing and packed send buffers land
 in their receive slots, their counts in the source-count rows, and the
 Combine return rows of other ranks' experts in this rank's return slot.
+With ``fp8`` the expert weights are quantised once, at construction, by the
+library's row quantiser, and the block runs those experts in FP8.
 All arithmetic runs in the library's kernels; torch only allocates memory.
 """
 
@@ -19,10 +21,26 @@ def _dt(cfg):
     return torch.float32 if cfg.dtype == "f32" else torch.bfloat16
 
 
+def _quantize(w):
+    """E4M3 codes and per-row scales of a weight tensor [..., cols] (rows
+    are its output channels), through the library's quantiser."""
+    rows, cols = w.numel() // w.shape[-1], w.shape[-1]
+    codes = torch.empty(w.shape, dtype=torch.uint8, device=w.device)
+    scales = torch.empty(w.shape[:-1], dtype=torch.float32, device=w.device)
+    L.fs_quantize_fp8(L.FS_F32 if w.dtype == torch.float32 else L.FS_BF16, rows, cols,
+                      w.contiguous(), codes, scales)
+    return codes, scales
+
+
 class MoEBlock:
     def __init__(self, cfg, w_router, sel_bias, w_gate_up, w_down, ws_gate_up=None, ws_down=None,
-                 max_recv_rows=None, device="cuda", with_comm=True, with_return=False):
+                 max_recv_rows=None, device="cuda", with_comm=True, with_return=False, fp8=None):
+        """fp8: None (bf16 experts), "routed" (FP8 routed experts) or "all"
+        (FP8 routed and shared experts)."""
+        if fp8 not in (None, "routed", "all"):
+            raise ValueError(f"fp8 must be None, 'routed' or 'all', not {fp8!r}")
         self.cfg = cfg
+        self.fp8 = fp8
         self.desc = make_desc(cfg)
         R, N, d, E, k = cfg.ep_size, cfg.n_tokens, cfg.hidden, cfg.n_experts, cfg.top_k
         cap = N * k
@@ -48,11 +66,21 @@ class MoEBlock:
             shared_out=torch.empty((N, d), dtype=dt, device=dev) if cfg.n_shared > 0 else None,
             ret=torch.empty((cap, d), dtype=dt, device=dev) if with_return else None,
         )
+        q = dict()
+        if fp8:
+            q["w_gate_up_fp8"], q["s_gate_up"] = _quantize(w_gate_up)
+            q["w_down_fp8"], q["s_down"] = _quantize(w_down)
+            if fp8 == "all" and ws_gate_up is not None:
+                q["ws_gate_up_fp8"], q["ss_gate_up"] = _quantize(ws_gate_up)
+                q["ws_down_fp8"], q["ss_down"] = _quantize(ws_down)
+        self.fp8_weights = q
         self.weights_keep = (w_router, sel_bias, w_gate_up, w_down, ws_gate_up, ws_down)
         self.weights = L.fs_moe_weights(L.ptr(w_router), L.ptr(sel_bias), L.ptr(w_gate_up),
-                                        L.ptr(w_down), L.ptr(ws_gate_up), L.ptr(ws_down))
+                                        L.ptr(w_down), L.ptr(ws_gate_up), L.ptr(ws_down),
+                                        *[L.ptr(q.get(n)) for n, _ in L.fs_moe_weights._fields_[6:]])
         self.buffers = L.fs_block_buffers(*[L.ptr(self.t[n]) for n, _ in L.fs_block_buffers._fields_])
-        ws_bytes = L.fs_workspace_size(self.desc, L.FS_OP_BLOCK, self.max_recv_rows)
+        self.ws_op = L.FS_OP_BLOCK_FP8 if fp8 else L.FS_OP_BLOCK
+        ws_bytes = L.fs_workspace_size(self.desc, self.ws_op, self.max_recv_rows)
         self.ws = torch.empty((max(ws_bytes, 256),), dtype=torch.uint8, device=dev)
         self.sync = L.fs_block_sync_create()
 
@@ -71,7 +99,7 @@ class MoEBlock:
         m = int(m)
         if m != self.max_recv_rows:
             self.max_recv_rows = m
-            ws_bytes = L.fs_workspace_size(self.desc, L.FS_OP_BLOCK, m)
+            ws_bytes = L.fs_workspace_size(self.desc, self.ws_op, m)
             if ws_bytes > self.ws.numel():
                 self.ws = torch.empty((ws_bytes,), dtype=torch.uint8, device=self.ws.device)
 

@@ -145,6 +145,20 @@ size_t router_bytes(const fs_moe_desc* d) {
 }
 size_t plan_bytes(const fs_moe_desc* d) { return align256(fs::plan_ws_bytes(d->n_tokens, d->n_experts)); }
 
+// Workspace of one FFN inside the block: bf16, or FP8 (row codes and scales
+// of the input, then the FP8 FFN's own workspace).
+size_t block_ffn_bytes(const fs_moe_desc* d, int64_t rows, int ffn, bool fp8) {
+  if (!fp8) return align256(fs::ffn_ws_bytes(d->dtype, rows, ffn, d->hidden));
+  return align256((size_t)rows * d->hidden) + align256((size_t)rows * 4) +
+         align256(fs::ffn_fp8_ws_bytes(rows, ffn));
+}
+
+size_t block_bytes(const fs_moe_desc* d, int64_t max_rows, bool fp8_routed, bool fp8_shared) {
+  size_t b = router_bytes(d) + plan_bytes(d) + block_ffn_bytes(d, max_rows, d->ffn, fp8_routed);
+  if (d->n_shared > 0) b += block_ffn_bytes(d, d->n_tokens, d->n_shared * d->ffn_shared, fp8_shared);
+  return b;
+}
+
 }  // namespace
 
 namespace fs {
@@ -199,12 +213,11 @@ fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_row
       if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
       *bytes = fs::ffn_fp8_ws_bytes(max_rows, ffn);
       return FS_OK;
-    case FS_OP_BLOCK: {
-      size_t b = router_bytes(desc) + plan_bytes(desc);
-      b += fs::ffn_ws_bytes(desc->dtype, max_rows, desc->ffn, desc->hidden);
-      if (desc->n_shared > 0)
-        b += fs::ffn_ws_bytes(desc->dtype, desc->n_tokens, desc->n_shared * desc->ffn_shared, desc->hidden);
-      *bytes = b;
+    case FS_OP_BLOCK: *bytes = block_bytes(desc, max_rows, false, false); return FS_OK;
+    case FS_OP_BLOCK_FP8: {
+      size_t a = block_bytes(desc, max_rows, true, true), b = block_bytes(desc, max_rows, true, false);
+      size_t c = block_bytes(desc, max_rows, false, true);
+      *bytes = a > b ? (a > c ? a : c) : (b > c ? b : c);
       return FS_OK;
     }
     default: return fail(FS_ERR_INVALID, "unknown op");
@@ -622,10 +635,21 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   const bool do_shared = phase == FS_PHASE_ALL || phase == FS_PHASE_BEGIN || phase == FS_PHASE_SHARED;
   const bool do_experts = phase == FS_PHASE_ALL || phase == FS_PHASE_FINISH || phase == FS_PHASE_EXPERTS;
   const bool do_combine = phase == FS_PHASE_ALL || phase == FS_PHASE_FINISH || phase == FS_PHASE_COMBINE;
-  size_t need = 0;
-  st = fs_workspace_size(desc, FS_OP_BLOCK, max_recv_rows, 0, &need);
-  if (st != FS_OK) return st;
-  if (ws_bytes < need) return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_BLOCK)");
+  const bool fp8_routed = wt->w_gate_up_fp8 != nullptr;
+  const bool fp8_shared = desc->n_shared > 0 && wt->ws_gate_up_fp8 != nullptr;
+  if (fp8_routed || fp8_shared) {
+    if (desc->dtype != FS_BF16) return fail(FS_ERR_UNSUPPORTED, "FP8 experts need a bf16 block");
+    if (D % 256 != 0) return fail(FS_ERR_UNSUPPORTED, "FP8 experts need hidden % 256 == 0");
+    if (fp8_routed && desc->ffn % 128 != 0)
+      return fail(FS_ERR_UNSUPPORTED, "FP8 routed experts need ffn % 128 == 0");
+    if (fp8_shared && (desc->n_shared * desc->ffn_shared) % 128 != 0)
+      return fail(FS_ERR_UNSUPPORTED, "FP8 shared experts need n_shared * ffn_shared % 128 == 0");
+  }
+  const size_t need = block_bytes(desc, max_recv_rows, fp8_routed, fp8_shared);
+  if (ws_bytes < need)
+    return fail(FS_ERR_WORKSPACE, fp8_routed || fp8_shared
+                                      ? "workspace smaller than fs_workspace_size(FS_OP_BLOCK_FP8)"
+                                      : "workspace smaller than fs_workspace_size(FS_OP_BLOCK)");
   if (N == 0) return FS_OK;
   NEED(ws, "ws");
   NEED(residual_in, "residual_in");
@@ -641,14 +665,28 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   if (do_shared) {
     NEED(partial_out, "partial_out");
     if (desc->n_shared > 0) {
-      NEED(wt->ws_gate_up, "weights->ws_gate_up");
-      NEED(wt->ws_down, "weights->ws_down");
+      if (fp8_shared) {
+        NEED(wt->ws_gate_up_fp8, "weights->ws_gate_up_fp8");
+        NEED4(wt->ss_gate_up, "weights->ss_gate_up");
+        NEED(wt->ws_down_fp8, "weights->ws_down_fp8");
+        NEED4(wt->ss_down, "weights->ss_down");
+      } else {
+        NEED(wt->ws_gate_up, "weights->ws_gate_up");
+        NEED(wt->ws_down, "weights->ws_down");
+      }
       NEED(b->shared_out, "buffers->shared_out");
     }
   }
   if (do_experts) {
-    NEED(wt->w_gate_up, "weights->w_gate_up");
-    NEED(wt->w_down, "weights->w_down");
+    if (fp8_routed) {
+      NEED(wt->w_gate_up_fp8, "weights->w_gate_up_fp8");
+      NEED4(wt->s_gate_up, "weights->s_gate_up");
+      NEED(wt->w_down_fp8, "weights->w_down_fp8");
+      NEED4(wt->s_down, "weights->s_down");
+    } else {
+      NEED(wt->w_gate_up, "weights->w_gate_up");
+      NEED(wt->w_down, "weights->w_down");
+    }
     NEED(b->y, "buffers->y");
     if (R > 1) {
       NEED4(b->group_rows, "buffers->group_rows");
@@ -675,10 +713,17 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   Carve c{reinterpret_cast<char*>(ws)};
   void* ws_router = c.take(router_bytes(desc));
   void* ws_plan = c.take(plan_bytes(desc));
-  void* ws_ffn = c.take(fs::ffn_ws_bytes(desc->dtype, max_recv_rows, desc->ffn, D));
-  void* ws_shared = desc->n_shared > 0
-                        ? c.take(fs::ffn_ws_bytes(desc->dtype, N, desc->n_shared * desc->ffn_shared, D))
-                        : nullptr;
+  char* ws_ffn = static_cast<char*>(c.take(block_ffn_bytes(desc, max_recv_rows, desc->ffn, fp8_routed)));
+  char* ws_shared =
+      desc->n_shared > 0
+          ? static_cast<char*>(c.take(block_ffn_bytes(desc, N, desc->n_shared * desc->ffn_shared, fp8_shared)))
+          : nullptr;
+  // FP8 parts of an FFN region: input codes, their scales, the FFN workspace
+  auto fp8_parts = [&](char* base, int64_t rows, uint8_t** codes, float** scales, void** rest) {
+    *codes = reinterpret_cast<uint8_t*>(base);
+    *scales = reinterpret_cast<float*>(base + align256((size_t)rows * D));
+    *rest = base + align256((size_t)rows * D) + align256((size_t)rows * 4);
+  };
   int32_t* my_counts = b->src_counts + (size_t)r * E;
   int32_t* my_offsets = b->src_offsets + (size_t)r * (E + 1);
   char* recv_slot = b->recv ? reinterpret_cast<char*>(b->recv) + (size_t)r * slot_bytes : nullptr;
@@ -712,7 +757,20 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   }
   if (do_shared) {
     // shared experts on o_{k-1}, then the next layer's partial input
-    if (desc->n_shared > 0) {
+    if (fp8_shared) {
+      uint8_t* xq;
+      float* xs;
+      void* rest;
+      fp8_parts(ws_shared, N, &xq, &xs, &rest);
+      fs::prof_begin(FS_K_QUANTIZE, sc);
+      FS_HIP(fs::launch_quantize_fp8(1, residual_in, N, D, nullptr, xq, xs, sc), "quantize_fp8");
+      fs::prof_end(FS_K_QUANTIZE, sc);
+      FS_HIP(fs::launch_grouped_ffn_fp8(1, desc->n_shared * desc->ffn_shared, D, xq, xs, nullptr,
+                                        nullptr, nullptr, N, wt->ws_gate_up_fp8, wt->ss_gate_up,
+                                        wt->ws_down_fp8, wt->ss_down, b->shared_out, rest, sc,
+                                        FS_K_SHARED_GATE_UP),
+             "shared_ffn_fp8");
+    } else if (desc->n_shared > 0) {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, 1, desc->n_shared * desc->ffn_shared, D,
                                     residual_in, nullptr, nullptr, nullptr, N, wt->ws_gate_up, wt->ws_down,
                                     b->shared_out, ws_shared, sc, FS_K_SHARED_GATE_UP),
@@ -743,10 +801,27 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       rows = nullptr;
       goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
     }
-    FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, rows, goff,
-                                  max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,
-                                  FS_K_GATE_UP),
-           "grouped_ffn");
+    if (fp8_routed) {
+      // the rows landing on local experts, quantised in grouped order; the
+      // outputs go back to their receive rows
+      uint8_t* xq;
+      float* xs;
+      void* rest;
+      fp8_parts(ws_ffn, max_recv_rows, &xq, &xs, &rest);
+      fs::prof_begin(FS_K_QUANTIZE, sc);
+      FS_HIP(fs::launch_quantize_fp8(1, in_rows, max_recv_rows, D, goff + E_loc, xq, xs, sc, rows),
+             "quantize_fp8");
+      fs::prof_end(FS_K_QUANTIZE, sc);
+      FS_HIP(fs::launch_grouped_ffn_fp8(E_loc, desc->ffn, D, xq, xs, nullptr, rows, goff,
+                                        max_recv_rows, wt->w_gate_up_fp8, wt->s_gate_up,
+                                        wt->w_down_fp8, wt->s_down, b->y, rest, sc, FS_K_GATE_UP),
+             "grouped_ffn_fp8");
+    } else {
+      FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, rows, goff,
+                                    max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,
+                                    FS_K_GATE_UP),
+             "grouped_ffn");
+    }
     // Combine stand-in: slot r of y (the rows this rank's tokens get back)
     // into ret, on the comm stream, else in order on compute
     if (b->ret) {

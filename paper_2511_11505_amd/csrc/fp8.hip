@@ -9,9 +9,10 @@
 // all-zero row gets scale 1 and zero codes.  The row then stands for
 // dec(code_i) * scale.
 //
-// One workgroup per row (grid-stride): a pass for amax over 16-byte
-// vectors, a block reduction, and a pass that converts and stores 8 or 4
-// codes per thread.
+// Rows may be gathered (output row i from source row gather[i]) and
+// bounded by a device row count.  One workgroup per row (grid-stride): a
+// pass for amax over 16-byte vectors, a block reduction, and a pass that
+// converts and stores 8 or 4 codes per thread.
 
 #include "common.hpp"
 #include "internal.hpp"
@@ -41,6 +42,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void quantize_fp8_kernel(const T* __restrict__ src, int64_t rows,
                                                            int cols,
                                                            const int32_t* __restrict__ row_count,
+                                                           const int32_t* __restrict__ gather,
                                                            uint8_t* __restrict__ codes,
                                                            float* __restrict__ scales) {
   __shared__ float red[4];
@@ -52,7 +54,7 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const T* __restrict__
   }
   const int nv = cols / V;
   for (int64_t r = blockIdx.x; r < n; r += gridDim.x) {
-    const T* row = src + r * cols;
+    const T* row = src + (gather ? (int64_t)gather[r] : r) * cols;
     float m = 0.f;
     for (int i = threadIdx.x; i < nv; i += 256) {
       Vec16<T> v;
@@ -90,15 +92,15 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const T* __restrict__
 
 hipError_t launch_quantize_fp8(int dtype, const void* src, int64_t rows, int cols,
                                const int32_t* row_count, uint8_t* codes, float* scales,
-                               hipStream_t s) {
+                               hipStream_t s, const int32_t* gather) {
   if (rows <= 0) return hipSuccess;
   const unsigned grid = (unsigned)(rows < 65536 ? rows : 65536);
   if (dtype == 0)
     quantize_fp8_kernel<float><<<grid, 256, 0, s>>>((const float*)src, rows, cols, row_count,
-                                                    codes, scales);
+                                                    gather, codes, scales);
   else
     quantize_fp8_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)src, rows, cols, row_count,
-                                                     codes, scales);
+                                                     gather, codes, scales);
   return hipGetLastError();
 }
 

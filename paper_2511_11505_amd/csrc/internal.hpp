@@ -50,9 +50,11 @@ hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const voi
 // FP8 (E4M3) experts: row quantisation, and the grouped SwiGLU FFN on
 // quantised operands (x and the weights by row scales; H is quantised per
 // row between the passes, inside the workspace).
+// Row i of the output quantises source row gather[i] (or row i) for
+// i < min(*row_count, rows) (or rows).
 hipError_t launch_quantize_fp8(int dtype, const void* src, int64_t rows, int cols,
                                const int32_t* row_count, uint8_t* codes, float* scales,
-                               hipStream_t s);
+                               hipStream_t s, const int32_t* gather = nullptr);
 size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn);
 hipError_t launch_grouped_ffn_fp8(int n_groups, int ffn, int d, const uint8_t* x,
                                   const float* x_scale, const int32_t* rows_in,

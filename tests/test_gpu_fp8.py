@@ -131,3 +131,92 @@ def test_grouped_ffn_fp8_steps(counts, F, d, gather):
     if rows is not None:
         untouched = np.setdiff1d(np.arange(x.shape[0]), src)
         assert np.all(np.isnan(out_n[untouched]))
+
+
+# ---------------------------------------------------------------- FP8 experts inside the block
+FP8_BLOCKS = {
+    "dsv2lite_f8s": CONFIGS["dsv2lite"].scaled(n_tokens=333, hidden=512, ffn=256, ffn_shared=128,
+                                               name="dsv2lite_f8s"),
+    "dsv3_prefill_f8s": CONFIGS["dsv3_prefill"].scaled(n_tokens=150, hidden=512, ffn=256,
+                                                       ffn_shared=256, ep_rank=3,
+                                                       name="dsv3_prefill_f8s"),
+    "dsv3_decode_f8s": CONFIGS["dsv3_decode"].scaled(n_tokens=9, hidden=512, ffn=256,
+                                                     ffn_shared=256, name="dsv3_decode_f8s"),
+}
+
+
+@pytest.mark.parametrize("name", list(FP8_BLOCKS))
+def test_block_fp8_chain(name):
+    # The block with FP8 experts: (a) gate, plan and pack equal the bf16
+    # block's bit for bit; (b) the local expert rows and the shared output
+    # equal the standalone FP8 FFN on the same inputs bit for bit (that FFN
+    # is checked step by step against the oracle above); (c) Combine and the
+    # residual add against the oracle on the GPU's rows; (d) the FP8 block
+    # stays within FP8's error of the bf16 block.
+    from paper_2511_11505_amd import MoEBlock, prepare_remote_sources
+    from tests._util import TOL
+    from workloads import make_workload
+    from workloads.generate import merge_shared
+
+    cfg = FP8_BLOCKS[name]
+    wl = make_workload(cfg, DEV)
+    sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
+    comm = torch.cuda.Stream()
+    blocks, outs = {}, {}
+    for mode in (None, "all"):
+        blk = MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn,
+                       device=DEV, fp8=mode)
+        if cfg.ep_size > 1:
+            blk.set_max_recv_rows(prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias,
+                                                         wl.y_remote))
+        x = wl.x
+        partial, out = torch.empty_like(x), x.clone()
+        blk.begin(x, partial, comm=comm)
+        blk.finish(x, out, comm=comm)
+        torch.cuda.synchronize()
+        blocks[mode], outs[mode] = blk, (out, partial)
+    b16, b8 = blocks[None], blocks["all"]
+    R, r, cap, E_loc = cfg.ep_size, cfg.ep_rank, b8.cap, cfg.n_local
+    for key in ("topk_ids", "topk_w", "slot_to_row", "row_to_slot", "src_counts", "src_offsets",
+                "rank_offsets", "send"):
+        assert torch.equal(b16.t[key], b8.t[key]), key
+    if R > 1:
+        assert torch.equal(b16.t["group_offsets"], b8.t["group_offsets"])
+        m = int(b8.t["group_offsets"][E_loc].item())
+        assert torch.equal(b16.t["group_rows"][:m], b8.t["group_rows"][:m])   # entries past M unwritten
+        in_rows, rows, goff = b8.t["recv"], b8.t["group_rows"], b8.t["group_offsets"]
+    else:
+        in_rows, rows, goff = b8.t["send"], None, b8.t["src_offsets"][r]
+    M = int(goff[E_loc].item())
+    q = b8.fp8_weights
+    xq, xs = quantize(in_rows)
+    y_ref = torch.full_like(b8.t["y"], float("nan"))
+    desc = b8.desc
+    ws = torch.empty((L.fs_workspace_size(desc, L.FS_OP_GROUPED_FFN_FP8, b8.max_recv_rows, cfg.ffn),),
+                     dtype=torch.uint8, device=DEV)
+    L.fs_grouped_expert_ffn_fp8(desc, E_loc, cfg.ffn, xq, xs, rows, goff, b8.max_recv_rows,
+                                q["w_gate_up_fp8"], q["s_gate_up"], q["w_down_fp8"], q["s_down"],
+                                y_ref, ws)
+    x = wl.x
+    xq_s, xs_s = quantize(x)
+    sh_ref = torch.empty_like(x)
+    W = cfg.n_shared * cfg.ffn_shared
+    ws_s = torch.empty((L.fs_workspace_size(desc, L.FS_OP_GROUPED_FFN_FP8, cfg.n_tokens, W),),
+                       dtype=torch.uint8, device=DEV)
+    L.fs_grouped_expert_ffn_fp8(desc, 1, W, xq_s, xs_s, None, None, cfg.n_tokens,
+                                q["ws_gate_up_fp8"], q["ss_gate_up"], q["ws_down_fp8"], q["ss_down"],
+                                sh_ref, ws_s)
+    torch.cuda.synchronize()
+    idx = rows[:M].long() if rows is not None else torch.arange(M, device=DEV)
+    assert torch.equal(b8.t["y"][idx], y_ref[idx])
+    assert torch.equal(b8.t["shared_out"], sh_ref)
+    out8, partial8 = outs["all"]
+    s2r = b8.t["slot_to_row"].cpu().numpy()
+    routed = oracle.combine(f64(b8.y_ret()), s2r, f64(b8.t["topk_w"]))
+    assert rel_err(out8, f64(x) + routed) <= TOL["bf16"]
+    assert rel_err(partial8, f64(x) + f64(b8.t["shared_out"])) <= TOL["bf16"]
+    rms = lambda a: np.sqrt(np.mean(a * a))
+    for a8, a16 in ((b8.t["y"][idx], b16.t["y"][idx]), (b8.t["shared_out"], b16.t["shared_out"])):
+        assert rms(f64(a8) - f64(a16)) <= 0.08 * rms(f64(a16))
+    for blk in blocks.values():
+        blk.close()
