@@ -24,6 +24,7 @@ if ROOT not in sys.path:
 
 METRIC = "MoE-block tokens/sec per GPU; grouped-GEMM % bf16 MFMA peak; permute % HBM"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_F32_VALU_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 
@@ -50,7 +51,8 @@ def measured_traffic(cfg_name):
 
 
 KERNEL_NAMES = ("router", "topk", "plan", "pack", "gate_up", "down", "combine", "shared_gate_up",
-                "shared_down", "dispatch_copy", "next_layer", "combine_copy", "allreduce_copy")
+                "shared_down", "dispatch_copy", "next_layer", "combine_copy", "allreduce_copy",
+                "quantize")
 
 
 def kernel_table(L):
@@ -64,27 +66,47 @@ def kernel_table(L):
     return out
 
 
-def step_roofs(cfg, M, active):
+def ffn_roofs(rows, groups, d, F, es, fp8):
+    """(bytes, flops, MFMA peak) of an FFN's gate/up and down passes.  FP8:
+    1-byte weights and input codes, H written in bf16, and the down pass
+    includes H's quantisation (read H, write its codes) before reading the
+    codes."""
+    if not fp8:
+        mm = (PEAK_BF16_TFLOPS if es == 2 else PEAK_F32_VALU_TFLOPS) * 1e12
+        return ((groups * 2 * F * d + rows * d + rows * F) * es, 2.0 * rows * d * 2 * F, mm), \
+               ((groups * d * F + rows * F + rows * d) * es, 2.0 * rows * d * F, mm)
+    mm = PEAK_FP8_TFLOPS * 1e12
+    return (groups * 2 * F * d + rows * d + 2 * rows * F + 4 * rows, 2.0 * rows * d * 2 * F, mm), \
+           (groups * d * F + 2 * rows * F + 2 * rows * F + 4 * rows + 2 * rows * d,
+            2.0 * rows * d * F, mm)
+
+
+def step_roofs(cfg, M, active, fp8_routed=False, fp8_shared=False):
     """Algorithmic (bytes, flops, roof time in us) of each step of one pass,
-    at HBM 8 TB/s, bf16 MFMA 2.5 PFLOP/s and fp32 vector 157.3 TFLOP/s."""
+    at HBM 8 TB/s, bf16 MFMA 2.5 PFLOP/s, fp8 MFMA 5.0 PFLOP/s and fp32
+    vector 157.3 TFLOP/s."""
     es = cfg.elem_bytes
     N, d, k, E, F = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts, cfg.ffn
     SF = cfg.n_shared * cfg.ffn_shared
-    mm = (PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS) * 1e12
     hbm, valu = PEAK_HBM_GBS * 1e9, PEAK_F32_VALU_TFLOPS * 1e12
+    gu, dn = ffn_roofs(M, active, d, F, es, fp8_routed)
     steps = {
         "router": (N * d * es + E * d * es + N * E * 4, 2.0 * N * d * E, valu),
         "topk": (N * E * 4 + N * k * 8, 0.0, valu),
         "plan": (12 * N * k, 0.0, valu),
         "pack": (N * d * es + N * k * d * es + 4 * N * k, 0.0, valu),
-        "gate_up": ((active * 2 * F * d + M * d + M * F) * es, 2.0 * M * d * 2 * F, mm),
-        "down": ((active * d * F + M * F + M * d) * es, 2.0 * M * d * F, mm),
+        "gate_up": gu,
+        "down": dn,
         "combine": (N * k * d * es + 8 * N * k + 2 * N * d * es, 0.0, valu),
     }
+    if fp8_routed:
+        steps["quantize"] = (M * d * es + M * d + 4 * M, 0.0, valu)
     if SF:
-        steps["shared_gate_up"] = ((2 * SF * d + N * d + N * SF) * es, 2.0 * N * d * 2 * SF, mm)
-        steps["shared_down"] = ((d * SF + N * SF + N * d) * es, 2.0 * N * d * SF, mm)
+        steps["shared_gate_up"], steps["shared_down"] = ffn_roofs(N, 1, d, SF, es, fp8_shared)
         steps["partial"] = (3 * N * d * es, 0.0, valu)
+        if fp8_shared:
+            b, f, p = steps["quantize"] if "quantize" in steps else (0, 0.0, valu)
+            steps["quantize"] = (b + N * d * es + N * d + 4 * N, f, p)
     return {k2: (b, f, 1e6 * max(b / hbm, f / peak)) for k2, (b, f, peak) in steps.items()}
 
 
@@ -368,6 +390,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0,
                     help="run this many stacked layers in the two-window schedule and the regular one "
                          "(replicated-activation workloads always run stacked layers, 4 by default)")
+    ap.add_argument("--fp8", choices=("routed", "all"), default=None,
+                    help="run the routed (or routed and shared) experts in FP8 E4M3")
     ap.add_argument("--farskip-only", action="store_true",
                     help="replicated-activation workloads: time only the two-stream FarSkip schedule "
                          "(for kernel traces)")
@@ -400,7 +424,8 @@ def main():
     sh_gu = sh_dn = None
     if cfg.n_shared > 0:
         sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
-    blk = fs.MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=dev)
+    blk = fs.MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=dev,
+                      fp8=args.fp8)
     M = cfg.cap
     if cfg.ep_size > 1:
         M = fs.prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias, wl.y_remote)
@@ -492,9 +517,12 @@ def main():
     lo = cfg.ep_rank * cfg.n_local
     rows_per_expert = blk.t["src_counts"][:, lo:lo + cfg.n_local].sum(0)
     active = int((rows_per_expert > 0).sum().item())
-    roofs = step_roofs(cfg, M, active)
+    fp8_routed, fp8_shared = args.fp8 is not None, args.fp8 == "all" and cfg.n_shared > 0
+    roofs = step_roofs(cfg, M, active, fp8_routed, fp8_shared)
     us = lambda name: kernels[name]["us_per_launch"] if name in kernels else None
     peak_f = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS
+    if fp8_routed:
+        peak_f = PEAK_FP8_TFLOPS
 
     # roofline of the dominant kernel, the routed gate/up SwiGLU GEMM: its
     # algorithmic work is 2 M d 2F flops and (active experts' gate/up weights
@@ -509,9 +537,10 @@ def main():
             bound = "mfma" if cfg.dtype == "bf16" else "alu"
         else:
             achieved, peak, unit, bound = bytes_gu / t / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
-        roof = {"bound": bound, "kernel": "gate_up SwiGLU grouped GEMM",
+        roof = {"bound": bound, "kernel": ("FP8 " if fp8_routed else "") + "gate_up SwiGLU grouped GEMM",
                 "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": measured_traffic(cfg.name),
+                "frac": round(achieved / peak, 4),
+                "traffic": None if fp8_routed else measured_traffic(cfg.name),
                 "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "algorithmic_flops_per_launch": flops_gu,
                 "algorithmic_bytes_per_launch": bytes_gu, "experts_with_rows": active,
@@ -527,8 +556,10 @@ def main():
             t = (us(gu_k) + us(dn_k)) * 1e-6
             b = roofs[gu_k][0] + roofs[dn_k][0]
             f = roofs[gu_k][1] + roofs[dn_k][1]
+            p_ffn = PEAK_FP8_TFLOPS if (fp8_routed if name == "routed" else fp8_shared) else \
+                (PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_VALU_TFLOPS)
             ffn[name] = {"us": round(t * 1e6, 2), "tflops": round(f / t / 1e12, 2),
-                         "mfma_frac": round(f / t / 1e12 / peak_f, 4),
+                         "mfma_frac": round(f / t / 1e12 / p_ffn, 4),
                          "hbm_gbs": round(b / t / 1e9, 1), "hbm_frac": round(b / t / 1e9 / PEAK_HBM_GBS, 4)}
     # permute kernels and the router against their roofs (algorithmic bytes;
     # the router against max(bytes / HBM, flops / fp32 vector peak))
@@ -566,13 +597,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": cfg.dtype,
+        "dtype": (f"fp8_e4m3 {'routed and shared' if fp8_shared else 'routed'} experts, "
+                  f"{cfg.dtype} elsewhere") if fp8_routed else cfg.dtype,
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: FarSkip MoE block forward, {N} tokens, d {d}, {E} experts "
                                f"top-{k} {cfg.score}, FFN {cfg.ffn}, {cfg.n_shared} shared, EP rank "
                                f"{cfg.ep_rank} of {cfg.ep_size}, {cfg.dtype}"
                                + (", with the next-layer stand-in between BEGIN and FINISH"
-                                  if args.overlap else ""),
+                                  if args.overlap else "")
+                               + (f", FP8 E4M3 experts ({args.fp8})" if fp8_routed else ""),
                    "tokens": N, "hidden": d, "experts": E, "top_k": k, "ffn": cfg.ffn,
                    "shared": cfg.n_shared, "ep_size": cfg.ep_size, "rows_local_experts": M,
                    "second_stream": comm is not None, "next_layer": bool(args.overlap)},
@@ -588,7 +621,10 @@ def main():
         res["overlap"] = overlap
     if graph is not None:
         res["graph"] = graph
-    if not args.no_cpu_baseline:
+    if fp8_routed:
+        res["grouped_gemm_frac_bf16_peak"] = None
+        res["grouped_gemm_frac_fp8_peak"] = None if roof is None else roof["mfma_frac"]
+    if not args.no_cpu_baseline and not fp8_routed:
         try:
             res["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_sample)
         except Exception as e:  # report, do not hide the GPU number

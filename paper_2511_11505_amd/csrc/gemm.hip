@@ -1566,13 +1566,16 @@ bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
   return mode == 2 || ring_tiles < 256;
 }
 
-// One FP8 GEMM pass: the bf16 variant rule picks the tile height (the
-// 256-row tiles of variants 7 and 8 -> 256 x 256, otherwise 128 x 256).
+// One FP8 GEMM pass, 128 x 256 tiles except where the bf16 rule takes the
+// dense register-staged variant (8, gate/up over groups of at least 2048
+// rows that fill the CUs): there 256 x 256.  Measured on the routed and
+// dense expert shapes, 256-row FP8 tiles lose everywhere else (the routed
+// down pass of the 32-expert 7168-wide prefill: 817 against 760 us).
 template <int MODE>
 void gemm_pass_f8(int v, const uint8_t* A, const int32_t* rows, const int32_t* goff, int G,
                   int64_t m_total, const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc,
                   const float* sA, const float* sB, hipStream_t s) {
-  if (v == 7 || v == 8)
+  if (v == 8)
     run_il_f8<MODE, 256, 256, 2>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
   else
     run_il_f8<MODE, 128, 256, 3>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
