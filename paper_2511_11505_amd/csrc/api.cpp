@@ -101,16 +101,28 @@ fs_status check_desc(const fs_moe_desc* d) {
 hipStream_t S(fs_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
 // ---------------------------------------------------------------- profiling
+// A timing window per (kernel id, stream).  Kernels launched on the stream
+// while its window is open (fs::launch_k) record the window's events from
+// their dispatch packets: the first kernel's start and every kernel's end,
+// so the window measures kernel time from the first start to the last end,
+// without the launch latency before the first kernel.  A window with no
+// kernel launch (a copy) falls back to events recorded on the stream.
 struct ProfState {
   std::mutex mu;
   bool on = false;
+  struct Window {
+    int kernel;
+    hipStream_t s;
+    hipEvent_t a, b, k0;  // stream-recorded start, end, first kernel start
+    bool kern;
+  };
   struct Rec {
     int kernel;
-    hipEvent_t a, b;
+    hipEvent_t a, b, spare;
   };
-  std::vector<Rec> open;         // recorded, not yet read
+  std::vector<Window> windows;   // open
+  std::vector<Rec> open;         // closed, not yet read
   std::vector<hipEvent_t> pool;  // reusable events
-  hipEvent_t pending[FS_K_COUNT] = {};
   double total_ms[FS_K_COUNT] = {};
   int64_t count[FS_K_COUNT] = {};
 };
@@ -166,16 +178,43 @@ void prof_begin(int kernel, hipStream_t s) {
   ProfState& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
   if (!p.on) return;
-  hipEvent_t e = take_event(p);
-  if (e && hipEventRecord(e, s) == hipSuccess) p.pending[kernel] = e;
+  hipEvent_t a = take_event(p), b = take_event(p), k0 = take_event(p);
+  if (!a || !b || !k0 || hipEventRecord(a, s) != hipSuccess) {
+    for (hipEvent_t e : {a, b, k0})
+      if (e) p.pool.push_back(e);
+    return;
+  }
+  p.windows.push_back({kernel, s, a, b, k0, false});
+}
+void prof_kernel_events(hipStream_t s, hipEvent_t* start, hipEvent_t* stop) {
+  *start = *stop = nullptr;
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  if (!p.on) return;
+  for (auto it = p.windows.rbegin(); it != p.windows.rend(); ++it) {
+    if (it->s != s) continue;
+    *start = it->kern ? nullptr : it->k0;
+    *stop = it->b;
+    it->kern = true;
+    return;
+  }
 }
 void prof_end(int kernel, hipStream_t s) {
   ProfState& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
-  if (!p.on || !p.pending[kernel]) return;
-  hipEvent_t e = take_event(p);
-  if (e && hipEventRecord(e, s) == hipSuccess) p.open.push_back({kernel, p.pending[kernel], e});
-  p.pending[kernel] = nullptr;
+  for (auto it = p.windows.begin(); it != p.windows.end(); ++it) {
+    if (it->kernel != kernel || it->s != s) continue;
+    const ProfState::Window w = *it;
+    p.windows.erase(it);
+    if (w.kern) {
+      p.open.push_back({kernel, w.k0, w.b, w.a});
+    } else if (hipEventRecord(w.b, s) == hipSuccess) {
+      p.open.push_back({kernel, w.a, w.b, w.k0});
+    } else {
+      for (hipEvent_t e : {w.a, w.b, w.k0}) p.pool.push_back(e);
+    }
+    return;
+  }
 }
 }  // namespace fs
 
@@ -879,6 +918,7 @@ fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches) {
     p.count[rec.kernel] += 1;
     p.pool.push_back(rec.a);
     p.pool.push_back(rec.b);
+    p.pool.push_back(rec.spare);
   }
   p.open.clear();
   if (total_ms) *total_ms = p.total_ms[kernel];
@@ -893,8 +933,14 @@ fs_status fs_profile_reset(void) {
     (void)hipEventSynchronize(rec.b);
     p.pool.push_back(rec.a);
     p.pool.push_back(rec.b);
+    p.pool.push_back(rec.spare);
   }
   p.open.clear();
+  for (auto& w : p.windows) {
+    (void)hipEventSynchronize(w.a);
+    for (hipEvent_t e : {w.a, w.b, w.k0}) p.pool.push_back(e);
+  }
+  p.windows.clear();
   for (int k = 0; k < FS_K_COUNT; ++k) {
     p.total_ms[k] = 0;
     p.count[k] = 0;

@@ -119,7 +119,9 @@ __global__ __launch_bounds__(64) void plan_rank_kernel(const int32_t* __restrict
 // Each lane moves one 16-byte chunk of one token row: it reads the chunk
 // once and writes it to the token's k send rows.  Waves are laid out
 // (token, 64-chunk block), so short batches still fill the machine.
-template <typename T>
+// KC > 0 fixes k at compile time (all k row indices are read before the
+// stores); KC = 0 loops over any k.
+template <typename T, int KC>
 __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ x,
                                                    const int32_t* __restrict__ slot_to_row, int N,
                                                    int k, int d, T* __restrict__ send) {
@@ -130,6 +132,15 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ x,
   const int c = (int)(wave % nb) * 64 + (threadIdx.x & 63);
   if (t >= N || c >= nch) return;
   const uint4 v = reinterpret_cast<const uint4*>(x + (size_t)t * d)[c];
+  if constexpr (KC > 0) {
+    int rw[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) rw[j] = slot_to_row[(size_t)t * KC + j];
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+      if (rw[j] >= 0) reinterpret_cast<uint4*>(send + (size_t)rw[j] * d)[c] = v;
+    return;
+  }
   for (int j = 0; j < k; ++j) {
     const int row = slot_to_row[(size_t)t * k + j];
     if (row >= 0) reinterpret_cast<uint4*>(send + (size_t)row * d)[c] = v;
@@ -199,10 +210,10 @@ hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* 
   uint64_t* bits = reinterpret_cast<uint64_t*>(ws);
   int32_t* hist = reinterpret_cast<int32_t*>(bits + (size_t)n_tiles * E);
   int32_t* tile_base = hist + (size_t)n_tiles * E;
-  plan_hist_kernel<<<n_tiles, 64, E * sizeof(uint64_t), s>>>(ids, N, k, E, bits, hist);
-  plan_scan_kernel<<<1, 512, 0, s>>>(hist, n_tiles, E, R, tile_base, counts, offsets,
+  launch_k(plan_hist_kernel, n_tiles, 64, E * sizeof(uint64_t), s, ids, N, k, E, bits, hist);
+  launch_k(plan_scan_kernel, 1, 512, 0, s, hist, n_tiles, E, R, tile_base, counts, offsets,
                                      rank_offsets);
-  plan_rank_kernel<<<n_tiles, 64, 0, s>>>(ids, N, k, E, bits, tile_base, offsets, slot_to_row,
+  launch_k(plan_rank_kernel, n_tiles, 64, 0, s, ids, N, k, E, bits, tile_base, offsets, slot_to_row,
                                           row_to_slot);
   return hipGetLastError();
 }
@@ -211,11 +222,24 @@ hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int
                        void* send, hipStream_t s) {
   const int64_t nb = ((int64_t)d * (dtype == 0 ? 4 : 2) / 16 + 63) / 64;
   dim3 grid((unsigned)((N * nb + 3) / 4));
-  if (dtype == 0)
-    pack_kernel<float><<<grid, 256, 0, s>>>((const float*)x, slot_to_row, N, k, d, (float*)send);
-  else
-    pack_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)x, slot_to_row, N, k, d,
-                                             (bf16_t*)send);
+#define FS_PACK(T, KC) \
+  launch_k(pack_kernel<T, KC>, grid, 256, 0, s, (const T*)x, slot_to_row, N, k, d, (T*)send)
+#define FS_PACK_T(T)                 \
+  switch (k) {                       \
+    case 1: FS_PACK(T, 1); break;    \
+    case 2: FS_PACK(T, 2); break;    \
+    case 4: FS_PACK(T, 4); break;    \
+    case 6: FS_PACK(T, 6); break;    \
+    case 8: FS_PACK(T, 8); break;    \
+    default: FS_PACK(T, 0); break;   \
+  }
+  if (dtype == 0) {
+    FS_PACK_T(float);
+  } else {
+    FS_PACK_T(bf16_t);
+  }
+#undef FS_PACK_T
+#undef FS_PACK
   return hipGetLastError();
 }
 
@@ -224,7 +248,7 @@ hipError_t launch_local_rows(const int32_t* offsets, const int32_t* rank_offsets
                              int32_t* local_tokens, int32_t* local_offsets, hipStream_t s) {
   const int E_loc = E / R;
   const int64_t rows = (int64_t)N * k, n = rows > E_loc + 1 ? rows : E_loc + 1;
-  local_rows_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+  launch_k(local_rows_kernel, (unsigned)((n + 255) / 256), 256, 0, s,
       offsets, rank_offsets, row_to_slot, k, E_loc, r, local_tokens, local_offsets);
   return hipGetLastError();
 }
@@ -232,7 +256,7 @@ hipError_t launch_local_rows(const int32_t* offsets, const int32_t* rank_offsets
 hipError_t launch_receive_rows(const int32_t* src_counts, const int32_t* src_offsets, int R,
                                int E, int r, int64_t cap, int32_t* group_rows,
                                int32_t* group_offsets, hipStream_t s) {
-  receive_rows_kernel<<<E / R, 256, 0, s>>>(src_counts, src_offsets, R, E, r, cap, group_rows,
+  launch_k(receive_rows_kernel, E / R, 256, 0, s, src_counts, src_offsets, R, E, r, cap, group_rows,
                                             group_offsets);
   return hipGetLastError();
 }

@@ -17,7 +17,10 @@ namespace {
 
 // Each lane handles one 16-byte chunk of one token row; waves are laid out
 // (token, 64-chunk block) so that short batches still fill the machine.
-template <typename T, bool LOCAL>
+// KC > 0 fixes k at compile time: the k row indices and weights, then the k
+// row chunks and the residual chunk are all requested before the first add,
+// so a lane has k + 1 loads in flight; KC = 0 handles any k with a loop.
+template <typename T, bool LOCAL, int KC>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
                                                       const int32_t* __restrict__ slot_to_row,
                                                       const float* __restrict__ topk_w,
@@ -41,6 +44,47 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
   if (LOCAL) {
     lo = row_range[0];
     hi = row_range[1];
+  }
+  if constexpr (KC > 0) {
+    int rw[KC];
+    float wj[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+      rw[j] = slot_to_row[(size_t)t * KC + j];
+      wj[j] = topk_w[(size_t)t * KC + j];
+      if (rw[j] >= 0 && LOCAL) rw[j] = (rw[j] < lo || rw[j] >= hi) ? -1 : rw[j] - lo;
+    }
+    Vec16<T> v[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+      if (rw[j] >= 0) v[j].raw = ld16(y + (size_t)rw[j] * d + (size_t)c * V);
+    Vec16<T> rv;
+    if (residual) rv.raw = ld16(residual + off);
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+      if (rw[j] >= 0) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(wj[j], v[j].get(i), acc[i]);
+      }
+    if (shared_out) {
+      Vec16<T> sv;
+      sv.raw = ld16(shared_out + off);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += sv.get(i);
+    }
+    if (routed_out) {
+      Vec16<T> o;
+#pragma unroll
+      for (int i = 0; i < V; ++i) o.set(i, acc[i]);
+      st16(routed_out + off, o.raw);
+    }
+    if (residual) {
+      Vec16<T> o;
+#pragma unroll
+      for (int i = 0; i < V; ++i) o.set(i, rv.get(i) + acc[i]);
+      st16(residual + off, o.raw);
+    }
+    return;
   }
   for (int j = 0; j < k; ++j) {
     int row = slot_to_row[(size_t)t * k + j];
@@ -105,10 +149,21 @@ hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_r
                           hipStream_t s) {
   const int64_t nb = ((int64_t)d / (dtype == 0 ? 4 : 8) + 63) / 64;
   dim3 grid((unsigned)((N * nb + 3) / 4));
-#define FS_COMBINE(T, L)                                                                    \
-  combine_kernel<T, L><<<grid, 256, 0, s>>>((const T*)y_ret, slot_to_row, topk_w,          \
-                                            (const T*)shared_out, (T*)routed_out,          \
-                                            (T*)residual, row_range, N, k, d)
+#define FS_COMBINE_K(T, L, KC)                                                              \
+  launch_k(combine_kernel<T, L, KC>, grid, 256, 0, s, (const T*)y_ret, slot_to_row, topk_w,      \
+                                                (const T*)shared_out, (T*)routed_out,      \
+                                                (T*)residual, row_range, N, k, d)
+#define FS_COMBINE(T, L)                    \
+  do {                                      \
+    switch (k) {                            \
+      case 1: FS_COMBINE_K(T, L, 1); break; \
+      case 2: FS_COMBINE_K(T, L, 2); break; \
+      case 4: FS_COMBINE_K(T, L, 4); break; \
+      case 6: FS_COMBINE_K(T, L, 6); break; \
+      case 8: FS_COMBINE_K(T, L, 8); break; \
+      default: FS_COMBINE_K(T, L, 0); break; \
+    }                                       \
+  } while (0)
   if (dtype == 0) {
     if (row_range) FS_COMBINE(float, true);
     else FS_COMBINE(float, false);
@@ -117,6 +172,7 @@ hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_r
     else FS_COMBINE(bf16_t, false);
   }
 #undef FS_COMBINE
+#undef FS_COMBINE_K
   return hipGetLastError();
 }
 
@@ -128,10 +184,10 @@ hipError_t launch_residual(int dtype, void* out, const void* a, const void* b, c
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
   if (dtype == 0)
-    residual_kernel<float><<<(int)blocks, 256, 0, s>>>((float*)out, (const float*)a,
+    launch_k(residual_kernel<float>, (int)blocks, 256, 0, s, (float*)out, (const float*)a,
                                                        (const float*)b, (const float*)c, n_vec);
   else
-    residual_kernel<bf16_t><<<(int)blocks, 256, 0, s>>>((bf16_t*)out, (const bf16_t*)a,
+    launch_k(residual_kernel<bf16_t>, (int)blocks, 256, 0, s, (bf16_t*)out, (const bf16_t*)a,
                                                         (const bf16_t*)b, (const bf16_t*)c,
                                                         n_vec);
   return hipGetLastError();

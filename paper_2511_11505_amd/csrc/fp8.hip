@@ -96,10 +96,11 @@ hipError_t launch_quantize_fp8(int dtype, const void* src, int64_t rows, int col
   if (rows <= 0) return hipSuccess;
   const unsigned grid = (unsigned)(rows < 65536 ? rows : 65536);
   if (dtype == 0)
-    quantize_fp8_kernel<float><<<grid, 256, 0, s>>>((const float*)src, rows, cols, row_count,
+    launch_k(quantize_fp8_kernel<float>, grid, 256, 0, s, (const float*)src, rows, cols, row_count,
                                                     gather, codes, scales);
   else
-    quantize_fp8_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)src, rows, cols, row_count,
+    launch_k(quantize_fp8_kernel<bf16_t>, grid, 256, 0, s,
+        (const bf16_t*)src, rows, cols, row_count,
                                                      gather, codes, scales);
   return hipGetLastError();
 }

@@ -1469,16 +1469,16 @@ void run_dma(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, i
              const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = grid_for(m_total, G, BM, NOUT / NCOL);
-  gemm_bf16_dma_kernel<MODE, BM, BN, BK, ST, WM, WN, OCC>
-      <<<(unsigned)g, 64 * WM * WN, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+  launch_k(gemm_bf16_dma_kernel<MODE, BM, BN, BK, ST, WM, WN, OCC>,
+      (unsigned)g, 64 * WM * WN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
 }
 template <int MODE, int BM, int BN, int BK, int ST, int OCC>
 void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, OCC);
-  gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>
-      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr);
+  launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>,
+      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr);
 }
 template <int MODE, int BM, int BN, int ST>
 void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
@@ -1486,16 +1486,16 @@ void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G
                const float* sB, hipStream_t s) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
-  gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>
-      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB);
+  launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>,
+      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB);
 }
 template <int MODE, int BM, int BN, int BK>
 void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
-  gemm_bf16_rs_kernel<MODE, BM, BN, BK>
-      <<<(unsigned)g, 256, 0, s>>>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
+  launch_k(gemm_bf16_rs_kernel<MODE, BM, BN, BK>,
+      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
 }
 // Every variant has BN = 256 and BK <= 64: it needs NOUT % 128 == 0 for
 // gate/up, NOUT % 256 == 0 for down and K % 64 == 0.
@@ -1638,16 +1638,17 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
       if (profile) prof_begin(pg, s);
       const unsigned grid = (unsigned)((int64_t)G * (ffn / 32) * spe);
       if (wide)
-        gemm_bf16_stream_kernel<MODE_GATEUP, 4><<<grid, 64, 0, s>>>(
+        launch_k(gemm_bf16_stream_kernel<MODE_GATEUP, 4>, grid, 64, 0, s,
             (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
             P, spe, kps);
       else
-        gemm_bf16_stream_kernel<MODE_GATEUP, 2><<<grid, 64, 0, s>>>(
+        launch_k(gemm_bf16_stream_kernel<MODE_GATEUP, 2>, grid, 64, 0, s,
             (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn,
             P, spe, kps);
       if (spe > 1)
-        stream_reduce_kernel<MODE_GATEUP><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * ffn, 256), 8192),
-                                            256, 0, s>>>(P, rows_in, goff, G, max_rows, ffn, spe, H, ffn);
+        launch_k(stream_reduce_kernel<MODE_GATEUP>,
+                 (unsigned)std::min<int64_t>(cdiv64(max_rows * ffn, 256), 8192), 256, 0, s, P,
+                 rows_in, goff, G, max_rows, ffn, spe, H, ffn);
       if (profile) prof_end(pg, s);
     }
     {
@@ -1656,15 +1657,15 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
       if (profile) prof_begin(pd, s);
       const unsigned grid = (unsigned)((int64_t)G * (d / 64) * spe);
       if (wide)
-        gemm_bf16_stream_kernel<MODE_DOWN, 4><<<grid, 64, 0, s>>>(
-            H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+        launch_k(gemm_bf16_stream_kernel<MODE_DOWN, 4>, grid, 64, 0, s, H, rows_out, goff, G,
+                 max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
       else
-        gemm_bf16_stream_kernel<MODE_DOWN, 2><<<grid, 64, 0, s>>>(
-            H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
+        launch_k(gemm_bf16_stream_kernel<MODE_DOWN, 2>, grid, 64, 0, s, H, rows_out, goff, G,
+                 max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, P, spe, kps);
       if (spe > 1)
-        stream_reduce_kernel<MODE_DOWN><<<(unsigned)std::min<int64_t>(cdiv64(max_rows * d, 256), 8192),
-                                          256, 0, s>>>(P, rows_out, goff, G, max_rows, d, spe,
-                                                       (bf16_t*)out, d);
+        launch_k(stream_reduce_kernel<MODE_DOWN>,
+                 (unsigned)std::min<int64_t>(cdiv64(max_rows * d, 256), 8192), 256, 0, s, P,
+                 rows_out, goff, G, max_rows, d, spe, (bf16_t*)out, d);
       if (profile) prof_end(pd, s);
     }
   } else if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
@@ -1681,24 +1682,24 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
     const int64_t g1 = grid_for(max_rows, G, kBM, ffn / (kBN / 2));
     if (profile) prof_begin(pg, s);
-    gemm_bf16_kernel<MODE_GATEUP, kBM, kBN, kBK, 2, 2><<<(unsigned)g1, 256, 0, s>>>(
+    launch_k(gemm_bf16_kernel<MODE_GATEUP, kBM, kBN, kBK, 2, 2>, (unsigned)g1, 256, 0, s,
         (const bf16_t*)in, rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn);
     if (profile) prof_end(pg, s);
     const int64_t g2 = grid_for(max_rows, G, kBM, d / kBN);
     if (profile) prof_begin(pd, s);
-    gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g2, 256, 0, s>>>(
+    launch_k(gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2>, (unsigned)g2, 256, 0, s,
         H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d);
     if (profile) prof_end(pd, s);
   } else {
     float* H = reinterpret_cast<float*>(ws);
     const int64_t g1 = grid_for(max_rows, G, 64, ffn / 32);
     if (profile) prof_begin(pg, s);
-    gemm_f32_kernel<MODE_GATEUP><<<(unsigned)g1, 256, 0, s>>>(
+    launch_k(gemm_f32_kernel<MODE_GATEUP>, (unsigned)g1, 256, 0, s,
         (const float*)in, rows_in, goff, G, max_rows, (const float*)w_gate_up, d, ffn, H, ffn);
     if (profile) prof_end(pg, s);
     const int64_t g2 = grid_for(max_rows, G, 64, d / 64);
     if (profile) prof_begin(pd, s);
-    gemm_f32_kernel<MODE_DOWN><<<(unsigned)g2, 256, 0, s>>>(
+    launch_k(gemm_f32_kernel<MODE_DOWN>, (unsigned)g2, 256, 0, s,
         H, rows_out, goff, G, max_rows, (const float*)w_down, ffn, d, (float*)out, d);
     if (profile) prof_end(pd, s);
   }
@@ -1714,11 +1715,11 @@ hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a,
                          m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n, s);
   } else if (dtype == 1) {
     const int64_t g = grid_for(m, 1, kBM, n / kBN);
-    gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2><<<(unsigned)g, 256, 0, s>>>(
+    launch_k(gemm_bf16_kernel<MODE_DOWN, kBM, kBN, kBK, 2, 2>, (unsigned)g, 256, 0, s,
         (const bf16_t*)a, nullptr, nullptr, 1, m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n);
   } else {
     const int64_t g = grid_for(m, 1, 64, n / 64);
-    gemm_f32_kernel<MODE_DOWN><<<(unsigned)g, 256, 0, s>>>(
+    launch_k(gemm_f32_kernel<MODE_DOWN>, (unsigned)g, 256, 0, s,
         (const float*)a, nullptr, nullptr, 1, m, (const float*)w, kdim, n, (float*)out, n);
   }
   return hipGetLastError();

@@ -2,6 +2,7 @@
 // first HIP error; arguments were validated by the caller.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -13,6 +14,18 @@ constexpr int kRouterSlice = 256;  // router reduction-order slice length
 // Per-kernel event timing (implemented in api.cpp).
 void prof_begin(int kernel, hipStream_t s);
 void prof_end(int kernel, hipStream_t s);
+// Events a kernel launched now on s records from its dispatch packet (both
+// null when no timing window is open on s).
+void prof_kernel_events(hipStream_t s, hipEvent_t* start, hipEvent_t* stop);
+
+// Kernel launch that feeds an open timing window on s with the kernel's
+// own start and end times (hipExtLaunchKernelGGL); a plain launch otherwise.
+template <typename F, typename... Args>
+inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t s, Args... args) {
+  hipEvent_t a, b;
+  prof_kernel_events(s, &a, &b);
+  hipExtLaunchKernelGGL(kernel, grid, block, shm, s, a, b, 0, args...);
+}
 
 // ---- router (router.hip)
 int router_slices(int d);

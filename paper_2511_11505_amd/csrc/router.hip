@@ -314,10 +314,10 @@ hipError_t launch_logits_t(const T* x, const T* w, int N, int d, int E, bool spl
   const int S = router_slices(d);
   if (E <= 16) {
     dim3 grid((N + 255) / 256, (E + 15) / 16, split ? S : 1);
-    router_logits_kernel<T, 256, 16><<<grid, 256, 0, s>>>(x, w, N, d, E, split ? 1 : 0, out);
+    launch_k(router_logits_kernel<T, 256, 16>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
   } else {
     dim3 grid((N + 63) / 64, (E + 63) / 64, split ? S : 1);
-    router_logits_kernel<T, 64, 64><<<grid, 256, 0, s>>>(x, w, N, d, E, split ? 1 : 0, out);
+    launch_k(router_logits_kernel<T, 64, 64>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
   }
   return hipGetLastError();
 }
@@ -350,7 +350,7 @@ hipError_t launch_topk(const float* src, int n_partials, int N, int E, const flo
                        float* logits_out, int32_t* ids, float* w, hipStream_t s) {
   dim3 grid((N + 3) / 4);
 #define FS_TOPK(EPL)                                                                       \
-  topk_kernel<EPL><<<grid, 256, 0, s>>>(src, n_partials, N, E, bias, score, k, G, TG, norm, \
+  launch_k(topk_kernel<EPL>, grid, 256, 0, s, src, n_partials, N, E, bias, score, k, G, TG, norm, \
                                         scale, logits_out, ids, w)
   if (E <= 64)
     FS_TOPK(1);
