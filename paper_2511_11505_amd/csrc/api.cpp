@@ -162,7 +162,7 @@ size_t plan_bytes(const fs_moe_desc* d) { return align256(fs::plan_ws_bytes(d->n
 size_t block_ffn_bytes(const fs_moe_desc* d, int64_t rows, int ffn, bool fp8) {
   if (!fp8) return align256(fs::ffn_ws_bytes(d->dtype, rows, ffn, d->hidden));
   return align256((size_t)rows * d->hidden) + align256((size_t)rows * 4) +
-         align256(fs::ffn_fp8_ws_bytes(rows, ffn));
+         align256(fs::ffn_fp8_ws_bytes(rows, ffn, d->hidden));
 }
 
 size_t block_bytes(const fs_moe_desc* d, int64_t max_rows, bool fp8_routed, bool fp8_shared) {
@@ -250,7 +250,7 @@ fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_row
       return FS_OK;
     case FS_OP_GROUPED_FFN_FP8:
       if (ffn <= 0) return fail(FS_ERR_INVALID, "ffn must be > 0");
-      *bytes = fs::ffn_fp8_ws_bytes(max_rows, ffn);
+      *bytes = fs::ffn_fp8_ws_bytes(max_rows, ffn, desc->hidden);
       return FS_OK;
     case FS_OP_BLOCK: *bytes = block_bytes(desc, max_rows, false, false); return FS_OK;
     case FS_OP_BLOCK_FP8: {
@@ -478,7 +478,7 @@ fs_status fs_grouped_expert_ffn_fp8(const fs_moe_desc* desc, int32_t n_groups, i
   NEED(w_down, "w_down");
   NEED4(s_down, "s_down");
   NEED(out_rows, "out_rows");
-  if (ws_bytes < fs::ffn_fp8_ws_bytes(max_rows, ffn))
+  if (ws_bytes < fs::ffn_fp8_ws_bytes(max_rows, ffn, desc->hidden))
     return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN_FP8)");
   NEED(ws, "ws");
   FS_HIP(fs::launch_grouped_ffn_fp8(n_groups, ffn, desc->hidden, x_codes, x_scales, group_rows,

@@ -602,6 +602,15 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
 // equals bf16's for twice the K.  The epilogue multiplies each accumulator by
 // its row's scale sA (indexed like the A rows) and its column's scale sB
 // (per group: 2 NOUT gate/up columns or NOUT down columns).
+//
+// Split K (SPL; the other instantiations carry none of it): every tile is
+// cut into `splits` K slices of `kps`
+// blocks (the last may be shorter, none empty); a work item is one slice of
+// one tile, the slices of a tile adjacent in the XCD's range.  An item writes
+// its fp32 partial (scales applied) to P[slice][row][col], columns as in
+// stream_reduce_kernel (gate/up: gate 0..NOUT-1, up NOUT..2 NOUT-1), which
+// then adds the slices in order and applies SwiGLU or the scatter.  Passes
+// whose tiles cannot fill the CUs use it.
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
@@ -610,12 +619,13 @@ __device__ __forceinline__ void wait_lgkm0() {
 
 typedef int int32x8 __attribute__((ext_vector_type(8)));
 
-template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false>
+template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false, bool SPL = false>
 __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ B, int K, int NOUT,
-    bf16_t* __restrict__ C, int ldc, const float* __restrict__ sA, const float* __restrict__ sB) {
+    bf16_t* __restrict__ C, int ldc, const float* __restrict__ sA, const float* __restrict__ sB,
+    int splits, int kps, float* __restrict__ P) {
   using TE = typename std::conditional<F8, uint8_t, bf16_t>::type;
   using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
   constexpr int NT = 256;
@@ -666,11 +676,13 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
 
   const int nn = NOUT / NCOL;
-  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int nspl = SPL ? splits : 1;
+  const int64_t total = (int64_t)nn * s_tpre[G] * nspl;
   const int64_t per_xcd = (total + kXcd - 1) / kXcd;
   const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
   const int64_t stride = gridDim.x / kXcd;
-  const int KT = K / BK;
+  const int KT_all = K / BK;
+  const int kpsv = SPL ? kps : KT_all;
   const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
   const int drow = lane / CPR, dpos = lane % CPR;
   auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
@@ -698,9 +710,13 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
     const int64_t L = xcd_base + j;
     if (L >= total) break;
-    const int g = find_group(s_tpre, G, nn, L);
+    const int64_t Lt = SPL ? L / nspl : L;
+    const int ksl = SPL ? (int)(L - Lt * nspl) : 0;
+    const int kbase = ksl * kpsv;
+    const int KT = (KT_all - kbase < kpsv) ? KT_all - kbase : kpsv;   // this item's K blocks
+    const int g = find_group(s_tpre, G, nn, Lt);
     const int Tg = s_tpre[g + 1] - s_tpre[g];
-    const int64_t local = L - (int64_t)nn * s_tpre[g];
+    const int64_t local = Lt - (int64_t)nn * s_tpre[g];
     const int nt = (int)(local / Tg), mt = (int)(local % Tg);
     const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
     const int m0 = mt * BM, n0 = nt * NCOL;
@@ -715,7 +731,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
       if (m >= rows_g) m = rows_g - 1;
       const int grow = row_base + m;
       const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      src[i] = A + sr * K + dchunk(blk) * CE;
+      src[i] = A + sr * K + (size_t)kbase * BK + dchunk(blk) * CE;
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
@@ -726,7 +742,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
       else
         wrow = n0 + r;
-      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * CE;
+      src[A_LD + i] = Bg + (size_t)wrow * K + (size_t)kbase * BK + dchunk(blk) * CE;
     }
     // wave-uniform LDS destinations: ring base + slot + this wave's blocks
     const unsigned ring_lds = lds_addr(ring);
@@ -872,6 +888,38 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
           col = n0 + wn * WTN + jn * 32;
         sbg[jn] = sBg[col + (lane & 31)];
       }
+    }
+    if constexpr (SPL) {
+      // split K: this slice's fp32 partial, straight from the accumulators
+      // (32 consecutive columns per row and accumulator element)
+      if constexpr (F8) __syncthreads();   // s_sa
+      const int W = (MODE == MODE_GATEUP) ? 2 * NOUT : NOUT;
+      float* Ps = P + (size_t)ksl * m_total * W;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          if (m0 + r >= rows_g) continue;
+          const float sa = F8 ? s_sa[r] : 1.f;
+          float* prow = Ps + (size_t)(row_base + m0 + r) * W;
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) {
+            int col;
+            if (MODE == MODE_GATEUP)
+              col = (jn < TN / 2) ? n0 + wn * (WTN / 2) + jn * 32
+                                  : NOUT + n0 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+            else
+              col = n0 + wn * WTN + jn * 32;
+            float y = acc[i][jn][v];
+            if constexpr (F8) y = y * sa * sbg[jn];
+            prow[col + (lane & 31)] = y;
+          }
+        }
+      // the next tile's prologue refills ring slots that slower waves may
+      // still be reading in their last steps (and F8 rewrites s_sa)
+      __syncthreads();
+      continue;
     }
     bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
     constexpr int PASSES = NCOL / ECOL;
@@ -1447,8 +1495,7 @@ int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
   return upper > cap ? cap : upper;
 }
 
-// occ workgroups per compute unit (capped by the tile count, a multiple of 8).
-int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
+int num_cus() {
   static const int cus = [] {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -1456,6 +1503,12 @@ int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
       n = 256;
     return n;
   }();
+  return cus;
+}
+
+// occ workgroups per compute unit (capped by the tile count, a multiple of 8).
+int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
+  const int cus = num_cus();
   const int64_t upper = grid_for(max_rows, G, BM, nn);
   int64_t g = ((int64_t)cus * occ + kXcd - 1) / kXcd * kXcd;
   return g < upper ? g : upper;
@@ -1472,22 +1525,40 @@ void run_dma(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, i
   launch_k(gemm_bf16_dma_kernel<MODE, BM, BN, BK, ST, WM, WN, OCC>,
       (unsigned)g, 64 * WM * WN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
 }
+// K split of an interleaved-ring pass: `splits` slices of `kps` K blocks
+// with fp32 partials in P (splits == 1: no split).
+struct KSplit {
+  int splits = 1;
+  int kps = 0;
+  float* P = nullptr;
+};
+
 template <int MODE, int BM, int BN, int BK, int ST, int OCC>
 void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
-            const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
+            const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s,
+            const KSplit& sp = KSplit{}) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
-  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, OCC);
-  launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>,
-      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr);
+  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, OCC);
+  if (sp.splits > 1)
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true>, (unsigned)g, 256, 0, s,
+             A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, sp.splits, sp.kps,
+             sp.P);
+  else
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>, (unsigned)g, 256, 0, s, A, rows, goff,
+             G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1, K / BK, nullptr);
 }
 template <int MODE, int BM, int BN, int ST>
 void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
                const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc, const float* sA,
-               const float* sB, hipStream_t s) {
+               const float* sB, hipStream_t s, const KSplit& sp) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
-  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
-  launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>,
-      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB);
+  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, 1);
+  if (sp.splits > 1)
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, true>, (unsigned)g, 256, 0, s, A,
+             rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, sp.splits, sp.kps, sp.P);
+  else
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>, (unsigned)g, 256, 0, s, A, rows,
+             goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128, nullptr);
 }
 template <int MODE, int BM, int BN, int BK>
 void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
@@ -1499,19 +1570,20 @@ void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
 }
 // Every variant has BN = 256 and BK <= 64: it needs NOUT % 128 == 0 for
 // gate/up, NOUT % 256 == 0 for down and K % 64 == 0.
+// (A K split applies to the interleaved variants 5 and 7 only.)
 template <int MODE>
 void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
                int64_t m_total, const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc,
-               hipStream_t s) {
+               hipStream_t s, const KSplit& sp = KSplit{}) {
 #define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
   switch (v) {
     case 0: run_dma<MODE, 128, 256, 64, 3, 2, 2, 1>(FS_ARGS); break;
     case 1: run_dma<MODE, 128, 256, 32, 6, 2, 2, 1>(FS_ARGS); break;
     case 2: run_dma<MODE, 256, 256, 32, 4, 2, 4, 1>(FS_ARGS); break;
     case 3: run_dma<MODE, 256, 256, 64, 2, 2, 4, 1>(FS_ARGS); break;
-    case 5: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS); break;
+    case 5: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS, sp); break;
     case 6: run_il<MODE, 128, 256, 32, 3, 2>(FS_ARGS); break;
-    case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS); break;
+    case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS, sp); break;
     case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
     case 9: run_il<MODE, 256, 256, 32, 4, 1>(FS_ARGS); break;
     default: run_dma<MODE, 128, 256, 32, 3, 2, 2, 2>(FS_ARGS); break;
@@ -1574,16 +1646,73 @@ bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
 template <int MODE>
 void gemm_pass_f8(int v, const uint8_t* A, const int32_t* rows, const int32_t* goff, int G,
                   int64_t m_total, const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc,
-                  const float* sA, const float* sB, hipStream_t s) {
+                  const float* sA, const float* sB, hipStream_t s, const KSplit& sp) {
   if (v == 8)
-    run_il_f8<MODE, 256, 256, 2>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
+    run_il_f8<MODE, 256, 256, 2>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s, sp);
   else
-    run_il_f8<MODE, 128, 256, 3>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s);
+    run_il_f8<MODE, 128, 256, 3>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s, sp);
 }
 
-size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn) {
+// K slices for an interleaved-ring pass with fewer tiles (BM rows x 128
+// gate/up or 256 down columns, estimated from the row bound) than CUs, so
+// that most CUs would idle: enough slices for about eight rounds of work
+// items, at most 8, at least 4 K blocks each, partials [slices, max_rows, W]
+// within pbytes.  A pass with at least one tile per CU is not split: there
+// the fp32 partials and the reduction cost more than the balance gains
+// (weight-streaming decode passes slow down by a sixth when split).
+// FS_GEMM_SPLITS forces a count (tuning).
+int ring_splits(bool gateup, int BM, int64_t max_rows, int G, int KT, int NOUT, size_t pbytes) {
+  static const int env = [] {
+    const char* e = getenv("FS_GEMM_SPLITS");
+    return e ? atoi(e) : -1;
+  }();
+  const int NCOL = gateup ? 128 : 256;
+  const int64_t tiles =
+      (int64_t)G * std::max<int64_t>(1, cdiv64(max_rows, (int64_t)BM * G)) * (NOUT / NCOL);
+  const int64_t want = (int64_t)8 * num_cus();
+  int64_t sl;
+  if (env >= 1)
+    sl = env;
+  else
+    sl = tiles >= num_cus() ? 1 : std::min<int64_t>(8, cdiv64(want, tiles));
+  sl = std::min<int64_t>(sl, KT / 4);
+  const size_t per = (size_t)std::max<int64_t>(max_rows, 1) * (gateup ? 2 * NOUT : NOUT) * 4;
+  while (sl > 1 && (size_t)sl * per > pbytes) --sl;
+  return sl < 2 ? 1 : (int)sl;
+}
+
+KSplit make_split(int sl, int KT, float* P) {
+  KSplit sp;
+  if (sl > 1 && P) {
+    sp.kps = (int)cdiv64(KT, sl);
+    sp.splits = (int)cdiv64(KT, sp.kps);    // no empty slice
+    sp.P = sp.splits > 1 ? P : nullptr;
+    if (sp.splits < 2) sp.splits = 1;
+  }
+  return sp;
+}
+
+// The slices' sum, in slice order, then SwiGLU into H (gate/up) or the rows
+// scattered through `rows` (down).
+template <int MODE>
+void reduce_split(const KSplit& sp, const int32_t* rows, const int32_t* goff, int G,
+                  int64_t m_total, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
+  if (sp.splits < 2) return;
+  launch_k(stream_reduce_kernel<MODE>, (unsigned)std::min<int64_t>(cdiv64(m_total * NOUT, 256), 8192),
+           256, 0, s, (const float*)sp.P, rows, goff, G, m_total, NOUT, sp.splits, C, ldc);
+}
+
+// fp32 partials of the split interleaved-ring passes: up to 8 slices of
+// max_rows x max(2F, d), at most kStreamPartialCap.
+size_t split_partial_bytes(int64_t max_rows, int ffn, int d) {
+  const size_t want = (size_t)8 * max_rows * std::max(2 * ffn, d) * 4;
+  return std::min(want, kStreamPartialCap);
+}
+
+size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn, int d) {
   const size_t h = (size_t)max_rows * ffn;
-  return (h * 2 + 255) / 256 * 256 + (h + 255) / 256 * 256 + ((size_t)max_rows * 4 + 255) / 256 * 256;
+  return (h * 2 + 255) / 256 * 256 + (h + 255) / 256 * 256 + ((size_t)max_rows * 4 + 255) / 256 * 256 +
+         (split_partial_bytes(max_rows, ffn, d) + 255) / 256 * 256;
 }
 
 hipError_t launch_grouped_ffn_fp8(int G, int ffn, int d, const uint8_t* x, const float* x_scale,
@@ -1598,15 +1727,31 @@ hipError_t launch_grouped_ffn_fp8(int G, int ffn, int d, const uint8_t* x, const
   bf16_t* H = reinterpret_cast<bf16_t*>(ws);
   uint8_t* Hq = reinterpret_cast<uint8_t*>(ws) + (h * 2 + 255) / 256 * 256;
   float* Hs = reinterpret_cast<float*>(Hq + (h + 255) / 256 * 256);
+  float* P = reinterpret_cast<float*>(reinterpret_cast<char*>(Hs) +
+                                      ((size_t)max_rows * 4 + 255) / 256 * 256);
+  const size_t pbytes = split_partial_bytes(max_rows, ffn, d);
+  bf16_t* Y = static_cast<bf16_t*>(out);
   if (profile) prof_begin(prof_gate_up, s);
-  gemm_pass_f8<MODE_GATEUP>(tile_choice(false, max_rows, G, d, ffn), x, rows_in, goff, G,
-                            max_rows, w_gate_up, d, ffn, H, ffn, x_scale, s_gate_up, s);
+  {
+    const int v = tile_choice(false, max_rows, G, d, ffn);
+    const KSplit sp = make_split(
+        ring_splits(true, v == 8 ? 256 : 128, max_rows, G, d / 128, ffn, pbytes), d / 128, P);
+    gemm_pass_f8<MODE_GATEUP>(v, x, rows_in, goff, G, max_rows, w_gate_up, d, ffn, H, ffn,
+                              x_scale, s_gate_up, s, sp);
+    reduce_split<MODE_GATEUP>(sp, rows_in, goff, G, max_rows, ffn, H, ffn, s);
+  }
   if (profile) prof_end(prof_gate_up, s);
   if (profile) prof_begin(prof_gate_up + 1, s);
   hipError_t e = launch_quantize_fp8(1, H, max_rows, ffn, goff ? goff + G : nullptr, Hq, Hs, s);
   if (e != hipSuccess) return e;
-  gemm_pass_f8<MODE_DOWN>(tile_choice(true, max_rows, G, ffn, d), Hq, rows_out, goff, G, max_rows,
-                          w_down, ffn, d, static_cast<bf16_t*>(out), d, Hs, s_down, s);
+  {
+    const int v = tile_choice(true, max_rows, G, ffn, d);
+    const KSplit sp = make_split(ring_splits(false, 128, max_rows, G, ffn / 128, d, pbytes),
+                                 ffn / 128, P);
+    gemm_pass_f8<MODE_DOWN>(v, Hq, rows_out, goff, G, max_rows, w_down, ffn, d, Y, d, Hs, s_down,
+                            s, sp);
+    reduce_split<MODE_DOWN>(sp, rows_out, goff, G, max_rows, d, Y, d, s);
+  }
   if (profile) prof_end(prof_gate_up + 1, s);
   return hipGetLastError();
 }
@@ -1670,13 +1815,31 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
     }
   } else if (dtype == 1 && ffn % 128 == 0 && d % 256 == 0) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+    float* P = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                        ((size_t)max_rows * ffn * 2 + 255) / 256 * 256);
+    const size_t pbytes = stream_partial_bytes(dtype, max_rows, ffn, d);
+    auto split_of = [&](int v, bool gateup, int K, int NOUT) {
+      if (v != 5 && v != 7) return KSplit{};
+      return make_split(ring_splits(gateup, v == 7 ? 256 : 128, max_rows, G, K / 64, NOUT, pbytes),
+                        K / 64, P);
+    };
     if (profile) prof_begin(pg, s);
-    gemm_pass<MODE_GATEUP>(tile_choice(false, max_rows, G, d, ffn), (const bf16_t*)in, rows_in, goff, G,
-                           max_rows, (const bf16_t*)w_gate_up, d, ffn, H, ffn, s);
+    {
+      const int v = tile_choice(false, max_rows, G, d, ffn);
+      const KSplit sp = split_of(v, true, d, ffn);
+      gemm_pass<MODE_GATEUP>(v, (const bf16_t*)in, rows_in, goff, G, max_rows,
+                             (const bf16_t*)w_gate_up, d, ffn, H, ffn, s, sp);
+      reduce_split<MODE_GATEUP>(sp, rows_in, goff, G, max_rows, ffn, H, ffn, s);
+    }
     if (profile) prof_end(pg, s);
     if (profile) prof_begin(pd, s);
-    gemm_pass<MODE_DOWN>(tile_choice(true, max_rows, G, ffn, d), H, rows_out, goff, G, max_rows,
-                         (const bf16_t*)w_down, ffn, d, (bf16_t*)out, d, s);
+    {
+      const int v = tile_choice(true, max_rows, G, ffn, d);
+      const KSplit sp = split_of(v, false, ffn, d);
+      gemm_pass<MODE_DOWN>(v, H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d,
+                           (bf16_t*)out, d, s, sp);
+      reduce_split<MODE_DOWN>(sp, rows_out, goff, G, max_rows, d, (bf16_t*)out, d, s);
+    }
     if (profile) prof_end(pd, s);
   } else if (dtype == 1) {
     bf16_t* H = reinterpret_cast<bf16_t*>(ws);

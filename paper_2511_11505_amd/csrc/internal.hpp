@@ -68,7 +68,7 @@ hipError_t launch_grouped_ffn(int dtype, int n_groups, int ffn, int d, const voi
 hipError_t launch_quantize_fp8(int dtype, const void* src, int64_t rows, int cols,
                                const int32_t* row_count, uint8_t* codes, float* scales,
                                hipStream_t s, const int32_t* gather = nullptr);
-size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn);
+size_t ffn_fp8_ws_bytes(int64_t max_rows, int ffn, int d);
 hipError_t launch_grouped_ffn_fp8(int n_groups, int ffn, int d, const uint8_t* x,
                                   const float* x_scale, const int32_t* rows_in,
                                   const int32_t* rows_out, const int32_t* goff, int64_t max_rows,

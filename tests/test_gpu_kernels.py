@@ -197,6 +197,35 @@ def test_grouped_ffn(dtype, G, d, F, gather):
     assert np.all(np.isnan(outn[untouched]))
 
 
+@pytest.mark.parametrize("counts,d,F,gather", [([100, 0, 170, 50], 1024, 1024, True),
+                                               ([41, 300, 7], 2048, 512, False)])
+def test_grouped_ffn_split_k(counts, d, F, gather):
+    """Few tiles and long K: the interleaved-ring passes split K into slices
+    with fp32 partials summed in slice order (gate/up and down here);
+    element by element against the oracle."""
+    counts = np.array(counts)
+    G, M = len(counts), int(counts.sum())
+    goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    gen = torch.Generator(device=DEV).manual_seed(d + 3 * F)
+    n_src = M + 9
+    X = torch.randn((n_src, d), generator=gen, device=DEV).to(torch.bfloat16)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(torch.bfloat16)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(torch.bfloat16)
+    rows = torch.randperm(n_src, generator=gen, device=DEV)[:M].to(torch.int32) if gather else None
+    out = torch.full((n_src, d), float("nan"), device=DEV).to(torch.bfloat16)
+    desc = L.make_desc(CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16"))
+    L.fs_grouped_expert_ffn(desc, G, F, X, rows, torch.from_numpy(goff).to(DEV), M, wgu, wd, out,
+                            ws_for(desc, L.FS_OP_GROUPED_FFN, M, F))
+    torch.cuda.synchronize()
+    Xn, gun, dnn, outn = f64(X), f64(wgu), f64(wd), f64(out)
+    rr = rows.cpu().numpy() if gather else np.arange(M)
+    for gi in range(G):
+        sel = rr[goff[gi]:goff[gi + 1]]
+        if len(sel):
+            assert rel_err(outn[sel], oracle.swiglu(Xn[sel], gun[gi], dnn[gi])) <= TOL["bf16"], f"group {gi}"
+    assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
+
+
 @pytest.mark.parametrize("counts,d,F,gather", [
     ([0, 1, 64, 65, 130], 768, 320, True),     # m-chunks of 64, split K 6 / 2 slices (3 + 2 blocks)
     ([37], 512, 256, False),                   # one group (a decode shared expert)
