@@ -95,6 +95,27 @@ __device__ __forceinline__ int find_group(const int* s_tpre, int G, int nn, int6
   return lo;
 }
 
+// find_group for a workgroup's items, which come in increasing order: the
+// answer is at least lo (the previous item's group), and most often lo or
+// lo + 1, so two LDS reads usually settle it before any binary search.
+__device__ __forceinline__ int find_group_from(const int* s_tpre, int G, int nn, int64_t L, int lo) {
+  if (lo + 1 < G && (int64_t)nn * s_tpre[lo + 1] <= L) {
+    ++lo;
+    if (lo + 1 < G && (int64_t)nn * s_tpre[lo + 1] <= L) {
+      int hi = G - 1;
+      ++lo;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)nn * s_tpre[mid] <= L)
+          lo = mid;
+        else
+          hi = mid - 1;
+      }
+    }
+  }
+  return lo;
+}
+
 // ---------------------------------------------------------------- bf16 MFMA
 template <int MODE, int BM, int BN, int BK, int WAVES_M, int WAVES_N>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(
@@ -611,6 +632,21 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
 // stream_reduce_kernel (gate/up: gate 0..NOUT-1, up NOUT..2 NOUT-1), which
 // then adds the slices in order and applies SwiGLU or the scatter.  Passes
 // whose tiles cannot fill the CUs use it.
+//
+// Across tiles (XT: 128-row tiles without split K whose epilogue staging
+// fits one ring slot): the ring's slot numbering runs on from tile
+// to tile, and the last STAGES - 1 blocks of a tile issue the DMAs of the
+// next tile's first STAGES - 1 blocks, so they land during the epilogue and
+// the next tile starts without a load latency.  The epilogue stages through
+// the slot of the tile's last block, the one slot no DMA is writing.  The
+// next tile's gathered A rows are read with scalar loads, which the vector
+// memory counter the ring's waits rely on does not see.  Vector memory
+// operations complete in issue order, so the epilogue's stores, issued after
+// the next tile's first DMAs, only make later waits a little stricter.
+//
+// The epilogue goes through LDS in passes of IPP 32-row accumulator rows per
+// wave, every wave converting in every pass (gate/up: SiLU(g) * u), then all
+// threads store whole 16-byte chunks of the staged rows.
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
@@ -641,8 +677,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;
   constexpr int NLD = A_LD + B_LD;
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
-  constexpr int ECOL = 128;
-  constexpr int CST = ECOL + 8;
+  constexpr int SST = NCOL + 8;                    // staged row, bf16 elements
   constexpr int KS = ROWB / (F8 ? 64 : 32);        // K steps per block
   constexpr int NF = TM + TN;                      // fragments per K step
   constexpr int MPS = TM * TN;                     // MFMAs per K step
@@ -660,10 +695,20 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   static_assert(DPQ <= 2, "two DMAs per MFMA at most");
   static_assert(!F8 || BK == 128, "FP8 rows are 128 elements");
   static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
-  static_assert(NCOL % ECOL == 0, "epilogue passes");
-  static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
+  // Cross-tile candidates: 128-row tiles without split K (256-row tiles
+  // already use every register).  Their staging must fit one slot, the
+  // others' the whole ring.  IPP: accumulator rows (of 32) per wave and
+  // epilogue pass; SROWS: staged rows per pass.
+  constexpr bool XTC = !SPL && BM == 128;
+  constexpr int SCAP = XTC ? STAGE : STAGES * STAGE;
+  constexpr int IPP = (TM % 4 == 0 && 256 * SST * 2 <= SCAP)   ? 4
+                      : (TM % 2 == 0 && 128 * SST * 2 <= SCAP) ? 2
+                                                               : 1;
+  constexpr int SROWS = 64 * IPP;
+  constexpr bool XT = XTC && SROWS * SST * 2 <= STAGE;
+  static_assert(SROWS * SST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
+  static_assert((SROWS * NCOL / 8) % NT == 0, "whole store rounds");
   static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
-  static_assert(MODE != MODE_DOWN || WTN == ECOL, "one epilogue pass per wave column");
 
   __shared__ int s_goff[kMaxGroups + 1];
   __shared__ int s_tpre[kMaxGroups + 1];
@@ -707,52 +752,103 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     bsw[jn] = (r / SWD) % CPR;
   }
 
-  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
-    const int64_t L = xcd_base + j;
-    if (L >= total) break;
+  // A work item: its tile, its K range and the DMA sources of its rows.
+  struct Item {
+    int g, m0, n0, row_base, rows_g, ksl, kbase, KT;
+  };
+  const int wave_s = XT ? __builtin_amdgcn_readfirstlane(wave) : wave;
+  int ghint = 0;   // group of the previous item: a lower bound for the next
+  auto decode = [&](int64_t L, Item& it, const TE* (&sp)[NLD]) {
     const int64_t Lt = SPL ? L / nspl : L;
-    const int ksl = SPL ? (int)(L - Lt * nspl) : 0;
-    const int kbase = ksl * kpsv;
-    const int KT = (KT_all - kbase < kpsv) ? KT_all - kbase : kpsv;   // this item's K blocks
-    const int g = find_group(s_tpre, G, nn, Lt);
-    const int Tg = s_tpre[g + 1] - s_tpre[g];
-    const int64_t local = Lt - (int64_t)nn * s_tpre[g];
-    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
-    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
-    const int m0 = mt * BM, n0 = nt * NCOL;
-    const TE* Bg = B + (size_t)g * bstride;
-
-    // DMA sources: NLD 16-byte chunks per lane per K block
-    const TE* src[NLD];
+    it.ksl = SPL ? (int)(L - Lt * nspl) : 0;
+    it.kbase = it.ksl * kpsv;
+    it.KT = (KT_all - it.kbase < kpsv) ? KT_all - it.kbase : kpsv;
+    // (wave-uniform values; XT makes them scalar for the row-index loads)
+    auto uni = [](int v) { return XT ? __builtin_amdgcn_readfirstlane(v) : v; };
+    it.g = uni(find_group_from(s_tpre, G, nn, Lt, ghint));
+    ghint = it.g;
+    const int Tg = s_tpre[it.g + 1] - s_tpre[it.g];
+    const int local = (int)(Lt - (int64_t)nn * s_tpre[it.g]);   // < nn * Tg
+    const int ntile = local / Tg;
+    it.n0 = uni(ntile * NCOL);
+    it.m0 = uni((local - ntile * Tg) * BM);
+    it.row_base = uni(s_goff[it.g]);
+    it.rows_g = uni(s_goff[it.g + 1]) - it.row_base;
+    const TE* Bg = B + (size_t)it.g * bstride;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
-      const int blk = wave * A_LD + i;
-      int m = m0 + blk * RPB + drow;
-      if (m >= rows_g) m = rows_g - 1;
-      const int grow = row_base + m;
-      const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      src[i] = A + sr * K + (size_t)kbase * BK + dchunk(blk) * CE;
+      const int blk = wave_s * A_LD + i;
+      int64_t sr;
+      if (XT && MODE == MODE_GATEUP && rows) {
+        // the block's RPB row indices with wave-uniform (scalar) loads; a
+        // lane takes the one of its row
+        int v = 0;
+#pragma unroll
+        for (int r = 0; r < RPB; ++r) {
+          int m = it.m0 + blk * RPB + r;
+          if (m >= it.rows_g) m = it.rows_g - 1;
+          const int x = rows[it.row_base + m];
+          v = drow == r ? x : v;
+        }
+        sr = v;
+      } else {
+        int m = it.m0 + blk * RPB + drow;
+        if (m >= it.rows_g) m = it.rows_g - 1;
+        const int grow = it.row_base + m;
+        sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      }
+      sp[i] = A + sr * K + (size_t)it.kbase * BK + dchunk(blk) * CE;
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
-      const int blk = wave * B_LD + i;
+      const int blk = wave_s * B_LD + i;
       const int r = blk * RPB + drow;
       int wrow;
       if (MODE == MODE_GATEUP)
-        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
+        wrow = (r < BN / 2) ? it.n0 + r : NOUT + it.n0 + (r - BN / 2);
       else
-        wrow = n0 + r;
-      src[A_LD + i] = Bg + (size_t)wrow * K + (size_t)kbase * BK + dchunk(blk) * CE;
+        wrow = it.n0 + r;
+      sp[A_LD + i] = Bg + (size_t)wrow * K + (size_t)it.kbase * BK + dchunk(blk) * CE;
     }
-    // wave-uniform LDS destinations: ring base + slot + this wave's blocks
-    const unsigned ring_lds = lds_addr(ring);
-    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
-    auto dst_of = [&](int i) {
-      return i < A_LD ? (wave_u * A_LD + i) * 1024u
-                      : (unsigned)(BM * ROWB) + (wave_u * B_LD + (i - A_LD)) * 1024u;
+  };
+
+  // wave-uniform LDS destinations: ring base + slot + this wave's blocks
+  const unsigned ring_lds = lds_addr(ring);
+  const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+  auto dst_of = [&](int i) {
+    return i < A_LD ? (wave_u * A_LD + i) * 1024u
+                    : (unsigned)(BM * ROWB) + (wave_u * B_LD + (i - A_LD)) * 1024u;
+  };
+  const bool xt_ok = XT && KT_all >= STAGES - 1;
+  int sb = 0;            // ring slot of the current item's block 0
+  bool primed = false;   // its first STAGES - 1 blocks are already in flight
+  const TE* src[NLD];
+  const TE* srcN[NLD];
+  Item itN;              // the next item, decoded during this one's last blocks
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    Item it;
+    if (XT && primed) {
+      it = itN;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) src[i] = srcN[i];
+    } else {
+      decode(L, it, src);
+    }
+    const int KT = it.KT, m0 = it.m0, n0 = it.n0, row_base = it.row_base, rows_g = it.rows_g;
+    const int g = it.g, ksl = it.ksl;
+    const int64_t jnext = j + stride;
+    const bool has_next = xt_ok && jnext < per_xcd && xcd_base + jnext < total;
+
+    auto slot_of = [&](int b) { return (unsigned)((sb + b) % STAGES); };
+    // DMA i of block b: b < KT from this item, b >= KT block b - KT of the next
+    auto dma_cur = [&](int i, int b) {
+      dma16_at(src[i] + b * BK, ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i));
     };
-    auto dma_one = [&](int i, int kt) {
-      dma16_at(src[i] + kt * BK, ring_lds + (unsigned)((kt % STAGES) * STAGE) + dst_of(i));
+    auto dma_nxt = [&](int i, int b) {
+      dma16_at(srcN[i] + (b - KT) * BK, ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i));
     };
 
     floatx16 acc[TM][TN];
@@ -767,7 +863,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
     // A1..A(TM-1); read r is issued after MFMA read_slot(r) of the step before
     auto read_one = [&](FragT (&F)[NF], int kt, int ks, int r) {
-      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
+      const unsigned char* slot = ring + slot_of(kt) * STAGE;
       const int f = r == 0 ? 0 : (r <= TN ? TM + r - 1 : r - TN);
       if constexpr (F8) {
         const int c = ks * 4 + 2 * (lane >> 5);
@@ -786,19 +882,16 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
       for (int r = 0; r < NF; ++r) read_one(F, kt, ks, r);
     };
-    // One K step: reads of the next step, then the MFMAs of this one with
-    // up to DPS DMAs of block kt + STAGES - 1 after the first MFMAs.  PF
-    // (a compile-time flag) says whether that block exists, so the main
-    // loop carries no per-DMA branch.
     // One K step: the MFMAs of this step, with the reads of the next step's
     // fragments spread between them (in the order the next step uses them)
     // and up to DPS DMAs of block kt + STAGES - 1 after the first MFMAs.  A
     // block's last step waits for the next block after its first MFMA, so the
-    // MFMA pipe is busy during the barrier.  PF (a compile-time flag) says
-    // whether block kt + STAGES - 1 exists, so the main loop carries no
-    // per-DMA branch.
+    // MFMA pipe is busy while the waves meet.  PF (compile time) says where
+    // block kt + STAGES - 1 comes from: 1 this item (the main loop, no
+    // per-DMA branch), 2 the next item if there is one, else nowhere (the
+    // last STAGES - 1 blocks; a wave-uniform branch).
     auto step = [&](FragT (&Fc)[NF], FragT (&Fn)[NF], int kt, int ks, auto PF) {
-      constexpr bool pf = decltype(PF)::value;
+      constexpr int pf = decltype(PF)::value;
       const bool more = ks < KS - 1 || kt + 1 < KT;
       const int rkt = ks < KS - 1 ? kt : kt + 1, rks = ks < KS - 1 ? ks + 1 : 0;
 #pragma unroll
@@ -810,12 +903,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         else
           acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if (q == 0 && ks == KS - 1 && (pf || kt + 1 < KT)) {
-          // block kt+1 has landed once at most the DMAs of the blocks issued
-          // after it (kt+2 .. kt+STAGES-1) remain; near the end fewer were
-          // issued, and the wait is complete
+        if (q == 0 && ks == KS - 1 && kt + 1 < KT) {
+          // block kt+1 has landed once at most the DMAs issued after it
+          // (blocks kt+2 .. kt+STAGES-1, of this item or the next) remain;
+          // with nothing prefetched, fewer were issued and the wait is complete
           wait_lgkm0();
-          if (pf)
+          if (pf == 1 || has_next)
             wait_vmcnt<(STAGES - 2) * NLD>();
           else
             wait_vmcnt<0>();
@@ -831,7 +924,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
             const int dl = q * DPQ + u;
             const int d = ks * DPS + dl;
             if (dl < DPS && d < NLD) {
-              if constexpr (pf) dma_one(d, kt + STAGES - 1);
+              if constexpr (pf == 1) dma_cur(d, kt + STAGES - 1);
+              if constexpr (pf == 2)
+                if (has_next) dma_nxt(d, kt + STAGES - 1);
             }
           }
         }
@@ -839,20 +934,27 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
       }
     };
 
-    // prologue: blocks 0 .. STAGES-2 in flight, block 0's first fragments read
+    // prologue: blocks 0 .. STAGES-2 in flight (issued here, or by the last
+    // blocks of the item before), then block 0's first fragments
+    if (!primed) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) dma_one(i, 0);
-    if (KT >= STAGES - 1) {
+      for (int i = 0; i < NLD; ++i) dma_cur(i, 0);
+      if (KT >= STAGES - 1) {
 #pragma unroll
-      for (int b = 1; b < STAGES - 1; ++b)
+        for (int b = 1; b < STAGES - 1; ++b)
 #pragma unroll
-        for (int i = 0; i < NLD; ++i) dma_one(i, b);
-      wait_vmcnt<(STAGES - 2) * NLD>();
+          for (int i = 0; i < NLD; ++i) dma_cur(i, b);
+        wait_vmcnt<(STAGES - 2) * NLD>();
+      } else {
+        for (int b = 1; b < KT; ++b)
+#pragma unroll
+          for (int i = 0; i < NLD; ++i) dma_cur(i, b);
+        wait_vmcnt<0>();
+      }
     } else {
-      for (int b = 1; b < KT; ++b)
-#pragma unroll
-        for (int i = 0; i < NLD; ++i) dma_one(i, b);
-      wait_vmcnt<0>();
+      // DMAs issued after block 0's: blocks 1 .. STAGES-2, then the
+      // previous epilogue's stores
+      wait_vmcnt<(STAGES - 2) * NLD>();
     }
     barrier_nofence();
     read_step(Fa, 0, 0);
@@ -863,11 +965,13 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
         step(Fb, Fa, kt, ks + 1, PF);
       }
     };
-    const int kt_pf = KT - (STAGES - 1);   // blocks that issue a prefetch
-    for (int kt = 0; kt < kt_pf; ++kt) run_block(kt, std::true_type{});
-    for (int kt = kt_pf < 0 ? 0 : kt_pf; kt < KT; ++kt) run_block(kt, std::false_type{});
+    const int kt_pf = KT - (STAGES - 1);   // blocks that prefetch from this item
+    for (int kt = 0; kt < kt_pf; ++kt) run_block(kt, std::integral_constant<int, 1>{});
+    if (has_next) decode(xcd_base + jnext, itN, srcN);
+    for (int kt = kt_pf < 0 ? 0 : kt_pf; kt < KT; ++kt)
+      run_block(kt, std::integral_constant<int, 2>{});
 
-    // Epilogue (as in the kernel above); F8 applies the row and column scales.
+    // Epilogue; F8 applies the row and column scales.
     float sbg[F8 ? TN : 1];
     if constexpr (F8) {
       for (int r = tid; r < BM; r += NT) {
@@ -921,56 +1025,62 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
       __syncthreads();
       continue;
     }
-    bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
-    constexpr int PASSES = NCOL / ECOL;
+    // staged rows: wave row wm's accumulator rows [p IPP, (p + 1) IPP) at
+    // staged rows [wm IPP 32, (wm + 1) IPP 32)
+    bf16_t* Cs = reinterpret_cast<bf16_t*>(ring + (XT ? slot_of(KT - 1) * STAGE : 0));
 #pragma unroll
-    for (int pass = 0; pass < PASSES; ++pass) {
+    for (int p = 0; p < TM / IPP; ++p) {
       __syncthreads();
-      if (MODE == MODE_GATEUP || wn == pass) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+      for (int ii = 0; ii < IPP; ++ii) {
+        const int i = p * IPP + ii;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            const float sa = F8 ? s_sa[r] : 1.f;
-            if (MODE == MODE_GATEUP) {
+        for (int v = 0; v < 16; ++v) {
+          const int rr = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          const int r = wm * WTM + i * 32 + rr;               // tile row
+          const int sr = wm * (IPP * 32) + ii * 32 + rr;      // staged row
+          const float sa = F8 ? s_sa[r] : 1.f;
+          if (MODE == MODE_GATEUP) {
 #pragma unroll
-              for (int jn = 0; jn < TN / 2; ++jn) {
-                float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
-                if constexpr (F8) {
-                  gt = gt * sa * sbg[jn];
-                  up = up * sa * sbg[jn + TN / 2];
-                }
-                const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(swiglu_bf16_epi(gt, up));
+            for (int jn = 0; jn < TN / 2; ++jn) {
+              float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+              if constexpr (F8) {
+                gt = gt * sa * sbg[jn];
+                up = up * sa * sbg[jn + TN / 2];
               }
-            } else {
+              const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
+              Cs[sr * SST + col] = f2bf(swiglu_bf16_epi(gt, up));
+            }
+          } else {
 #pragma unroll
-              for (int jn = 0; jn < TN; ++jn) {
-                const int col = jn * 32 + (lane & 31);
-                float y = acc[i][jn][v];
-                if constexpr (F8) y = y * sa * sbg[jn];
-                Cs[r * CST + col] = f2bf(y);
-              }
+            for (int jn = 0; jn < TN; ++jn) {
+              const int col = wn * WTN + jn * 32 + (lane & 31);
+              float y = acc[i][jn][v];
+              if constexpr (F8) y = y * sa * sbg[jn];
+              Cs[sr * SST + col] = f2bf(y);
             }
           }
         }
       }
       __syncthreads();
-      constexpr int CPRC = ECOL / 8;
+      constexpr int CPRC = NCOL / 8;   // 16-byte chunks per staged row
 #pragma unroll 4
-      for (int c = tid; c < BM * CPRC; c += NT) {
-        const int r = c / CPRC, ch = c % CPRC;
+      for (int c = tid; c < SROWS * CPRC; c += NT) {
+        const int sr = c / CPRC, ch = c % CPRC;
+        const int r = (sr / (IPP * 32)) * WTM + p * IPP * 32 + sr % (IPP * 32);
         const int m = m0 + r;
         if (m < rows_g) {
           const int grow = row_base + m;
           const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-          st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
-               *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
+          st16(C + orow * ldc + n0 + ch * 8, *reinterpret_cast<const uint4*>(Cs + sr * SST + ch * 8));
         }
       }
     }
     __syncthreads();
+    if constexpr (XT) {
+      sb = (sb + KT) % STAGES;
+      primed = has_next;
+    }
   }
 }
 
