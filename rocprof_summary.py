@@ -24,6 +24,12 @@ cycles the MFMA units were busy, SQ_VALU_MFMA_BUSY_CYCLES summed over the
 1024 SIMDs / (GRBM_GUI_ACTIVE summed over the 8 XCDs * 128), and the clock
 the kernel ran at, GRBM_GUI_ACTIVE / 8 / its duration in the trace.
 
+With --memory PMC_DIR (repeatable; runs holding TCP_TCC_READ_REQ_LATENCY_sum,
+TCP_TCC_READ_REQ_sum, TCP_PENDING_STALL_CYCLES_sum, TA_TA_BUSY_sum,
+TCC_HIT_sum, TCC_MISS_sum and GRBM_GUI_ACTIVE), it reports per GEMM kernel
+the mean L1 -> L2 read latency in cycles, the L2 hit rate, and the shares of
+CU cycles in which the L1 waits on pending L2 data and the TA is busy.
+
 With --traffic-json, the calibrated HBM bytes per launch (FETCH + WRITE) of
 the one kernel whose short name contains --kernel are written to OUT, with
 the sha256 of the kernel's source file, so that a reader of OUT can tell
@@ -112,6 +118,44 @@ def mfma_report(trace_dir, pmc_dir, min_us):
         print(f"| {key[0]} | {key[1]} | {avg:.2f} | {100 * b / (g * 128):.1f}% | {g / 8 / avg / 1e3:.2f} |")
 
 
+def memory_report(trace_dir, pmc_dirs, min_us):
+    """Per GEMM kernel: L1 -> L2 read latency, L2 hit rate and the share of
+    cycles the L1 stalls on pending L2 data, from counter runs that hold
+    TCP_TCC_READ_REQ_LATENCY_sum, TCP_TCC_READ_REQ_sum,
+    TCP_PENDING_STALL_CYCLES_sum, TCC_HIT_sum, TCC_MISS_sum and
+    GRBM_GUI_ACTIVE (any split over the directories)."""
+    agg = trace_table(trace_dir)
+    names = ("TCP_TCC_READ_REQ_LATENCY_sum", "TCP_TCC_READ_REQ_sum", "TCP_PENDING_STALL_CYCLES_sum",
+             "TCC_HIT_sum", "TCC_MISS_sum", "GRBM_GUI_ACTIVE", "TA_TA_BUSY_sum")
+    cnt = {}
+    for d in pmc_dirs:
+        for c in names:
+            t = counter_table(d, c)
+            if t:
+                cnt[c] = t
+    missing = [c for c in names if c not in cnt]
+    if missing:
+        raise SystemExit(f"--memory: no counter run holds {missing}")
+    avg = lambda c, key: (sum(cnt[c][key]) / len(cnt[c][key])) if cnt[c].get(key) else None
+    print("| kernel | grid | avg us (trace) | L2 read latency (cycles) | L2 hit rate | "
+          "L1 stalled on L2 | TA busy |")
+    print("|---|---|---|---|---|---|---|")
+    for key, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        t = sum(v) / len(v)
+        vals = {c: avg(c, key) for c in names}
+        if t < min_us or any(x is None for x in vals.values()) or not vals["TCP_TCC_READ_REQ_sum"]:
+            continue
+        if "gemm" not in key[0]:
+            continue
+        lat = vals["TCP_TCC_READ_REQ_LATENCY_sum"] / vals["TCP_TCC_READ_REQ_sum"]
+        hit = vals["TCC_HIT_sum"] / (vals["TCC_HIT_sum"] + vals["TCC_MISS_sum"])
+        # per-CU cycles: GRBM_GUI_ACTIVE sums the 8 XCDs; 256 CUs
+        cyc = vals["GRBM_GUI_ACTIVE"] / 8 * 256
+        print(f"| {key[0]} | {key[1]} | {t:.2f} | {lat:.0f} | {100 * hit:.1f}% | "
+              f"{100 * vals['TCP_PENDING_STALL_CYCLES_sum'] / cyc:.1f}% | "
+              f"{100 * vals['TA_TA_BUSY_sum'] / cyc:.1f}% |")
+
+
 def counter_table(pmc_dir, counter):
     rows = list(csv.DictReader(open(one(os.path.join(pmc_dir, "*_counter_collection.csv")))))
     agg = collections.defaultdict(list)
@@ -131,6 +175,8 @@ def main():
     ap.add_argument("--overlap", action="store_true")
     ap.add_argument("--skip", type=int, default=0, help="--overlap: leading copies to skip (warm-up)")
     ap.add_argument("--mfma")
+    ap.add_argument("--memory", action="append", default=[],
+                    help="counter-run directories for the GEMM memory-pipeline table")
     ap.add_argument("--traffic-json")
     ap.add_argument("--kernel")
     ap.add_argument("--workload")
@@ -147,6 +193,9 @@ def main():
         return
     if a.mfma:
         mfma_report(a.trace_dir, a.mfma, a.min_us)
+        return
+    if a.memory:
+        memory_report(a.trace_dir, a.memory, a.min_us)
         return
     agg = trace_table(a.trace_dir)
     print("| kernel | grid (threads) | launches | avg us | min us | max us |")
