@@ -61,27 +61,61 @@ __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 
 // Wave-wide reductions (64 lanes).
+// Wave-wide reductions without LDS traffic: inside each 16-lane row by DPP
+// (swap neighbours, swap pairs, mirror each half-row, mirror the row), so
+// that every lane of a row holds the row's result, then the four row results
+// are read with v_readlane and combined; the result is wave-uniform.  Max
+// and arg-max select exactly, so their result does not depend on the tree;
+// the sum is one fixed tree.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // row_half_mirror
+constexpr int kDppMirror = 0x140;     // row_mirror
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, FS_WAVE));
-  return v;
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, FS_WAVE);
-  return v;
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
 // Arg-max of (key, idx): larger key wins, equal keys go to the lower idx.
-__device__ __forceinline__ void wave_argmax(float& key, int& idx) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float k2 = __shfl_xor(key, o, FS_WAVE);
-    int i2 = __shfl_xor(idx, o, FS_WAVE);
-    if (k2 > key || (k2 == key && i2 < idx)) {
-      key = k2;
-      idx = i2;
-    }
+__device__ __forceinline__ void argmax_pick(float& key, int& idx, float k2, int i2) {
+  if (k2 > key || (k2 == key && i2 < idx)) {
+    key = k2;
+    idx = i2;
   }
+}
+__device__ __forceinline__ void wave_argmax(float& key, int& idx) {
+  argmax_pick(key, idx, dpp_f<kDppXor1>(key), dpp_i<kDppXor1>(idx));
+  argmax_pick(key, idx, dpp_f<kDppXor2>(key), dpp_i<kDppXor2>(idx));
+  argmax_pick(key, idx, dpp_f<kDppHalfMirror>(key), dpp_i<kDppHalfMirror>(idx));
+  argmax_pick(key, idx, dpp_f<kDppMirror>(key), dpp_i<kDppMirror>(idx));
+  float k = lane_f(key, 0);
+  int i = __builtin_amdgcn_readlane(idx, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16)
+    argmax_pick(k, i, lane_f(key, r), __builtin_amdgcn_readlane(idx, r));
+  key = k;
+  idx = i;
 }
 
 static inline int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }

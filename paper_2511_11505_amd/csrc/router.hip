@@ -25,6 +25,7 @@ namespace fs {
 namespace {
 
 constexpr int kBK = 32;  // hidden elements staged per step (divides the slice)
+constexpr int kRouterSmallN = 128;  // token counts that take the 16-token tiles
 
 template <typename T>
 __device__ __forceinline__ float prod_acc(float acc, float a, float b);
@@ -38,16 +39,16 @@ __device__ __forceinline__ float prod_acc<float>(float acc, float a, float b) {
   return acc + p;
 }
 
-// Each workgroup computes a BT x BE tile of logits; each thread 4 tokens x 4
+// Each workgroup computes a BT x BE tile of logits; each thread TT tokens x 4
 // experts.  split != 0: the workgroup handles the single slice blockIdx.z
 // and writes its slice sum to out[slice][N][E]; otherwise it runs every
 // slice in order and writes the final logits to out[N][E].
-template <typename T, int BT, int BE>
+template <typename T, int BT, int BE, int TT>
 __global__ __launch_bounds__(256) void router_logits_kernel(const T* __restrict__ x,
                                                             const T* __restrict__ w, int N, int d,
                                                             int E, int split,
                                                             float* __restrict__ out) {
-  constexpr int TT = 4, TE = 4;
+  constexpr int TE = 4;
   constexpr int NTG = BT / TT;
   static_assert(NTG * (BE / TE) == 256, "tile must map onto 256 threads");
   constexpr int V = 16 / sizeof(T);
@@ -124,9 +125,15 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const T* __restrict_
     if (st + 1 < n_steps) load(kb + kBK);
 #pragma unroll
     for (int kk = 0; kk < kBK; ++kk) {
-      const float4 xv = *reinterpret_cast<const float4*>(&xs[kk][tg * TT]);
+      float xa[TT];
+      if constexpr (TT == 4) {
+        const float4 xv = *reinterpret_cast<const float4*>(&xs[kk][tg * TT]);
+        xa[0] = xv.x, xa[1] = xv.y, xa[2] = xv.z, xa[3] = xv.w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < TT; ++i) xa[i] = xs[kk][tg * TT + i];
+      }
       const float4 wv = *reinterpret_cast<const float4*>(&ws[kk][eg * TE]);
-      const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
       const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
 #pragma unroll
       for (int i = 0; i < TT; ++i)
@@ -183,30 +190,48 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
   const float NEG = -INFINITY;
 
   float z[EPL], key[EPL];
+  if (n_partials == 0) {
 #pragma unroll
-  for (int j = 0; j < EPL; ++j) {
-    const int e = lane + 64 * j;
-    float v = NEG;
-    if (e < E) {
-      if (n_partials == 0) {
-        v = src[(size_t)t * E + e];
-      } else {
-        // slice sums in ascending order; loads are issued eight at a time
-        float a = 0.f;
-        int s = 0;
-        for (; s + 8 <= n_partials; s += 8) {
-          float p[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) p[i] = src[((size_t)(s + i) * N + t) * E + e];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) a = a + p[i];
-        }
-        for (; s < n_partials; ++s) a = a + src[((size_t)s * N + t) * E + e];
-        v = a;
-      }
-      if (logits_out) logits_out[(size_t)t * E + e] = v;
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + 64 * j;
+      z[j] = e < E ? src[(size_t)t * E + e] : NEG;
     }
-    z[j] = v;
+  } else {
+    // slice sums, each expert's in ascending slice order starting from zero;
+    // the loads of eight slices for all EPL experts go out together
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) z[j] = 0.f;
+    int s = 0;
+    for (; s + 8 <= n_partials; s += 8) {
+      float p[8][EPL];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < EPL; ++j) {
+          const int e = lane + 64 * j;
+          p[i][j] = e < E ? src[((size_t)(s + i) * N + t) * E + e] : 0.f;
+        }
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < EPL; ++j) z[j] = z[j] + p[i][j];
+    }
+    for (; s < n_partials; ++s)
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const int e = lane + 64 * j;
+        z[j] = z[j] + (e < E ? src[((size_t)s * N + t) * E + e] : 0.f);
+      }
+#pragma unroll
+    for (int j = 0; j < EPL; ++j)
+      if (lane + 64 * j >= E) z[j] = NEG;
+  }
+  if (logits_out) {
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + 64 * j;
+      if (e < E) logits_out[(size_t)t * E + e] = z[j];
+    }
   }
 
   float zmax = NEG, sumexp = 0.f;
@@ -289,7 +314,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
       if (lane + 64 * j == bi) zb = z[j];
-    zb = __shfl(zb, bi & 63, FS_WAVE);
+    zb = lane_f(zb, bi & 63);
     const float base = (score == 0) ? expf(zb - zmax) / sumexp : sigmoidf_(zb);
     if (lane == r) {
       my_id = bi;
@@ -300,7 +325,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       if (lane + 64 * j == bi) key[j] = NEG;
   }
   float wsum = 0.f;
-  for (int r = 0; r < k; ++r) wsum += __shfl(my_w, r, FS_WAVE);
+  for (int r = 0; r < k; ++r) wsum += lane_f(my_w, r);
   if (lane < k) {
     float wv = norm ? my_w / wsum : my_w;
     ids[(size_t)t * k + lane] = my_id;
@@ -314,10 +339,15 @@ hipError_t launch_logits_t(const T* x, const T* w, int N, int d, int E, bool spl
   const int S = router_slices(d);
   if (E <= 16) {
     dim3 grid((N + 255) / 256, (E + 15) / 16, split ? S : 1);
-    launch_k(router_logits_kernel<T, 256, 16>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
+    launch_k(router_logits_kernel<T, 256, 16, 4>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
+  } else if (N <= kRouterSmallN) {
+    // few tokens (decode): 16-token tiles, one token per thread, for more
+    // workgroups
+    dim3 grid((N + 15) / 16, (E + 63) / 64, split ? S : 1);
+    launch_k(router_logits_kernel<T, 16, 64, 1>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
   } else {
     dim3 grid((N + 63) / 64, (E + 63) / 64, split ? S : 1);
-    launch_k(router_logits_kernel<T, 64, 64>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
+    launch_k(router_logits_kernel<T, 64, 64, 4>, grid, 256, 0, s, x, w, N, d, E, split ? 1 : 0, out);
   }
   return hipGetLastError();
 }
@@ -327,7 +357,7 @@ hipError_t launch_logits_t(const T* x, const T* w, int N, int d, int E, bool spl
 int router_slices(int d) { return (d + kRouterSlice - 1) / kRouterSlice; }
 
 bool router_split(int N, int d, int E) {
-  const int64_t BT = E <= 16 ? 256 : 64, BE = E <= 16 ? 16 : 64;
+  const int64_t BT = E <= 16 ? 256 : (N <= kRouterSmallN ? 16 : 64), BE = E <= 16 ? 16 : 64;
   const int64_t tiles = cdiv64(N, BT) * cdiv64(E, BE);
   return router_slices(d) > 1 && tiles < 512;
 }

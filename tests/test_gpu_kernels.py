@@ -64,9 +64,17 @@ def check_ids(cfg, ids_gpu, ids_ref, near):
     return int(near.sum())
 
 
-@pytest.mark.parametrize("name", list(SMALL))
+# router-only cases: 37 tokens take the 16-token tiles (three, one ragged)
+# over five slices of the hidden dimension
+ROUTER_EXTRA = {
+    "dsv3_decode_m": CONFIGS["dsv3_decode"].scaled(n_tokens=37, hidden=1280, ffn=192,
+                                                   ffn_shared=192, name="dsv3_decode_m"),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL) + list(ROUTER_EXTRA))
 def test_router_logits_bitexact_and_topk(name):
-    cfg = SMALL[name]
+    cfg = SMALL.get(name) or ROUTER_EXTRA[name]
     wl = make_workload(cfg, DEV, with_experts=False)
     for s in range(cfg.ep_size):
         x = wl.x_all[s]
