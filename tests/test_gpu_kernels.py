@@ -281,8 +281,10 @@ def test_dense_linear(dtype, m, n, kd):
     assert rel_err(out, oracle.dense_linear(f64(a), f64(w))) <= TOL[dtype]
 
 
+# the last two cases have wide rows (640 and 544 16-byte chunks)
 @pytest.mark.parametrize("dtype,N,k,d,shared", [("f32", 37, 2, 256, False), ("bf16", 130, 8, 512, True),
-                                                ("bf16", 5, 1, 128, False)])
+                                                ("bf16", 5, 1, 128, False), ("bf16", 67, 8, 5120, True),
+                                                ("f32", 33, 6, 2176, False)])
 def test_combine_and_residual(dtype, N, k, d, shared):
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     cfg = CONFIGS["tiny"].scaled(n_tokens=N, top_k=k, hidden=d, n_experts=16, dtype=dtype)
