@@ -84,7 +84,8 @@ def ffn_roofs(rows, groups, d, F, es, fp8):
 def step_roofs(cfg, M, active, fp8_routed=False, fp8_shared=False):
     """Algorithmic (bytes, flops, roof time in us) of each step of one pass,
     at HBM 8 TB/s, bf16 MFMA 2.5 PFLOP/s, fp8 MFMA 5.0 PFLOP/s and fp32
-    vector 157.3 TFLOP/s."""
+    vector 157.3 TFLOP/s.  With FP8 routed experts the N token rows are
+    quantised once before pack, and pack moves codes (1 byte) and scales."""
     es = cfg.elem_bytes
     N, d, k, E, F = cfg.n_tokens, cfg.hidden, cfg.top_k, cfg.n_experts, cfg.ffn
     SF = cfg.n_shared * cfg.ffn_shared
@@ -94,13 +95,14 @@ def step_roofs(cfg, M, active, fp8_routed=False, fp8_shared=False):
         "router": (N * d * es + E * d * es + N * E * 4, 2.0 * N * d * E, valu),
         "topk": (N * E * 4 + N * k * 8, 0.0, valu),
         "plan": (12 * N * k, 0.0, valu),
-        "pack": (N * d * es + N * k * d * es + 4 * N * k, 0.0, valu),
+        "pack": ((N * d + N * k * d + 4 * N + 4 * N * k + 4 * N * k) if fp8_routed
+                 else (N * d * es + N * k * d * es + 4 * N * k), 0.0, valu),
         "gate_up": gu,
         "down": dn,
         "combine": (N * k * d * es + 8 * N * k + 2 * N * d * es, 0.0, valu),
     }
     if fp8_routed:
-        steps["quantize"] = (M * d * es + M * d + 4 * M, 0.0, valu)
+        steps["quantize"] = (N * d * es + N * d + 4 * N, 0.0, valu)
     if SF:
         steps["shared_gate_up"], steps["shared_down"] = ffn_roofs(N, 1, d, SF, es, fp8_shared)
         steps["partial"] = (3 * N * d * es, 0.0, valu)
@@ -573,7 +575,7 @@ def main():
     t_roof = sum(r[2] for r in roofs.values())
     overlap = None
     if args.overlap:
-        copy_bytes = cfg.cap * d * es
+        copy_bytes = cfg.cap * d * (1 if fp8_routed else es) + (4 * cfg.cap if fp8_routed else 0)
         overlap = {"next_layer_us": us("next_layer"), "dispatch_copy_us": us("dispatch_copy"),
                    "dispatch_bytes": copy_bytes,
                    "xgmi_equivalent_us": round(copy_bytes / 8 / 153e9 * 1e6, 2),

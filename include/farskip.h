@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 4
+#define FS_ABI_VERSION 5
 
 typedef enum {
   FS_OK = 0,
@@ -92,7 +92,8 @@ typedef enum {
   FS_OP_GROUPED_FFN = 2,
   FS_OP_BLOCK = 3,
   FS_OP_GROUPED_FFN_FP8 = 4,
-  FS_OP_BLOCK_FP8 = 5
+  FS_OP_BLOCK_FP8 = 5,
+  FS_OP_DISPATCH_PACK_FP8 = 6
 } fs_op;
 
 /* One MoE block on one EP rank (Section 2.1).  A plain host struct, read
@@ -132,7 +133,9 @@ int32_t fs_abi_version(void);
  *   op = FS_OP_GROUPED_FFN_FP8: fs_grouped_expert_ffn_fp8 with up to
  *                             max_rows rows and width ffn
  *   op = FS_OP_BLOCK_FP8:     fs_moe_block_forward with FP8 routed and
- *                             shared experts (enough for either alone) */
+ *                             shared experts (enough for either alone)
+ *   op = FS_OP_DISPATCH_PACK_FP8: fs_dispatch_pack_fp8 (max_rows, ffn
+ *                             ignored) */
 fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_rows,
                             int32_t ffn, size_t* bytes);
 
@@ -177,6 +180,27 @@ fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, con
                            int32_t* expert_counts, int32_t* expert_offsets,
                            int32_t* rank_offsets, int32_t* slot_to_row, int32_t* row_to_slot,
                            void* send, void* ws, size_t ws_bytes, fs_stream stream);
+
+/* Dispatch plan and pack of FP8 rows, for FP8 routed experts (the FP8
+ * experts of the paper's inference runs, Section 5.2).  Each token row of x
+ * is quantised once, as fs_quantize_fp8, and its codes and scale go to the
+ * token's k send rows: the send rows are what fs_quantize_fp8 gives for
+ * the bf16 send rows of fs_dispatch_pack, in about half the bytes.
+ *   x            [N, d] bf16 (desc->dtype FS_BF16, d % 16 == 0;
+ *                FS_ERR_UNSUPPORTED otherwise)
+ *   send_codes   [N*k, d] uint8 out, 16-byte aligned
+ *   send_scales  [N*k] fp32 out
+ * The plan outputs are those of fs_dispatch_pack.  Workspace:
+ * FS_OP_DISPATCH_PACK_FP8 (the plan's, then the token codes and scales).
+ * An FP8 row buffer of n rows (the block's send and recv with FP8 routed
+ * experts) holds codes [n, d] at byte 0 and scales [n] at byte a(n*d),
+ * where a(b) rounds b up to a multiple of 256; it fits in the bytes of a
+ * bf16 [n, d] buffer. */
+fs_status fs_dispatch_pack_fp8(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
+                               int32_t* expert_counts, int32_t* expert_offsets,
+                               int32_t* rank_offsets, int32_t* slot_to_row,
+                               int32_t* row_to_slot, uint8_t* send_codes, float* send_scales,
+                               void* ws, size_t ws_bytes, fs_stream stream);
 
 /* Rows landing on this rank's experts after Dispatch (Section 2.1).  The
  * receive buffer holds, for every source rank s, that rank's whole send
@@ -345,10 +369,14 @@ typedef struct {
   const void* ws_gate_up; /* NULL when S = 0 */
   const void* ws_down;
   /* FP8 experts (fs_quantize_fp8 codes and row scales; bf16 blocks only).
-   * When w_gate_up_fp8 is given the routed experts run in FP8
-   * (fs_grouped_expert_ffn_fp8 on the received rows, quantised per row
-   * first) and w_gate_up / w_down are not read; likewise ws_gate_up_fp8
-   * for the shared experts.  Dispatch and Combine stay bf16. */
+   * When w_gate_up_fp8 is given the routed experts run in FP8 and
+   * w_gate_up / w_down are not read: the gate phase packs FP8 rows
+   * (fs_dispatch_pack_fp8), so `send` and `recv` hold FP8 row buffers
+   * (send: N*k rows; recv: R*N*k rows, slot s = rows [s*N*k, (s+1)*N*k)
+   * of its codes and of its scales), Dispatch moves codes and scales, and
+   * fs_grouped_expert_ffn_fp8 reads the received codes.  Likewise
+   * ws_gate_up_fp8 for the shared experts, which quantise their N input
+   * rows.  y and Combine stay bf16. */
   const uint8_t* w_gate_up_fp8;  /* [E/R, 2F, d] or NULL */
   const float* s_gate_up;        /* [E/R, 2F] */
   const uint8_t* w_down_fp8;     /* [E/R, d, F] */

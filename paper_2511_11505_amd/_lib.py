@@ -18,11 +18,11 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_PHASE_ALL, FS_PHASE_BEGIN, FS_PHASE_FINISH, FS_PHASE_GATE, FS_PHASE_SHARED, FS_PHASE_EXPERTS,
  FS_PHASE_COMBINE) = range(7)
 (FS_OP_ROUTER_TOPK, FS_OP_DISPATCH_PACK, FS_OP_GROUPED_FFN, FS_OP_BLOCK, FS_OP_GROUPED_FFN_FP8,
- FS_OP_BLOCK_FP8) = range(6)
+ FS_OP_BLOCK_FP8, FS_OP_DISPATCH_PACK_FP8) = range(7)
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
  FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_QUANTIZE, FS_K_COUNT) = range(15)
-FS_ABI_VERSION = 4
+FS_ABI_VERSION = 5
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -62,6 +62,8 @@ _SIGS = {
     "fs_workspace_size": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i64, _i32, ctypes.POINTER(_sz)]),
     "fs_router_topk": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_dispatch_pack": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "fs_dispatch_pack_fp8": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _sz, _vp]),
     "fs_receive_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
     "fs_local_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
     "fs_grouped_expert_ffn_gathered": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp,
@@ -179,6 +181,15 @@ def fs_dispatch_pack(desc, topk_ids, x, expert_counts, expert_offsets, rank_offs
     _check(load().fs_dispatch_pack(ctypes.byref(desc), ptr(topk_ids), ptr(x), ptr(expert_counts),
                                    ptr(expert_offsets), ptr(rank_offsets), ptr(slot_to_row),
                                    ptr(row_to_slot), ptr(send), wp, wb, stream_handle(stream)))
+
+
+def fs_dispatch_pack_fp8(desc, topk_ids, x, expert_counts, expert_offsets, rank_offsets, slot_to_row,
+                         row_to_slot, send_codes, send_scales, ws, stream=None):
+    wp, wb = _ws(ws)
+    _check(load().fs_dispatch_pack_fp8(ctypes.byref(desc), ptr(topk_ids), ptr(x), ptr(expert_counts),
+                                       ptr(expert_offsets), ptr(rank_offsets), ptr(slot_to_row),
+                                       ptr(row_to_slot), ptr(send_codes), ptr(send_scales), wp, wb,
+                                       stream_handle(stream)))
 
 
 def fs_receive_rows(desc, src_counts, src_offsets, group_rows, group_offsets, stream=None):

@@ -32,6 +32,17 @@ def _quantize(w):
     return codes, scales
 
 
+def fp8_row_views(buf, rows, d):
+    """Views of an FP8 row buffer of `rows` rows held in the device tensor
+    buf (any dtype, contiguous): codes [rows, d] uint8 at byte 0, scales
+    [rows] fp32 at byte rows * d rounded up to a multiple of 256."""
+    raw = buf.reshape(-1).view(torch.uint8)
+    at = (rows * d + 255) // 256 * 256
+    if raw.numel() < at + 4 * rows:
+        raise ValueError("buffer too small for the FP8 rows")
+    return raw[:rows * d].view(rows, d), raw[at:at + 4 * rows].view(torch.float32)
+
+
 class MoEBlock:
     def __init__(self, cfg, w_router, sel_bias, w_gate_up, w_down, ws_gate_up=None, ws_down=None,
                  max_recv_rows=None, device="cuda", with_comm=True, with_return=False, fp8=None):
@@ -130,7 +141,9 @@ def prepare_remote_sources(block, x_all, w_router, sel_bias, y_remote, stream=No
 
     For every source rank s != r, run the library's router + top-k and plan
     + pack on that rank's tokens; the packed send buffer is written straight
-    into receive slot s and the counts / offsets into row s.  Fill this
+    into receive slot s and the counts / offsets into row s.  With FP8
+    routed experts the sources pack FP8 rows (fs_dispatch_pack_fp8) into
+    slot s of the receive buffer's codes and scales.  Fill this
     rank's Combine-return slot with the rows other ranks' experts send back.
     Then run this rank's routing once to learn how many rows land on the
     local experts (what the counts exchange tells the receiver) and return
@@ -148,11 +161,27 @@ def prepare_remote_sources(block, x_all, w_router, sel_bias, y_remote, stream=No
     r2s = torch.empty((cap,), dtype=torch.int32, device=dev)
     ws_r = torch.empty((max(L.fs_workspace_size(desc, L.FS_OP_ROUTER_TOPK), 256),), dtype=torch.uint8, device=dev)
     ws_p = torch.empty((max(L.fs_workspace_size(desc, L.FS_OP_DISPATCH_PACK), 256),), dtype=torch.uint8, device=dev)
+    fp8 = block.fp8 is not None
+    if fp8:
+        # FP8 routed experts: every source packs FP8 rows, into its slot of
+        # the receive buffer's codes and scales
+        ws_p = torch.empty((max(L.fs_workspace_size(desc, L.FS_OP_DISPATCH_PACK_FP8), 256),),
+                           dtype=torch.uint8, device=dev)
+        recv_codes, recv_scales = fp8_row_views(t["recv"], R * cap, cfg.hidden)
+        send_codes, send_scales = fp8_row_views(t["send"], cap, cfg.hidden)
     for s in range(R):
-        send_s = t["recv"][s * cap:(s + 1) * cap] if s != r else t["send"]
         L.fs_router_topk(desc, x_all[s], w_router, sel_bias, None, None, ids, w, ws_r, stream)
-        L.fs_dispatch_pack(desc, ids, x_all[s], t["src_counts"][s], t["src_offsets"][s], ro, s2r, r2s,
-                           send_s, ws_p, stream)
+        if fp8:
+            if s != r:
+                codes_s, scales_s = recv_codes[s * cap:(s + 1) * cap], recv_scales[s * cap:(s + 1) * cap]
+            else:
+                codes_s, scales_s = send_codes, send_scales
+            L.fs_dispatch_pack_fp8(desc, ids, x_all[s], t["src_counts"][s], t["src_offsets"][s], ro,
+                                   s2r, r2s, codes_s, scales_s, ws_p, stream)
+        else:
+            send_s = t["recv"][s * cap:(s + 1) * cap] if s != r else t["send"]
+            L.fs_dispatch_pack(desc, ids, x_all[s], t["src_counts"][s], t["src_offsets"][s], ro, s2r,
+                               r2s, send_s, ws_p, stream)
     if y_remote is not None:
         block.y_ret().copy_(y_remote)
     torch.cuda.synchronize()

@@ -165,8 +165,21 @@ size_t block_ffn_bytes(const fs_moe_desc* d, int64_t rows, int ffn, bool fp8) {
          align256(fs::ffn_fp8_ws_bytes(rows, ffn, d->hidden));
 }
 
+// FP8 pack: the plan's workspace, then the N token rows' codes and scales.
+size_t plan_fp8_bytes(const fs_moe_desc* d) {
+  return plan_bytes(d) + align256((size_t)d->n_tokens * d->hidden) + align256((size_t)d->n_tokens * 4);
+}
+
+// Routed experts inside the block: bf16, or FP8 reading the received codes
+// (the FFN's own workspace only).
+size_t routed_ffn_bytes(const fs_moe_desc* d, int64_t max_rows, bool fp8) {
+  if (!fp8) return block_ffn_bytes(d, max_rows, d->ffn, false);
+  return align256(fs::ffn_fp8_ws_bytes(max_rows, d->ffn, d->hidden));
+}
+
 size_t block_bytes(const fs_moe_desc* d, int64_t max_rows, bool fp8_routed, bool fp8_shared) {
-  size_t b = router_bytes(d) + plan_bytes(d) + block_ffn_bytes(d, max_rows, d->ffn, fp8_routed);
+  size_t b = router_bytes(d) + (fp8_routed ? plan_fp8_bytes(d) : plan_bytes(d)) +
+             routed_ffn_bytes(d, max_rows, fp8_routed);
   if (d->n_shared > 0) b += block_ffn_bytes(d, d->n_tokens, d->n_shared * d->ffn_shared, fp8_shared);
   return b;
 }
@@ -253,6 +266,7 @@ fs_status fs_workspace_size(const fs_moe_desc* desc, int32_t op, int64_t max_row
       *bytes = fs::ffn_fp8_ws_bytes(max_rows, ffn, desc->hidden);
       return FS_OK;
     case FS_OP_BLOCK: *bytes = block_bytes(desc, max_rows, false, false); return FS_OK;
+    case FS_OP_DISPATCH_PACK_FP8: *bytes = plan_fp8_bytes(desc); return FS_OK;
     case FS_OP_BLOCK_FP8: {
       size_t a = block_bytes(desc, max_rows, true, true), b = block_bytes(desc, max_rows, true, false);
       size_t c = block_bytes(desc, max_rows, false, true);
@@ -343,6 +357,54 @@ static fs_status plan_pack_impl(const fs_moe_desc* d, const int32_t* ids, const 
     fs::prof_end(FS_K_PACK, s);
   }
   return FS_OK;
+}
+
+// FP8 rows: quantise the N token rows once, plan, pack codes and scales.
+static fs_status plan_pack_fp8_impl(const fs_moe_desc* d, const int32_t* ids, const void* x,
+                                    int32_t* counts, int32_t* offsets, int32_t* rank_offsets,
+                                    int32_t* s2r, int32_t* r2s, uint8_t* send_codes,
+                                    float* send_scales, void* ws, hipStream_t s) {
+  const int N = d->n_tokens, D = d->hidden;
+  if (N == 0) return FS_OK;
+  char* base = static_cast<char*>(ws) + plan_bytes(d);
+  uint8_t* xq = reinterpret_cast<uint8_t*>(base);
+  float* xs = reinterpret_cast<float*>(base + align256((size_t)N * D));
+  fs::prof_begin(FS_K_QUANTIZE, s);
+  FS_HIP(fs::launch_quantize_fp8(1, x, N, D, nullptr, xq, xs, s), "quantize_fp8");
+  fs::prof_end(FS_K_QUANTIZE, s);
+  fs_status st = plan_pack_impl(d, ids, nullptr, counts, offsets, rank_offsets, s2r, r2s, nullptr,
+                                ws, s);
+  if (st != FS_OK) return st;
+  fs::prof_begin(FS_K_PACK, s);
+  FS_HIP(fs::launch_pack_fp8(xq, xs, s2r, N, d->top_k, D, send_codes, send_scales, s), "pack_fp8");
+  fs::prof_end(FS_K_PACK, s);
+  return FS_OK;
+}
+
+fs_status fs_dispatch_pack_fp8(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
+                               int32_t* expert_counts, int32_t* expert_offsets,
+                               int32_t* rank_offsets, int32_t* slot_to_row, int32_t* row_to_slot,
+                               uint8_t* send_codes, float* send_scales, void* ws, size_t ws_bytes,
+                               fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->dtype != FS_BF16) return fail(FS_ERR_UNSUPPORTED, "FP8 rows need a bf16 desc");
+  if (desc->hidden % 16 != 0) return fail(FS_ERR_UNSUPPORTED, "FP8 rows need hidden % 16 == 0");
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED4(topk_ids, "topk_ids");
+  NEED4(expert_counts, "expert_counts");
+  NEED4(expert_offsets, "expert_offsets");
+  NEED4(rank_offsets, "rank_offsets");
+  NEED4(slot_to_row, "slot_to_row");
+  NEED4(row_to_slot, "row_to_slot");
+  NEED(x, "x");
+  NEED(send_codes, "send_codes");
+  NEED4(send_scales, "send_scales");
+  if (ws_bytes < plan_fp8_bytes(desc))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_DISPATCH_PACK_FP8)");
+  NEED(ws, "ws");
+  return plan_pack_fp8_impl(desc, topk_ids, x, expert_counts, expert_offsets, rank_offsets,
+                            slot_to_row, row_to_slot, send_codes, send_scales, ws, S(stream));
 }
 
 fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, const void* x,
@@ -751,8 +813,8 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   const size_t slot_bytes = (size_t)cap * D * es;
   Carve c{reinterpret_cast<char*>(ws)};
   void* ws_router = c.take(router_bytes(desc));
-  void* ws_plan = c.take(plan_bytes(desc));
-  char* ws_ffn = static_cast<char*>(c.take(block_ffn_bytes(desc, max_recv_rows, desc->ffn, fp8_routed)));
+  void* ws_plan = c.take(fp8_routed ? plan_fp8_bytes(desc) : plan_bytes(desc));
+  char* ws_ffn = static_cast<char*>(c.take(routed_ffn_bytes(desc, max_recv_rows, fp8_routed)));
   char* ws_shared =
       desc->n_shared > 0
           ? static_cast<char*>(c.take(block_ffn_bytes(desc, N, desc->n_shared * desc->ffn_shared, fp8_shared)))
@@ -766,6 +828,33 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   int32_t* my_counts = b->src_counts + (size_t)r * E;
   int32_t* my_offsets = b->src_offsets + (size_t)r * (E + 1);
   char* recv_slot = b->recv ? reinterpret_cast<char*>(b->recv) + (size_t)r * slot_bytes : nullptr;
+  // FP8 routed experts: send and recv are FP8 row buffers (codes, then
+  // scales at a(rows * d)); slot s of recv is rows [s*cap, (s+1)*cap)
+  uint8_t* send_codes = static_cast<uint8_t*>(b->send);
+  float* send_scales =
+      b->send ? reinterpret_cast<float*>(static_cast<char*>(b->send) + align256((size_t)cap * D))
+              : nullptr;
+  uint8_t* recv_codes = static_cast<uint8_t*>(b->recv);
+  float* recv_scales =
+      b->recv ? reinterpret_cast<float*>(static_cast<char*>(b->recv) + align256((size_t)R * cap * D))
+              : nullptr;
+  // the Dispatch stand-in: the whole send buffer into receive slot r
+  auto dispatch_copy = [&](hipStream_t st) -> fs_status {
+    fs::prof_begin(FS_K_DISPATCH_COPY, st);
+    if (fp8_routed) {
+      FS_HIP(hipMemcpyAsync(recv_codes + (size_t)r * cap * D, send_codes, (size_t)cap * D,
+                            hipMemcpyDeviceToDevice, st),
+             "hipMemcpyAsync");
+      FS_HIP(hipMemcpyAsync(recv_scales + (size_t)r * cap, send_scales, (size_t)cap * 4,
+                            hipMemcpyDeviceToDevice, st),
+             "hipMemcpyAsync");
+    } else {
+      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, st),
+             "hipMemcpyAsync");
+    }
+    fs::prof_end(FS_K_DISPATCH_COPY, st);
+    return FS_OK;
+  };
   char* y_slot = b->y ? reinterpret_cast<char*>(b->y) + (size_t)r * slot_bytes : nullptr;
 
   if (do_gate) {
@@ -773,25 +862,26 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
     st = router_impl(desc, residual_in, wt->w_router, wt->sel_bias, nullptr, b->logits,
                      b->topk_ids, b->topk_w, ws_router, sc);
     if (st != FS_OK) return st;
-    st = plan_pack_impl(desc, b->topk_ids, residual_in, my_counts, my_offsets, b->rank_offsets,
-                        b->slot_to_row, b->row_to_slot, b->send, ws_plan, sc);
+    if (fp8_routed)
+      st = plan_pack_fp8_impl(desc, b->topk_ids, residual_in, my_counts, my_offsets,
+                              b->rank_offsets, b->slot_to_row, b->row_to_slot, send_codes,
+                              send_scales, ws_plan, sc);
+    else
+      st = plan_pack_impl(desc, b->topk_ids, residual_in, my_counts, my_offsets, b->rank_offsets,
+                          b->slot_to_row, b->row_to_slot, b->send, ws_plan, sc);
     if (st != FS_OK) return st;
     // Dispatch stand-in: the whole send buffer into receive slot r, on the
     // comm stream, else in order on compute
     if (sm) {
       FS_HIP(hipEventRecord(sync->packed, sc), "hipEventRecord");
       FS_HIP(hipStreamWaitEvent(sm, sync->packed, 0), "hipStreamWaitEvent");
-      fs::prof_begin(FS_K_DISPATCH_COPY, sm);
-      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, sm),
-             "hipMemcpyAsync");
-      fs::prof_end(FS_K_DISPATCH_COPY, sm);
+      st = dispatch_copy(sm);
+      if (st != FS_OK) return st;
       FS_HIP(hipEventRecord(sync->dispatched, sm), "hipEventRecord");
       sync->have_dispatch = true;
     } else if (recv_slot) {
-      fs::prof_begin(FS_K_DISPATCH_COPY, sc);
-      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, sc),
-             "hipMemcpyAsync");
-      fs::prof_end(FS_K_DISPATCH_COPY, sc);
+      st = dispatch_copy(sc);
+      if (st != FS_OK) return st;
     }
   }
   if (do_shared) {
@@ -841,19 +931,13 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       goff = my_offsets;  // E + 1 entries = E_loc + 1 when R == 1
     }
     if (fp8_routed) {
-      // the rows landing on local experts, quantised in grouped order; the
-      // outputs go back to their receive rows
-      uint8_t* xq;
-      float* xs;
-      void* rest;
-      fp8_parts(ws_ffn, max_recv_rows, &xq, &xs, &rest);
-      fs::prof_begin(FS_K_QUANTIZE, sc);
-      FS_HIP(fs::launch_quantize_fp8(1, in_rows, max_recv_rows, D, goff + E_loc, xq, xs, sc, rows),
-             "quantize_fp8");
-      fs::prof_end(FS_K_QUANTIZE, sc);
-      FS_HIP(fs::launch_grouped_ffn_fp8(E_loc, desc->ffn, D, xq, xs, nullptr, rows, goff,
+      // the received codes and scales, gathered through the receive rows;
+      // the outputs go back to their receive rows
+      const uint8_t* xq = b->recv ? recv_codes : send_codes;
+      const float* xs = b->recv ? recv_scales : send_scales;
+      FS_HIP(fs::launch_grouped_ffn_fp8(E_loc, desc->ffn, D, xq, xs, rows, rows, goff,
                                         max_recv_rows, wt->w_gate_up_fp8, wt->s_gate_up,
-                                        wt->w_down_fp8, wt->s_down, b->y, rest, sc, FS_K_GATE_UP),
+                                        wt->w_down_fp8, wt->s_down, b->y, ws_ffn, sc, FS_K_GATE_UP),
              "grouped_ffn_fp8");
     } else {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, rows, goff,

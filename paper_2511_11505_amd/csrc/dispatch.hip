@@ -200,17 +200,28 @@ __global__ __launch_bounds__(1024) void plan_fused_kernel(const int32_t* __restr
 // once and writes it to the token's k send rows.  Waves are laid out
 // (token, 64-chunk block), so short batches still fill the machine.
 // KC > 0 fixes k at compile time (all k row indices are read before the
-// stores); KC = 0 loops over any k.
+// stores); KC = 0 loops over any k.  FP8 rows (T = uint8_t codes) also carry
+// one fp32 scale per row: the lane of chunk 0 copies the token's scale to
+// its k send rows.
 template <typename T, int KC>
 __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ x,
                                                    const int32_t* __restrict__ slot_to_row, int N,
-                                                   int k, int d, T* __restrict__ send) {
+                                                   int k, int d, T* __restrict__ send,
+                                                   const float* __restrict__ x_scale,
+                                                   float* __restrict__ send_scale) {
   const int nch = d * (int)sizeof(T) / 16;
   const int nb = (nch + 63) / 64;
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int t = (int)(wave / nb);
   const int c = (int)(wave % nb) * 64 + (threadIdx.x & 63);
   if (t >= N || c >= nch) return;
+  if (x_scale && c == 0) {
+    const float sc = x_scale[t];
+    for (int j = 0; j < k; ++j) {
+      const int row = slot_to_row[(size_t)t * k + j];
+      if (row >= 0) send_scale[row] = sc;
+    }
+  }
   const uint4 v = reinterpret_cast<const uint4*>(x + (size_t)t * d)[c];
   if constexpr (KC > 0) {
     int rw[KC];
@@ -307,8 +318,9 @@ hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int
                        void* send, hipStream_t s) {
   const int64_t nb = ((int64_t)d * (dtype == 0 ? 4 : 2) / 16 + 63) / 64;
   dim3 grid((unsigned)((N * nb + 3) / 4));
-#define FS_PACK(T, KC) \
-  launch_k(pack_kernel<T, KC>, grid, 256, 0, s, (const T*)x, slot_to_row, N, k, d, (T*)send)
+#define FS_PACK(T, KC)                                                                         \
+  launch_k(pack_kernel<T, KC>, grid, 256, 0, s, (const T*)x, slot_to_row, N, k, d, (T*)send, \
+           (const float*)nullptr, (float*)nullptr)
 #define FS_PACK_T(T)                 \
   switch (k) {                       \
     case 1: FS_PACK(T, 1); break;    \
@@ -325,6 +337,26 @@ hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int
   }
 #undef FS_PACK_T
 #undef FS_PACK
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_fp8(const uint8_t* codes, const float* scales, const int32_t* slot_to_row,
+                           int N, int k, int d, uint8_t* send_codes, float* send_scales,
+                           hipStream_t s) {
+  const int64_t nb = ((int64_t)d / 16 + 63) / 64;
+  dim3 grid((unsigned)((N * nb + 3) / 4));
+#define FS_PACK8(KC)                                                                        \
+  launch_k(pack_kernel<uint8_t, KC>, grid, 256, 0, s, codes, slot_to_row, N, k, d, send_codes, \
+           scales, send_scales)
+  switch (k) {
+    case 1: FS_PACK8(1); break;
+    case 2: FS_PACK8(2); break;
+    case 4: FS_PACK8(4); break;
+    case 6: FS_PACK8(6); break;
+    case 8: FS_PACK8(8); break;
+    default: FS_PACK8(0); break;
+  }
+#undef FS_PACK8
   return hipGetLastError();
 }
 

@@ -44,6 +44,11 @@ hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* 
                        int32_t* row_to_slot, void* ws, hipStream_t s);
 hipError_t launch_pack(int dtype, const void* x, const int32_t* slot_to_row, int N, int k, int d,
                        void* send, hipStream_t s);
+// FP8 rows: codes [N, d] bytes and one fp32 scale per row, to the send rows
+// of slot_to_row (codes [rows, d], scales [rows]).
+hipError_t launch_pack_fp8(const uint8_t* codes, const float* scales, const int32_t* slot_to_row,
+                           int N, int k, int d, uint8_t* send_codes, float* send_scales,
+                           hipStream_t s);
 hipError_t launch_local_rows(const int32_t* offsets, const int32_t* rank_offsets,
                              const int32_t* row_to_slot, int N, int k, int E, int R, int r,
                              int32_t* local_tokens, int32_t* local_offsets, hipStream_t s);

@@ -138,6 +138,40 @@ def test_grouped_ffn_fp8_steps(counts, F, d, gather):
         assert np.all(np.isnan(out_n[untouched]))
 
 
+# ---------------------------------------------------------------- FP8 dispatch
+@pytest.mark.parametrize("N,E,k,R,d", [(77, 16, 2, 1, 256), (300, 64, 6, 4, 512), (9, 256, 8, 8, 1024)])
+def test_dispatch_pack_fp8_bit_exact(N, E, k, R, d):
+    # plan equal to the oracle's; every send row holds the E4M3 codes and
+    # the scale of its token row (oracle quantisation), an all-zero token
+    # included
+    from paper_2511_11505_amd.block import fp8_row_views
+    from workloads.generate import synthetic_topk_ids
+    cfg = CONFIGS["tiny"].scaled(n_tokens=N, n_experts=E, top_k=k, ep_size=R, hidden=d, dtype="bf16")
+    desc = L.make_desc(cfg)
+    ids = synthetic_topk_ids(N, E, k, seed=N + d, device=DEV)
+    g = torch.Generator(device=DEV).manual_seed(N)
+    x = (torch.randn((N, d), generator=g, device=DEV) *
+         torch.exp(4 * torch.rand((N, 1), generator=g, device=DEV) - 2)).to(torch.bfloat16)
+    x[N // 2] = 0
+    cap = N * k
+    i32 = dict(dtype=torch.int32, device=DEV)
+    counts, offsets, ro = torch.empty(E, **i32), torch.empty(E + 1, **i32), torch.empty(R + 1, **i32)
+    s2r, r2s = torch.empty(cap, **i32), torch.empty(cap, **i32)
+    buf = torch.full((cap, d), float("nan"), dtype=torch.bfloat16, device=DEV)   # a bf16-sized buffer
+    codes, scales = fp8_row_views(buf, cap, d)
+    ws = torch.empty((L.fs_workspace_size(desc, L.FS_OP_DISPATCH_PACK_FP8),), dtype=torch.uint8, device=DEV)
+    L.fs_dispatch_pack_fp8(desc, ids, x, counts, offsets, ro, s2r, r2s, codes, scales, ws)
+    torch.cuda.synchronize()
+    plan = oracle.dispatch_plan(ids.cpu().numpy(), E, R)
+    for key, t in (("counts", counts), ("offsets", offsets), ("rank_offsets", ro),
+                   ("slot_to_row", s2r), ("row_to_slot", r2s)):
+        assert np.array_equal(t.cpu().numpy(), plan[key]), key
+    qc, qs = of8.quantize_rows(f64(x).astype(np.float32))
+    tok = plan["row_to_slot"] // k
+    assert np.array_equal(np_u8(codes), qc[tok])
+    assert np.array_equal(scales.cpu().numpy(), qs[tok])
+
+
 # ---------------------------------------------------------------- FP8 experts inside the block
 FP8_BLOCKS = {
     "dsv2lite_f8s": CONFIGS["dsv2lite"].scaled(n_tokens=333, hidden=512, ffn=256, ffn_shared=128,
@@ -152,13 +186,14 @@ FP8_BLOCKS = {
 
 @pytest.mark.parametrize("name", list(FP8_BLOCKS))
 def test_block_fp8_chain(name):
-    # The block with FP8 experts: (a) gate, plan and pack equal the bf16
-    # block's bit for bit; (b) the local expert rows and the shared output
+    # The block with FP8 experts: (a) gate and plan equal the bf16 block's
+    # bit for bit, and its send and receive rows (FP8 dispatch) are the
+    # codes and scales of the bf16 block's rows; (b) the local expert rows and the shared output
     # equal the standalone FP8 FFN on the same inputs bit for bit (that FFN
     # is checked step by step against the oracle above); (c) Combine and the
     # residual add against the oracle on the GPU's rows; (d) the FP8 block
     # stays within FP8's error of the bf16 block.
-    from paper_2511_11505_amd import MoEBlock, prepare_remote_sources
+    from paper_2511_11505_amd import MoEBlock, fp8_row_views, prepare_remote_sources
     from tests._util import TOL
     from workloads import make_workload
     from workloads.generate import merge_shared
@@ -183,15 +218,20 @@ def test_block_fp8_chain(name):
     b16, b8 = blocks[None], blocks["all"]
     R, r, cap, E_loc = cfg.ep_size, cfg.ep_rank, b8.cap, cfg.n_local
     for key in ("topk_ids", "topk_w", "slot_to_row", "row_to_slot", "src_counts", "src_offsets",
-                "rank_offsets", "send"):
+                "rank_offsets"):
         assert torch.equal(b16.t[key], b8.t[key]), key
+    d = cfg.hidden
+    for key, rows_n in (("send", cap), ("recv", R * cap)):
+        codes8, scales8 = fp8_row_views(b8.t[key], rows_n, d)
+        codes16, scales16 = quantize(b16.t[key])
+        assert torch.equal(codes8, codes16) and torch.equal(scales8, scales16), key
     if R > 1:
         assert torch.equal(b16.t["group_offsets"], b8.t["group_offsets"])
         m = int(b8.t["group_offsets"][E_loc].item())
         assert torch.equal(b16.t["group_rows"][:m], b8.t["group_rows"][:m])   # entries past M unwritten
-        in_rows, rows, goff = b8.t["recv"], b8.t["group_rows"], b8.t["group_offsets"]
+        in_rows, rows, goff = b16.t["recv"], b8.t["group_rows"], b8.t["group_offsets"]
     else:
-        in_rows, rows, goff = b8.t["send"], None, b8.t["src_offsets"][r]
+        in_rows, rows, goff = b16.t["send"], None, b8.t["src_offsets"][r]
     M = int(goff[E_loc].item())
     q = b8.fp8_weights
     xq, xs = quantize(in_rows)
