@@ -254,6 +254,13 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
 
   if (G > 1) {
     const int gsz = E / G;
+    // group of each of this lane's experts (E for lanes past the last)
+    int grp[EPL];
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + 64 * j;
+      grp[j] = e < E ? e / gsz : G;
+    }
     float gscore = NEG;
     for (int g = 0; g < G; ++g) {
       float m1 = NEG;
@@ -261,7 +268,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
         const int e = lane + 64 * j;
-        if (e < E && e / gsz == g && (key[j] > m1 || (key[j] == m1 && e < i1))) {
+        if (grp[j] == g && (key[j] > m1 || (key[j] == m1 && e < i1))) {
           m1 = key[j];
           i1 = e;
         }
@@ -273,7 +280,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
-          if (e < E && e / gsz == g && e != i1) m2 = fmaxf(m2, key[j]);
+          if (grp[j] == g && e != i1) m2 = fmaxf(m2, key[j]);
         }
         m2 = wave_max(m2);
         sc = m1 + m2;
@@ -291,10 +298,8 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       if (lane == bi) gk = NEG;
     }
 #pragma unroll
-    for (int j = 0; j < EPL; ++j) {
-      const int e = lane + 64 * j;
-      if (e < E && !((keep >> (e / gsz)) & 1ull)) key[j] = NEG;
-    }
+    for (int j = 0; j < EPL; ++j)
+      if (grp[j] < G && !((keep >> grp[j]) & 1ull)) key[j] = NEG;
   }
 
   int my_id = 0;

@@ -91,9 +91,11 @@ def test_router_logits_bitexact_and_topk(name):
         assert rel_err(w.cpu().numpy()[far], w_ref[far]) <= 2e-6
 
 
+# groups of 16, 24, 32 and 64 experts
 @pytest.mark.parametrize("score,G,TG,k,E", [("softmax", 1, 1, 4, 40), ("sigmoid", 4, 2, 3, 96),
                                             ("sigmoid", 8, 4, 8, 256), ("softmax", 16, 3, 5, 512),
-                                            ("sigmoid", 1, 1, 32, 200)])
+                                            ("sigmoid", 1, 1, 32, 200), ("sigmoid", 16, 5, 6, 256),
+                                            ("softmax", 4, 2, 4, 256)])
 def test_topk_from_given_logits(score, G, TG, k, E):
     # Quantised logits create exact ties: selection must break them toward
     # the lower expert (softmax compares the logits themselves).
