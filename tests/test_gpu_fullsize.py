@@ -130,3 +130,67 @@ def test_fullsize_block(name):
     tol = TOL[cfg.dtype]
     assert rel_err(f64(out)[samp], want) <= tol
     blk.close()
+
+
+@pytest.mark.parametrize("name", ["dsv2lite", "dsv3_prefill", "dsv3_decode"])
+def test_fullsize_block_fp8(name):
+    """The block with FP8 routed experts (FP8 dispatch) at full size: the
+    residual output of sampled tokens against the oracle's FP8 experts (its
+    own E4M3 quantisation of the bf16 weights and of each token row, H
+    rounded to bf16 and quantised per row), shared experts in bf16."""
+    from oracle import fp8 as of8
+    cfg = CONFIGS[name]
+    wl = make_workload(cfg, DEV)
+    sh_gu = sh_dn = None
+    if cfg.n_shared > 0:
+        sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
+    blk = MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=DEV,
+                   fp8="routed")
+    if cfg.ep_size > 1:
+        blk.set_max_recv_rows(prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias, wl.y_remote))
+    comm = torch.cuda.Stream()
+    x = wl.x
+    partial = torch.empty_like(x)
+    blk.begin(x, partial, comm=comm)
+    blk.finish(x, partial, comm=comm)
+    torch.cuda.synchronize()
+
+    N, k, E = cfg.n_tokens, cfg.top_k, cfg.n_experts
+    z_ref = oracle.logits_routing_f32(f64(x).astype(np.float32), f64(wl.w_router).astype(np.float32))
+    bias = None if wl.bias is None else f64(wl.bias)
+    ids_ref, w_ref, near, _ = oracle.route(z_ref, cfg.score, k, cfg.n_groups, cfg.topk_groups,
+                                           cfg.norm_topk, cfg.routed_scale, bias)
+    ids_gpu = blk.t["topk_ids"].cpu().numpy()
+    assert np.array_equal(ids_gpu[~near], ids_ref[~near])
+    # the plan of the GPU's own selection, bit for bit; the rows other ranks
+    # return sit at its positions, so near ties elsewhere do not matter
+    plan = oracle.dispatch_plan(ids_gpu, E, cfg.ep_size)
+    assert np.array_equal(blk.t["slot_to_row"].cpu().numpy(), plan["slot_to_row"])
+    samp = np.array([t for t in sample_tokens(N, 3, cfg.seed + 1) if not near[t]])
+    lo = cfg.ep_rank * cfg.n_local
+    yr = None if wl.y_remote is None else f64(wl.y_remote)
+    cache = {}
+
+    def fp8_expert(el):
+        if el not in cache:
+            gq, gs = of8.quantize_rows(f64(wl.w_gate_up[el]).astype(np.float32))
+            dq, ds = of8.quantize_rows(f64(wl.w_down[el]).astype(np.float32))
+            cache[el] = (gq, gs, dq, ds)
+        return cache[el]
+
+    xs = f64(x)[samp]
+    routed = np.zeros_like(xs)
+    for i, t in enumerate(samp):
+        for j in range(k):
+            e = int(ids_ref[t, j])
+            if lo <= e < lo + cfg.n_local:
+                y = of8.swiglu_fp8(xs[i:i + 1], *fp8_expert(e - lo))[0][0]
+            else:
+                y = yr[plan["slot_to_row"][t * k + j]]
+            routed[i] += w_ref[t, j] * y
+    shared = np.zeros_like(xs)
+    if cfg.n_shared > 0:
+        shared = oracle.shared_ffn(xs, f64(wl.sh_gate_up), f64(wl.sh_down))
+    want = oracle.residual_add(xs, shared, routed)
+    assert rel_err(f64(partial)[samp], want) <= TOL["bf16"]
+    blk.close()
