@@ -82,13 +82,16 @@ def ffn_case(G, F, d, counts, gather, seed):
 
 # [2304] is one dense group whose 256-row tiles fill the CUs: its gate/up
 # pass takes the 256 x 256 FP8 tiles, every other pass 128 x 256; the last
-# case has few tiles and long K, so both passes split K')
+# case but one has few tiles and long K, so both passes split K; the last
+# has more tiles than workgroups with two-block K rings (the ring runs on
+# from tile to tile)
 @pytest.mark.parametrize("counts,F,d,gather", [([0, 1, 64, 65, 130], 256, 512, True),
                                                ([37], 128, 256, False),
                                                ([3, 0, 5, 300, 1, 0, 2, 7], 384, 768, True),
                                                ([513, 700], 512, 1024, False),
                                                ([2304], 4096, 256, False),
-                                               ([100, 0, 170, 50], 1024, 2048, True)])
+                                               ([100, 0, 170, 50], 1024, 2048, True),
+                                               ([12000, 0, 9001, 1, 8000, 11111], 256, 256, True)])
 def test_grouped_ffn_fp8_steps(counts, F, d, gather):
     G = len(counts)
     x, wgu, wdn, goff, rows, M = ffn_case(G, F, d, counts, gather, seed=sum(counts) + F)

@@ -210,6 +210,36 @@ def test_grouped_ffn(dtype, G, d, F, gather):
     assert np.all(np.isnan(outn[untouched]))
 
 
+@pytest.mark.parametrize("counts,d,F,gather", [([12000, 0, 9001, 1, 8000, 11111], 256, 128, True),
+                                               ([12000, 0, 9001, 1, 8000, 11111], 512, 256, False)])
+def test_grouped_ffn_many_tiles(counts, d, F, gather):
+    """More 128-row tiles than workgroups, so the interleaved ring runs on
+    from tile to tile (the last blocks of a tile prefetch the next tile's
+    first ones; gathered rows through scalar loads), with K rings of 2, 4
+    and 8 blocks; element by element against the oracle."""
+    counts = np.array(counts)
+    G, M = len(counts), int(counts.sum())
+    goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    gen = torch.Generator(device=DEV).manual_seed(d + 5 * F)
+    n_src = M + 37
+    X = torch.randn((n_src, d), generator=gen, device=DEV).to(torch.bfloat16)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(torch.bfloat16)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(torch.bfloat16)
+    rows = torch.randperm(n_src, generator=gen, device=DEV)[:M].to(torch.int32) if gather else None
+    out = torch.full((n_src, d), float("nan"), device=DEV).to(torch.bfloat16)
+    desc = L.make_desc(CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16"))
+    L.fs_grouped_expert_ffn(desc, G, F, X, rows, torch.from_numpy(goff).to(DEV), M, wgu, wd, out,
+                            ws_for(desc, L.FS_OP_GROUPED_FFN, M, F))
+    torch.cuda.synchronize()
+    Xn, gun, dnn, outn = f64(X), f64(wgu), f64(wd), f64(out)
+    rr = rows.cpu().numpy() if gather else np.arange(M)
+    for gi in range(G):
+        sel = rr[goff[gi]:goff[gi + 1]]
+        if len(sel):
+            assert rel_err(outn[sel], oracle.swiglu(Xn[sel], gun[gi], dnn[gi])) <= TOL["bf16"], f"group {gi}"
+    assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
+
+
 @pytest.mark.parametrize("counts,d,F,gather", [([100, 0, 170, 50], 1024, 1024, True),
                                                ([41, 300, 7], 2048, 512, False)])
 def test_grouped_ffn_split_k(counts, d, F, gather):
