@@ -1594,7 +1594,10 @@ int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
   if (down) {
     if (dn_env >= 0) return dn_env;
     const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 256);
-    return K < 2816 && max_rows >= 1024 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
+    // 256-row tiles only for long groups (a dense shared expert): on routed
+    // groups of about a thousand rows the 128-row kernel, which primes each
+    // tile's first K blocks during the previous tile, is faster.
+    return K < 2816 && max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
   }
   if (gu_env >= 0) return gu_env;
   const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 128);
