@@ -460,7 +460,8 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
 
 /* Dense linear out[m, n] = a[m, :] . w[n, :] in dtype with fp32
  * accumulation; stands in for the next layer's computation.  a [m, kdim],
- * w [n, kdim], out [m, n]; kdim % 64 == 0, n % 64 == 0. */
+ * w [n, kdim], out [m, n]; kdim % 64 == 0; n % 128 == 0 for bf16, n % 64 == 0
+ * for fp32 (else FS_ERR_UNSUPPORTED). */
 fs_status fs_dense_linear(int32_t dtype, int32_t m, int32_t n, int32_t kdim, const void* a,
                           const void* w, void* out, fs_stream stream);
 

@@ -1592,6 +1592,7 @@ int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
     return e ? atoi(e) : -1;
   }();
   if (down) {
+    if (nout % 256 != 0) return 10;   // the only down variant for such widths
     if (dn_env >= 0) return dn_env;
     const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 256);
     // 256-row tiles only for long groups (a dense shared expert): on routed
@@ -1599,7 +1600,7 @@ int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
     // tile's first K blocks during the previous tile, is faster.
     return K < 2816 && max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
   }
-  if (gu_env >= 0) return gu_env;
+  if (gu_env >= 0 && gu_env != 10) return gu_env;   // 10 is down only
   const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 128);
   return max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 8 : 5;
 }
@@ -1685,8 +1686,9 @@ void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
   launch_k(gemm_bf16_rs_kernel<MODE, BM, BN, BK>,
       (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
 }
-// Every variant has BN = 256 and BK <= 64: it needs NOUT % 128 == 0 for
-// gate/up, NOUT % 256 == 0 for down and K % 64 == 0.
+// Variants 0-9 have BN = 256 and BK <= 64: they need NOUT % 128 == 0 for
+// gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
+// only) has 128 x 128 tiles for NOUT % 128 == 0.
 // (A K split applies to the interleaved variants 5 and 7 only.)
 template <int MODE>
 void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
@@ -1703,6 +1705,10 @@ void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff,
     case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS, sp); break;
     case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
     case 9: run_il<MODE, 256, 256, 32, 4, 1>(FS_ARGS); break;
+    case 10:
+      // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
+      if constexpr (MODE == MODE_DOWN) run_il<MODE, 128, 128, 64, 4, 1>(FS_ARGS);
+      break;
     default: run_dma<MODE, 128, 256, 32, 3, 2, 2, 2>(FS_ARGS); break;
   }
 #undef FS_ARGS
@@ -1993,8 +1999,9 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s) {
   if (m <= 0) return hipSuccess;
-  if (dtype == 1 && n % 256 == 0) {
-    // the LDS-ring kernels as one group of m rows
+  if (dtype == 1 && n % 128 == 0) {
+    // the LDS-ring kernels as one group of m rows (128 x 128 tiles when n is
+    // not a multiple of 256)
     gemm_pass<MODE_DOWN>(tile_choice(true, m, 1, kdim, n), (const bf16_t*)a, nullptr, nullptr, 1,
                          m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n, s);
   } else if (dtype == 1) {

@@ -300,8 +300,13 @@ def test_grouped_ffn_streaming(counts, d, F, gather):
     assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
 
 
+# n not a multiple of 256 takes 128 x 128 tiles: one K block (no cross-tile
+# prefetch), exactly the three blocks a tile prefetches, and the
+# tensor-parallel attention part [4096 x 5120] x [5120 x 640] with a ragged m
 @pytest.mark.parametrize("dtype,m,n,kd", [("f32", 70, 128, 256), ("bf16", 300, 256, 512), ("bf16", 1, 128, 64),
-                                         ("bf16", 2049, 768, 640), ("bf16", 333, 640, 512)])
+                                         ("bf16", 2049, 768, 640), ("bf16", 333, 640, 512),
+                                         ("bf16", 129, 384, 64), ("bf16", 257, 384, 192),
+                                         ("bf16", 4099, 640, 5120)])
 def test_dense_linear(dtype, m, n, kd):
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     gen = torch.Generator(device=DEV).manual_seed(m)
