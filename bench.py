@@ -66,6 +66,48 @@ def kernel_table(L):
     return out
 
 
+KERNELS_NOTE = ("per-launch us from library HIP events: gate_up from the timed steps, where only "
+                "its events are on; the others from an untimed pass of as many steps with "
+                "every kernel's events on")
+
+
+def time_steps(L, run, steps, warmup, stream):
+    """Warm up, then time `steps` runs between torch events on `stream`.
+    Only the routed gate/up pass (the roofline's kernel) carries the
+    library's HIP events in those steps: every timed kernel adds stream
+    events, which slow a step of short kernels by up to a fifth.  A second,
+    untimed pass of `steps` runs with every kernel's events on gives the
+    other kernels' times.  Returns (ms per step, per-kernel table whose
+    gate_up entry comes from the timed steps)."""
+    import torch
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    L.fs_profile_reset()
+    L.fs_profile_select([L.FS_K_GATE_UP])
+    L.fs_profile_enable(True)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        run()
+    b.record(stream)
+    torch.cuda.synchronize()
+    L.fs_profile_enable(False)
+    ms = a.elapsed_time(b) / steps
+    timed_gu = kernel_table(L).get("gate_up")
+    L.fs_profile_reset()
+    L.fs_profile_select(None)
+    L.fs_profile_enable(True)
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    L.fs_profile_enable(False)
+    table = kernel_table(L)
+    if timed_gu is not None:
+        table["gate_up"] = timed_gu
+    return ms, table
+
+
 def ffn_roofs(rows, groups, d, F, es, fp8):
     """(bytes, flops, MFMA peak) of an FFN's gate/up and down passes.  FP8:
     1-byte weights and input codes, H written in bf16, and the down pass
@@ -178,19 +220,7 @@ def bench_layers(args, cfg, torch, L):
     log(f"setup {time.perf_counter() - t0:.1f}s: {args.layers} layers of {cfg.name}")
 
     def timed(run):
-        for _ in range(args.warmup):
-            run()
-        torch.cuda.synchronize()
-        L.fs_profile_reset()
-        L.fs_profile_enable(True)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(compute)
-        for _ in range(args.steps):
-            run()
-        b.record(compute)
-        torch.cuda.synchronize()
-        L.fs_profile_enable(False)
-        return a.elapsed_time(b) / args.steps, kernel_table(L)
+        return time_steps(L, run, args.steps, args.warmup, compute)
 
     ms_fs, k_fs = timed(lambda: st.farskip(x, compute=compute, comm=comm))
     ms_rg, k_rg = timed(lambda: st.regular(x, compute=compute))
@@ -230,6 +260,7 @@ def bench_layers(args, cfg, torch, L):
                              "gate": round(gate, 2),
                              "window": round(per_layer - routed - gate, 2),
                              "fits": comm_us <= per_layer - routed - gate},
+        "kernels_us_note": KERNELS_NOTE,
         "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()},
         "kernels_us_regular": {k2: round(v["us_per_launch"], 2) for k2, v in k_rg.items()},
     }
@@ -280,19 +311,7 @@ def bench_replicated(args, cfg, torch, L):
         f"local rows per layer {rows}")
 
     def timed(run):
-        for _ in range(args.warmup):
-            run()
-        torch.cuda.synchronize()
-        L.fs_profile_reset()
-        L.fs_profile_enable(True)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(compute)
-        for _ in range(args.steps):
-            run()
-        b.record(compute)
-        torch.cuda.synchronize()
-        L.fs_profile_enable(False)
-        return a.elapsed_time(b) / args.steps, kernel_table(L)
+        return time_steps(L, run, args.steps, args.warmup, compute)
 
     ms_fs, k_fs = timed(lambda: st.farskip(x, compute=compute, comm=comm))
     if args.farskip_only:
@@ -370,6 +389,7 @@ def bench_replicated(args, cfg, torch, L):
                             "note": "measured times with each stand-in copy replaced by a ring "
                                     "all-reduce of the message over R ranks (model, not a "
                                     "measurement); FarSkip pays only what exceeds its window"},
+        "kernels_us_note": KERNELS_NOTE,
         "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()},
         "kernels_us_regular": {k2: round(v["us_per_launch"], 2) for k2, v in k_rg.items()},
     }
@@ -460,20 +480,12 @@ def main():
             blk.finish(xs[j], partials[j], compute=compute, comm=comm_stream)
 
     def timed(comm_stream):
-        for i in range(args.warmup):
-            step(i, comm_stream)
-        torch.cuda.synchronize()
-        L.fs_profile_reset()
-        L.fs_profile_enable(True)
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        start.record(compute)
-        for i in range(args.steps):
-            step(i, comm_stream)
-        end.record(compute)
-        torch.cuda.synchronize()
-        L.fs_profile_enable(False)
-        return start.elapsed_time(end) / args.steps, kernel_table(L)
+        n = [0]
+
+        def run():
+            step(n[0], comm_stream)
+            n[0] += 1
+        return time_steps(L, run, args.steps, args.warmup, compute)
 
     ms, kernels = timed(comm)
     serial = timed(None) if (args.overlap and comm is not None) else None
@@ -617,6 +629,7 @@ def main():
         "permute_frac_hbm": {k2: round(v / PEAK_HBM_GBS, 4) for k2, v in hbm.items()},
         "step_roofline_frac": steps_frac,
         "block_roofline_frac": round(t_roof / (ms * 1e3), 4),
+        "kernels_us_note": KERNELS_NOTE,
         "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in kernels.items()},
     }
     if overlap is not None:

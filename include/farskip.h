@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 5
+#define FS_ABI_VERSION 6
 
 typedef enum {
   FS_OK = 0,
@@ -496,6 +496,12 @@ typedef enum {
   FS_K_COUNT = 14
 } fs_kernel_id;
 fs_status fs_profile_enable(int32_t on);
+/* Which kernels fs_profile_enable times: bit i of mask selects fs_kernel_id
+ * i (all by default).  Every timed kernel adds a stream event, and on a
+ * step of many short kernels those events slow the step itself, so a
+ * caller that times the whole step can select only the kernels it needs.
+ * Bits at or above FS_K_COUNT: FS_ERR_INVALID. */
+fs_status fs_profile_select(uint32_t mask);
 fs_status fs_profile_read(int32_t kernel, double* total_ms, int64_t* launches);
 fs_status fs_profile_reset(void);
 

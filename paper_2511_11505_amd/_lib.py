@@ -22,7 +22,7 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
  FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_QUANTIZE, FS_K_COUNT) = range(15)
-FS_ABI_VERSION = 5
+FS_ABI_VERSION = 6
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -84,6 +84,7 @@ _SIGS = {
                                     _vp, _vp, _vp]),
     "fs_dense_linear": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "fs_profile_enable": (_i32, [_i32]),
+    "fs_profile_select": (_i32, [ctypes.c_uint32]),
     "fs_profile_read": (_i32, [_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]),
     "fs_profile_reset": (_i32, []),
 }
@@ -287,6 +288,12 @@ def fs_moe_block_forward(desc, phase, weights, residual_in, partial_out, residua
 
 def fs_profile_enable(on=True):
     _check(load().fs_profile_enable(int(on)))
+
+
+def fs_profile_select(kernels=None):
+    """Time only the given fs_kernel_id values (None: all)."""
+    mask = (1 << FS_K_COUNT) - 1 if kernels is None else sum(1 << int(k) for k in set(kernels))
+    _check(load().fs_profile_select(mask))
 
 
 def fs_profile_read(kernel):

@@ -110,6 +110,7 @@ hipStream_t S(fs_stream s) { return reinterpret_cast<hipStream_t>(s); }
 struct ProfState {
   std::mutex mu;
   bool on = false;
+  uint32_t mask = (1u << FS_K_COUNT) - 1;   // kernel ids that open windows
   struct Window {
     int kernel;
     hipStream_t s;
@@ -190,7 +191,7 @@ namespace fs {
 void prof_begin(int kernel, hipStream_t s) {
   ProfState& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
-  if (!p.on) return;
+  if (!p.on || !((p.mask >> kernel) & 1u)) return;
   hipEvent_t a = take_event(p), b = take_event(p), k0 = take_event(p);
   if (!a || !b || !k0 || hipEventRecord(a, s) != hipSuccess) {
     for (hipEvent_t e : {a, b, k0})
@@ -985,6 +986,14 @@ fs_status fs_profile_enable(int32_t on) {
   ProfState& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
   p.on = on != 0;
+  return FS_OK;
+}
+
+fs_status fs_profile_select(uint32_t mask) {
+  if (mask >> FS_K_COUNT) return fail(FS_ERR_INVALID, "mask has bits beyond FS_K_COUNT");
+  ProfState& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.mask = mask;
   return FS_OK;
 }
 

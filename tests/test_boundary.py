@@ -41,6 +41,10 @@ def test_binding_constants_match_the_header():
     assert L.fs_profile_read(L.FS_K_COUNT - 1) == (0.0, 0)
     with pytest.raises(L.FsError):
         L.fs_profile_read(L.FS_K_COUNT)
+    with pytest.raises(L.FsError):
+        L.fs_profile_select([L.FS_K_COUNT])
+    L.fs_profile_select([L.FS_K_GATE_UP, L.FS_K_DOWN])
+    L.fs_profile_select(None)
 
 
 def test_status_strings():

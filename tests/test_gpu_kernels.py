@@ -353,3 +353,34 @@ def test_combine_and_residual(dtype, N, k, d, shared):
     L.fs_farskip_residual(desc, resid0, resid0, routed)
     torch.cuda.synchronize()
     assert rel_err(resid0, want_inplace) <= TOL[dtype]
+
+
+def test_profile_select_times_only_the_selected_kernels():
+    """fs_profile_select: with only the gate/up pass selected, a grouped FFN
+    records gate/up launches and no down launches; with all selected, both."""
+    G, per, d, F = 4, 100, 256, 256
+    M = G * per
+    gen = torch.Generator(device=DEV).manual_seed(5)
+    X = torch.randn((M, d), generator=gen, device=DEV).to(torch.bfloat16)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(torch.bfloat16)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(torch.bfloat16)
+    goff = torch.arange(0, M + 1, per, dtype=torch.int32, device=DEV)
+    out = torch.empty((M, d), dtype=torch.bfloat16, device=DEV)
+    desc = L.make_desc(CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16"))
+    ws = ws_for(desc, L.FS_OP_GROUPED_FFN, M, F)
+    try:
+        for sel, want_down in (([L.FS_K_GATE_UP], 0), (None, 2)):
+            L.fs_profile_reset()
+            L.fs_profile_select(sel)
+            L.fs_profile_enable(True)
+            for _ in range(2):
+                L.fs_grouped_expert_ffn(desc, G, F, X, None, goff, M, wgu, wd, out, ws)
+            torch.cuda.synchronize()
+            L.fs_profile_enable(False)
+            ms_gu, n_gu = L.fs_profile_read(L.FS_K_GATE_UP)
+            assert n_gu == 2 and ms_gu > 0
+            assert L.fs_profile_read(L.FS_K_DOWN)[1] == want_down
+    finally:
+        L.fs_profile_enable(False)
+        L.fs_profile_select(None)
+        L.fs_profile_reset()
