@@ -98,11 +98,13 @@ __device__ __forceinline__ float wave_sum(float v) {
   return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
 }
 // Arg-max of (key, idx): larger key wins, equal keys go to the lower idx.
+// Bitwise | and & evaluate both comparisons, so this is a compare and two
+// selects; a short-circuit || / && compiles to exec-mask branches, a serial
+// chain of scalar instructions in every reduction step.
 __device__ __forceinline__ void argmax_pick(float& key, int& idx, float k2, int i2) {
-  if (k2 > key || (k2 == key && i2 < idx)) {
-    key = k2;
-    idx = i2;
-  }
+  const bool take = (k2 > key) | ((k2 == key) & (i2 < idx));
+  key = take ? k2 : key;
+  idx = take ? i2 : idx;
 }
 __device__ __forceinline__ void wave_argmax(float& key, int& idx) {
   argmax_pick(key, idx, dpp_f<kDppXor1>(key), dpp_i<kDppXor1>(idx));

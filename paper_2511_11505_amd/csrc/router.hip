@@ -208,8 +208,10 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
-          const int e = lane + 64 * j;
-          p[i][j] = e < E ? src[((size_t)(s + i) * N + t) * E + e] : 0.f;
+          // lanes past the last expert load the last one's and take 0
+          const int e = lane + 64 * j, ec = e < E ? e : E - 1;
+          const float v = src[((size_t)(s + i) * N + t) * E + ec];
+          p[i][j] = e < E ? v : 0.f;
         }
 #pragma unroll
       for (int i = 0; i < 8; ++i)
@@ -219,8 +221,9 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
     for (; s < n_partials; ++s)
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
-        const int e = lane + 64 * j;
-        z[j] = z[j] + (e < E ? src[((size_t)s * N + t) * E + e] : 0.f);
+        const int e = lane + 64 * j, ec = e < E ? e : E - 1;
+        const float v = src[((size_t)s * N + t) * E + ec];
+        z[j] = z[j] + (e < E ? v : 0.f);
       }
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
@@ -267,11 +270,11 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       int i1 = INT_MAX;
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
+        // (selects, not branches: see argmax_pick)
         const int e = lane + 64 * j;
-        if (grp[j] == g && (key[j] > m1 || (key[j] == m1 && e < i1))) {
-          m1 = key[j];
-          i1 = e;
-        }
+        const bool take = (grp[j] == g) & ((key[j] > m1) | ((key[j] == m1) & (e < i1)));
+        m1 = take ? key[j] : m1;
+        i1 = take ? e : i1;
       }
       wave_argmax(m1, i1);
       float sc = m1;
@@ -280,12 +283,12 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
-          if (grp[j] == g && e != i1) m2 = fmaxf(m2, key[j]);
+          m2 = ((grp[j] == g) & (e != i1)) ? fmaxf(m2, key[j]) : m2;
         }
         m2 = wave_max(m2);
         sc = m1 + m2;
       }
-      if (lane == g) gscore = sc;
+      gscore = lane == g ? sc : gscore;
     }
     uint64_t keep = 0;
     float gk = (lane < G) ? gscore : NEG;
@@ -295,11 +298,11 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
       int bi = gi;
       wave_argmax(bk, bi);
       if (bi < 64) keep |= 1ull << bi;
-      if (lane == bi) gk = NEG;
+      gk = lane == bi ? NEG : gk;
     }
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
-      if (grp[j] < G && !((keep >> grp[j]) & 1ull)) key[j] = NEG;
+      key[j] = ((grp[j] < G) & !((keep >> grp[j]) & 1ull)) ? NEG : key[j];
   }
 
   int my_id = 0;
@@ -309,25 +312,20 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ src
     int bi = INT_MAX;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      if (key[j] > bk) {
-        bk = key[j];
-        bi = lane + 64 * j;
-      }
+      const bool take = key[j] > bk;
+      bk = take ? key[j] : bk;
+      bi = take ? lane + 64 * j : bi;
     }
     wave_argmax(bk, bi);
     float zb = NEG;
 #pragma unroll
-    for (int j = 0; j < EPL; ++j)
-      if (lane + 64 * j == bi) zb = z[j];
+    for (int j = 0; j < EPL; ++j) zb = lane + 64 * j == bi ? z[j] : zb;
     zb = lane_f(zb, bi & 63);
     const float base = (score == 0) ? expf(zb - zmax) / sumexp : sigmoidf_(zb);
-    if (lane == r) {
-      my_id = bi;
-      my_w = base;
-    }
+    my_id = lane == r ? bi : my_id;
+    my_w = lane == r ? base : my_w;
 #pragma unroll
-    for (int j = 0; j < EPL; ++j)
-      if (lane + 64 * j == bi) key[j] = NEG;
+    for (int j = 0; j < EPL; ++j) key[j] = lane + 64 * j == bi ? NEG : key[j];
   }
   float wsum = 0.f;
   for (int r = 0; r < k; ++r) wsum += lane_f(my_w, r);
