@@ -30,6 +30,12 @@ TCC_HIT_sum, TCC_MISS_sum and GRBM_GUI_ACTIVE), it reports per GEMM kernel
 the mean L1 -> L2 read latency in cycles, the L2 hit rate, and the shares of
 CU cycles in which the L1 waits on pending L2 data and the TA is busy.
 
+With --window SUBSTRING START COUNT, it also prints the mean duration of
+launches START .. START+COUNT-1 (in start order, from 0) of the one kernel
+whose short name contains SUBSTRING: bench.py runs warm-up steps, the timed
+steps and then an untimed pass with every kernel's events on, so the timed
+steps' launches are a window of the trace.
+
 With --traffic-json, the calibrated HBM bytes per launch (FETCH + WRITE) of
 the one kernel whose short name contains --kernel are written to OUT, with
 the sha256 of the kernel's source file, so that a reader of OUT can tell
@@ -66,6 +72,22 @@ def trace_table(trace_dir):
         key = (short(r["Kernel_Name"]), int(r["Grid_Size_X"]))
         agg[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     return agg
+
+
+def window_report(trace_dir, substring, start, count):
+    rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
+    names = {short(r["Kernel_Name"]) for r in rows if substring in short(r["Kernel_Name"])}
+    if len(names) != 1:
+        raise SystemExit(f"--window: {substring!r} matches {sorted(names)}")
+    name, = names
+    sel = sorted((r for r in rows if short(r["Kernel_Name"]) == name),
+                 key=lambda r: int(r["Start_Timestamp"]))[start:start + count]
+    if len(sel) != count:
+        raise SystemExit(f"--window: {name} has {len(sel)} launches in [{start}, {start + count})")
+    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel]
+    print()
+    print(f"{name}: launches {start}..{start + count - 1} (start order) average "
+          f"{sum(d) / len(d):.2f} us (min {min(d):.2f}, max {max(d):.2f})")
 
 
 def overlap_report(trace_dir, min_us, skip):
@@ -183,6 +205,7 @@ def main():
     ap.add_argument("--source")
     ap.add_argument("--tile", default="")
     ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--window", nargs=3, metavar=("SUBSTRING", "START", "COUNT"))
     ap.add_argument("--all-kernels", action="store_true",
                     help="also list torch's kernels (input generation during setup)")
     a = ap.parse_args()
@@ -205,6 +228,8 @@ def main():
         if avg < a.min_us or not keep(k):
             continue
         print(f"| {k} | {g} | {len(v)} | {avg:.2f} | {min(v):.2f} | {max(v):.2f} |")
+    if a.window:
+        window_report(a.trace_dir, a.window[0], int(a.window[1]), int(a.window[2]))
     for label, d, ctr in (("FETCH_SIZE", a.fetch, "FETCH_SIZE"), ("WRITE_SIZE", a.write, "WRITE_SIZE")):
         if not d:
             continue
