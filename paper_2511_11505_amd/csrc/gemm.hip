@@ -682,7 +682,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   constexpr int NF = TM + TN;                      // fragments per K step
   constexpr int MPS = TM * TN;                     // MFMAs per K step
   // read r of the next step goes out after MFMA read_slot(r) of this one
-  auto read_slot = [](int r) { return ((r + 1) * MPS) / NF - 1; };
+  // (with fewer MFMAs than fragments per step, as for one 32-row block per
+  // wave, the first reads all go out after MFMA 0)
+  auto read_slot = [](int r) { return std::max(0, ((r + 1) * MPS) / NF - 1); };
   // The DMAs of block kt + STAGES - 1 go out during block kt: spread over its
   // steps 0..KS-2 with three or more slots, all in step 0 with two (they must
   // land before the block's last step).
