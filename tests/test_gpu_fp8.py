@@ -44,8 +44,13 @@ def np_u8(t):
     return t.cpu().numpy().astype(np.uint8)
 
 
+# 1024 rows and more take one wave per row for bf16 rows up to 8192 wide
+# (16 columns: two vectors, most lanes idle; 2064: a ragged 16-vector row;
+# 8192 the widest; 8208 falls back to a workgroup per row)
 @pytest.mark.parametrize("dtype,rows,cols", [("bf16", 37, 512), ("f32", 21, 256), ("bf16", 1, 7168),
-                                             ("bf16", 300, 2048)])
+                                             ("bf16", 300, 2048), ("bf16", 1030, 16),
+                                             ("bf16", 1500, 2048), ("bf16", 1025, 2064),
+                                             ("bf16", 1024, 8192), ("bf16", 1024, 8208)])
 def test_quantize_rows_bit_exact(dtype, rows, cols):
     g = torch.Generator(device=DEV).manual_seed(rows * 7 + cols)
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
