@@ -1,5 +1,6 @@
 """Host logic of rocprof_summary.py on small synthetic rocprofv3 CSV files:
-the overlap fraction of the copy stream, and the calibrated traffic record."""
+the overlap fraction of the copy stream, the calibrated traffic record and
+the mean over a window of one kernel's launches."""
 
 import csv
 import json
@@ -70,3 +71,22 @@ def test_traffic_record(tmp_path):
     assert rec["hbm_bytes_per_launch"] == (1000 * 2 + 300) * 1024
     assert rec["commands"] == ["cmd"] and rec["workload"] == "w"
     assert len(rec["source_sha256"]) == 64
+
+
+def test_launch_window(tmp_path):
+    # five launches of one GEMM (written out of order) with durations 10, 20,
+    # 30, 40, 50 us by start time; launches 1..3 average 30 us
+    us = 1000
+    write_trace(str(tmp_path), [
+        (0, "void fs::gemm<0>(int)", 300 * us, 340 * us, 65536),
+        (0, "void fs::gemm<0>(int)", 0, 10 * us, 65536),
+        (0, "void fs::gemm<0>(int)", 100 * us, 120 * us, 65536),
+        (0, "void fs::gemm<0>(int)", 400 * us, 450 * us, 65536),
+        (0, "void fs::gemm<0>(int)", 200 * us, 230 * us, 65536),
+        (0, "void fs::combine(int)", 500 * us, 505 * us, 4096),
+    ])
+    out = run(str(tmp_path), "--window", "gemm<0>", "1", "3")
+    assert "gemm<0>: launches 1..3 (start order) average 30.00 us (min 20.00, max 40.00)" in out
+    r = subprocess.run([sys.executable, TOOL, str(tmp_path), "--window", "gemm<0>", "3", "5"],
+                       capture_output=True, text=True)
+    assert r.returncode != 0 and "has 2 launches" in r.stderr
