@@ -20,6 +20,9 @@ Parity status per function (what pins it is in tests/test_oracle_pins.py):
   receive_rows ..................... pinned (per-source decomposition)
   swiglu ........................... pinned (closed forms)
   combine, moe_block ............... pinned (dense masked brute force)
+  route_given ...................... pinned (route's own selection, slot order)
+  moe_tokens_direct ................ pinned (dense gate-matrix mixture, the packed
+                                     block with remote rows, a hand value)
   farskip_pair, regular_pair ....... pinned (zero-output equality, conservation)
   farskip_stack, regular_stack ..... pinned (zero-output equality, conservation,
                                      one layer = the block, the dropped dependency)

@@ -474,3 +474,78 @@ def test_route_given_matches_route_on_its_own_selection():
     flipped = own["me"]["ids"][:, ::-1].copy()   # same experts, other slot order
     other = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, ids_given=flipped)
     assert np.allclose(own["routed"], other["routed"], rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- token-by-token MoE
+def _dense_mask_routed(cfg, x, ids, w, gu, dn, y_rows):
+    """MoE(A) = sum_j G_j MLP^j(A) (Section 2.1) as a dense mixture: every
+    local expert evaluated on every token at once, weighted by a gate matrix
+    G [N, E] that is zero off the selection; the rows of experts on other
+    ranks come from y_rows[t, j]."""
+    N, k = ids.shape
+    lo = cfg.ep_rank * cfg.n_local
+    G = np.zeros((N, cfg.n_experts))
+    np.put_along_axis(G, ids.astype(np.int64), w, axis=1)
+    out = np.zeros_like(x)
+    for e in range(cfg.n_local):
+        h = x @ gu[e][:cfg.ffn].T.astype(np.float64)
+        u = x @ gu[e][cfg.ffn:].T.astype(np.float64)
+        out += G[:, lo + e:lo + e + 1] * ((h / (1 + np.exp(-h)) * u) @ dn[e].T.astype(np.float64))
+    remote = (ids < lo) | (ids >= lo + cfg.n_local)
+    out += np.einsum("tj,tjd->td", np.where(remote, w, 0.0), y_rows)
+    return out
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(ep_size=3, ep_rank=1),
+                                dict(ep_size=2, ep_rank=1, score="sigmoid", norm_topk=True),
+                                dict(score="sigmoid", n_groups=3, topk_groups=2, top_k=3,
+                                     ep_size=3, ep_rank=2)])
+def test_tokens_direct_equals_dense_mask_and_packed_block(kw):
+    # moe_tokens_direct evaluates the experts token by token with no plan or
+    # pack.  It must equal (1) the dense gate-matrix mixture and (2) the
+    # packed data flow of moe_block (pinned above), with the rows of other
+    # ranks' experts taken from the return buffer at the plan row of each
+    # (token, slot).  Ranks other than 0 make a local index off by the
+    # rank's first expert fail, and every case mixes local and remote rows.
+    cfg = _tiny_cfg(n_tokens=17, **kw)
+    g = rng(26)
+    x_all, wr, bias, gu, dn, yr = _tiny_inputs(cfg, g)
+    out = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, y_remote=yr)
+    me = out["me"]
+    ids, w, k = me["ids"], me["w"], cfg.top_k
+    lo = cfg.ep_rank * cfg.n_local
+    local = (ids >= lo) & (ids < lo + cfg.n_local)
+    assert local.any()
+    if cfg.ep_size > 1:
+        assert (~local).any()
+    s2r = me["plan"]["slot_to_row"]
+    y_rows = np.zeros((cfg.n_tokens, k, cfg.hidden))
+    if yr is not None:
+        y_rows = yr.astype(np.float64)[s2r.reshape(cfg.n_tokens, k)]
+    x = x_all[cfg.ep_rank].astype(np.float64)
+    direct = oracle.moe_tokens_direct(cfg, x, ids, w, lambda e: (gu[e], dn[e]), y_rows)
+    assert np.allclose(direct, _dense_mask_routed(cfg, x, ids, w, gu, dn, y_rows),
+                       rtol=1e-12, atol=1e-12)
+    assert np.allclose(direct, out["routed"], rtol=1e-12, atol=1e-12)
+    # tokens are independent: a subset in any order gives the same rows
+    sub = np.array([5, 0, 16, 9])
+    part = oracle.moe_tokens_direct(cfg, x[sub], ids[sub], w[sub], lambda e: (gu[e], dn[e]),
+                                    y_rows[sub])
+    assert np.allclose(part, direct[sub], rtol=1e-14, atol=1e-14)
+
+
+def test_tokens_direct_hand_value():
+    # One local expert of width 1 with gate and up weights e_0 and down
+    # weights 1: MLP(x) = SiLU(x_0) * x_0 in every output column.  Token
+    # x_0 = 2 with weight 0.5 gives 0.5 * 2 * 2 / (1 + e^-2); a remote row of
+    # 3s with weight 0.25 adds 0.75.
+    cfg = _tiny_cfg(n_tokens=1, hidden=2, n_experts=2, top_k=2, ffn=1, ep_size=2, ep_rank=1)
+    gu = np.array([[[1.0, 0.0], [1.0, 0.0]]])
+    dn = np.array([[[1.0], [1.0]]])
+    x = np.array([[2.0, -7.0]])
+    ids = np.array([[1, 0]])
+    w = np.array([[0.5, 0.25]])
+    got = oracle.moe_tokens_direct(cfg, x, ids, w, lambda e: (gu[e], dn[e]),
+                                   [[None, np.array([3.0, 3.0])]])
+    want = 0.5 * 4.0 / (1.0 + math.exp(-2.0)) + 0.75
+    assert np.allclose(got, [[want, want]], rtol=1e-15, atol=0)
