@@ -4,10 +4,13 @@ One step = one pass of the whole hot path over one batch: router + top-k,
 dispatch plan + pack, the dispatch stand-in copy on a second stream, shared
 and routed grouped SwiGLU experts, Combine and the deferred residual add
 (fs_moe_block_forward BEGIN + FINISH).  The default workload is the
-DeepSeek-V2-Lite-shaped layer (4096 tokens, d 2048, 64 experts top-6, two
-shared experts of width 1408, bf16), inputs resident in HBM.
+Llama-4-Scout-shaped layer (8192 tokens, d 5120, 16 experts top-1 sigmoid
+with a uniform selection bias, one shared expert, expert FFN 8192, bf16),
+the largest single-GPU workload, inputs resident in HBM.  The same step is
+then timed on the DeepSeek-V2-Lite-shaped layer and the DeepSeek-V3-shaped
+prefill and decode ranks (``--extra``), reported under ``workloads``.
 
-    python bench.py [--steps K] [--warmup W] [--config NAME] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--extra A,B] [--gpus 1]
 
 Prints one JSON line.
 """
@@ -162,6 +165,13 @@ def cpu_baseline(cfg, wl, sample_tokens):
 
     import oracle
     f64 = lambda t: None if t is None else t.detach().float().cpu().numpy().astype(np.float64)
+    if sample_tokens <= 0:
+        # about 1 TFLOP of fp64 work per pass: router, the k routed experts
+        # (local ones only when R > 1: about k / R per token) and the shared
+        # experts, 6 d F flops per SwiGLU row
+        per_token = 2 * cfg.hidden * cfg.n_experts + 6 * cfg.hidden * (
+            cfg.top_k / cfg.ep_size * cfg.ffn + cfg.n_shared * cfg.ffn_shared)
+        sample_tokens = max(64, int(1e12 / per_token))
     n = min(sample_tokens, cfg.n_tokens)
     x = f64(wl.x[:n])
     wr, bias = f64(wl.w_router), f64(wl.bias)
@@ -178,7 +188,11 @@ def cpu_baseline(cfg, wl, sample_tokens):
             z32 = oracle.logits_routing_f32(x, wr)
             ids, w, _, _ = oracle.route(z32, cfg.score, cfg.top_k, cfg.n_groups, cfg.topk_groups,
                                         cfg.norm_topk, cfg.routed_scale, bias)
-            rows = [[yr[t * cfg.top_k + j] for j in range(cfg.top_k)] for t in range(n)]
+            # the sample's own plan; the other ranks' experts return their
+            # rows at its positions in the return buffer
+            plan = oracle.dispatch_plan(ids, cfg.n_experts, cfg.ep_size)
+            s2r = plan["slot_to_row"]
+            rows = [[yr[s2r[t * cfg.top_k + j]] for j in range(cfg.top_k)] for t in range(n)]
             routed = oracle.moe_tokens_direct(cfg, x, ids, w, lambda e: (gu[e], dn[e]), rows)
             shared = oracle.shared_ffn(x, sgu, sdn)
         oracle.residual_add(x, shared, routed)
@@ -396,14 +410,21 @@ def bench_replicated(args, cfg, torch, L):
     print(json.dumps(res), flush=True)
 
 
+EXTRA_DEFAULT = "dsv2lite,dsv3_prefill,dsv3_decode"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="dsv2lite")
-    ap.add_argument("--cpu-sample", type=int, default=4096,
-                    help="tokens of the workload the oracle runs on the host")
+    ap.add_argument("--config", default="scout")
+    ap.add_argument("--extra", default=EXTRA_DEFAULT,
+                    help="comma-separated workloads also timed in the same run (same steps), "
+                         "reported under 'workloads' in the JSON line; '' for none")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="tokens of the workload the oracle runs on the host (0: as many as about "
+                         "1 TFLOP of fp64 work per pass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serial", action="store_true", help="no second stream")
     ap.add_argument("--rotate", type=int, default=4, help="input sets rotated across steps")
@@ -428,19 +449,40 @@ def main():
 
     import torch
 
-    import paper_2511_11505_amd as fs
     from paper_2511_11505_amd import _lib as L
-    from workloads import CONFIGS, make_workload
-    from workloads.generate import merge_shared, source_tokens
+    from workloads import CONFIGS
 
     cfg = CONFIGS[args.config]
-    dev = "cuda:0"
     torch.cuda.set_device(0)
     if cfg.ep_mode == "allreduce":
         args.layers = args.layers or 4
         return bench_replicated(args, cfg, torch, L)
     if args.layers > 0:
         return bench_layers(args, cfg, torch, L)
+    res = bench_block(args, cfg, torch, L, with_cpu=not args.no_cpu_baseline)
+    extra = [n for n in args.extra.split(",") if n and n != cfg.name]
+    if extra:
+        res["workloads_note"] = ("the same step timed on the other block workloads in this run "
+                                 "(same steps and warm-up, no CPU leg); roofline as in the headline")
+        res["workloads"] = {}
+        for name in extra:
+            torch.cuda.empty_cache()
+            r2 = bench_block(args, CONFIGS[name], torch, L, with_cpu=False)
+            res["workloads"][name] = {key: r2[key] for key in (
+                "value", "unit", "ms_per_step", "config", "roofline", "ffn", "permute_frac_hbm",
+                "step_roofline_frac", "block_roofline_frac", "kernels_us") if key in r2}
+            torch.cuda.empty_cache()
+    print(json.dumps(res), flush=True)
+
+
+def bench_block(args, cfg, torch, L, with_cpu):
+    """Time fs_moe_block_forward (BEGIN + FINISH) on one workload; returns
+    the result dict of the JSON line."""
+    import paper_2511_11505_amd as fs
+    from workloads import make_workload
+    from workloads.generate import merge_shared, source_tokens
+
+    dev = "cuda:0"
     t_setup = time.perf_counter()
     wl = make_workload(cfg, dev)
     sh_gu = sh_dn = None
@@ -639,13 +681,14 @@ def main():
     if fp8_routed:
         res["grouped_gemm_frac_bf16_peak"] = None
         res["grouped_gemm_frac_fp8_peak"] = None if roof is None else roof["mfma_frac"]
-    if not args.no_cpu_baseline and not fp8_routed:
+    if with_cpu and not fp8_routed:
         try:
             res["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_sample)
         except Exception as e:  # report, do not hide the GPU number
             res["cpu_baseline"] = {"error": repr(e)}
     blk.close()
-    print(json.dumps(res), flush=True)
+    del blk, wl, xs, partials
+    return res
 
 
 if __name__ == "__main__":
