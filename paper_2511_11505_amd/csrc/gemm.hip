@@ -388,220 +388,6 @@ __device__ __forceinline__ void store_tile(floatx16 (&acc)[TM][TN], unsigned cha
   __syncthreads();
 }
 
-template <int MODE, int BM, int BN, int BK, int STAGES, int WM, int WN, int OCC>
-__global__ __launch_bounds__(64 * WM * WN, OCC) void gemm_bf16_dma_kernel(
-    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
-    int NOUT, bf16_t* __restrict__ C, int ldc) {
-  constexpr int NW = WM * WN, NT = 64 * NW;
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int ROWB = BK * 2;                       // bytes per staged row
-  constexpr int CPR = BK / 8;                        // 16-byte chunks per staged row
-  constexpr int RPB = 1024 / ROWB;                   // rows per 1 KB DMA block
-  constexpr int SWD = 16 / CPR;                      // rows sharing one swizzle value
-  constexpr int STAGE = (BM + BN) * ROWB;            // bytes per ring slot
-  constexpr int A_LD = BM / RPB / NW, B_LD = BN / RPB / NW;  // DMA blocks per wave per slot
-  constexpr int NLD = A_LD + B_LD;
-  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
-  constexpr int ECOL = 128;                          // output columns staged per epilogue pass
-  constexpr int CST = ECOL + 8;                      // epilogue LDS row stride (bf16)
-  constexpr int KS = BK / 16;                        // MFMA K steps per block
-  static_assert(BK == 32 || BK == 64, "K block");
-  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (NW * RPB) == 0 && BN % (NW * RPB) == 0, "tile");
-  static_assert(NCOL % ECOL == 0, "epilogue passes");
-  static_assert(BM * CST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
-  static_assert(MODE != MODE_GATEUP || (TN % 2 == 0 && WN * WTN / 2 == ECOL), "gate/up pairing");
-  static_assert(MODE != MODE_DOWN || ECOL % WTN == 0, "a wave's columns stay in one pass");
-  static_assert(STAGES >= 2 && STAGES <= 6, "ring");
-  static_assert(NLD * (STAGES - 2) < 64, "vmcnt range");
-
-  __shared__ int s_goff[kMaxGroups + 1];
-  __shared__ int s_tpre[kMaxGroups + 1];
-  __shared__ int s_wtot[NT / 64];
-  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
-
-  const int nn = NOUT / NCOL;
-  const int64_t total = (int64_t)nn * s_tpre[G];
-  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
-  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
-  const int64_t stride = gridDim.x / kXcd;
-  const int KT = K / BK;
-  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
-  // This lane's place inside a 1 KB DMA block: row l / CPR, position l % CPR;
-  // it fetches the logical chunk stored at that position.
-  const int drow = lane / CPR, dpos = lane % CPR;
-  auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
-
-  // fragment rows of this lane and their byte offsets inside a slot
-  int aoff[TM], boff[TN], asw[TM], bsw[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = wm * WTM + i * 32 + (lane & 31);
-    aoff[i] = r * ROWB;
-    asw[i] = (r / SWD) % CPR;
-  }
-#pragma unroll
-  for (int jn = 0; jn < TN; ++jn) {
-    int r;
-    if (MODE == MODE_GATEUP)
-      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
-    else
-      r = wn * WTN + jn * 32;
-    r += lane & 31;
-    boff[jn] = BM * ROWB + r * ROWB;
-    bsw[jn] = (r / SWD) % CPR;
-  }
-
-  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
-    const int64_t L = xcd_base + j;
-    if (L >= total) break;
-    const int g = find_group(s_tpre, G, nn, L);
-    const int Tg = s_tpre[g + 1] - s_tpre[g];
-    const int64_t local = L - (int64_t)nn * s_tpre[g];
-    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
-    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
-    const int m0 = mt * BM, n0 = nt * NCOL;
-    const bf16_t* Bg = B + (size_t)g * bstride;
-
-    const bf16_t* pa[A_LD];
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int blk = wave * A_LD + i;
-      int m = m0 + blk * RPB + drow;
-      if (m >= rows_g) m = rows_g - 1;
-      const int grow = row_base + m;
-      const int64_t src = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      pa[i] = A + src * K + dchunk(blk) * 8;
-    }
-    const bf16_t* pb[B_LD];
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int blk = wave * B_LD + i;
-      const int r = blk * RPB + drow;
-      int wrow;
-      if (MODE == MODE_GATEUP)
-        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
-      else
-        wrow = n0 + r;
-      pb[i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
-    }
-    const unsigned ring_lds = lds_addr(ring);
-    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
-    auto issue = [&](int kt) {
-      const unsigned slot = ring_lds + (unsigned)((kt % STAGES) * STAGE);
-#pragma unroll
-      for (int i = 0; i < A_LD; ++i) dma16_at(pa[i] + kt * BK, slot + (wave_u * A_LD + i) * 1024u);
-#pragma unroll
-      for (int i = 0; i < B_LD; ++i)
-        dma16_at(pb[i] + kt * BK, slot + (unsigned)(BM * ROWB) + (wave_u * B_LD + i) * 1024u);
-    };
-
-    floatx16 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < TN; ++jn)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
-
-#pragma unroll
-    for (int st = 0; st < STAGES - 1; ++st)
-      if (st < KT) issue(st);
-    for (int kt = 0; kt < KT; ++kt) {
-      // block kt has landed once at most the blocks issued after it remain
-      const int after = min(STAGES - 2, KT - 1 - kt);
-      if (after >= STAGES - 2)
-        wait_vmcnt<(STAGES - 2) * NLD>();
-      else if (after == 3)
-        wait_vmcnt<(STAGES > 5 ? 3 : 0) * NLD>();
-      else if (after == 2)
-        wait_vmcnt<(STAGES > 4 ? 2 : 0) * NLD>();
-      else if (after == 1)
-        wait_vmcnt<(STAGES > 3 ? 1 : 0) * NLD>();
-      else
-        wait_vmcnt<0>();
-      barrier_nofence();
-      if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1);
-      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
-      // all fragments of the K block first, then its MFMAs: the LDS latency
-      // is exposed once per block instead of once per 16-wide K step
-      bf16x8 af[KS][TM], bfr[KS][TN];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int c = ks * 2 + (lane >> 5);   // logical 16-byte chunk of this lane
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[ks][i] = *reinterpret_cast<const bf16x8*>(slot + aoff[i] + ((c ^ asw[i]) << 4));
-#pragma unroll
-        for (int jn = 0; jn < TN; ++jn)
-          bfr[ks][jn] = *reinterpret_cast<const bf16x8*>(slot + boff[jn] + ((c ^ bsw[jn]) << 4));
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int jn = 0; jn < TN; ++jn)
-            acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][jn],
-                                                                 acc[i][jn], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, KS * (TM + TN), 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, KS * TM * TN, 0);
-    }
-
-    // Epilogue: accumulator element v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
-    // column l%32 of its 32x32 tile.  Passes of 128 output columns are
-    // staged as bf16 in the ring, then stored as 16-byte row chunks.
-    bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
-    constexpr int PASSES = NCOL / ECOL;
-#pragma unroll
-    for (int pass = 0; pass < PASSES; ++pass) {
-      barrier_nofence();
-      if (MODE == MODE_GATEUP || (wn * WTN) / ECOL == pass) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            if (MODE == MODE_GATEUP) {
-#pragma unroll
-              for (int jn = 0; jn < TN / 2; ++jn) {
-                const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
-                const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(swiglu_bf16_epi(gt, up));
-              }
-            } else {
-#pragma unroll
-              for (int jn = 0; jn < TN; ++jn) {
-                const int col = (wn * WTN) % ECOL + jn * 32 + (lane & 31);
-                Cs[r * CST + col] = f2bf(acc[i][jn][v]);
-              }
-            }
-          }
-        }
-      }
-      __syncthreads();
-      constexpr int CPRC = ECOL / 8;   // 16-byte chunks per staged row
-#pragma unroll 4
-      for (int c = tid; c < BM * CPRC; c += NT) {
-        const int r = c / CPRC, ch = c % CPRC;
-        const int m = m0 + r;
-        if (m < rows_g) {
-          const int grow = row_base + m;
-          const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-          st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
-               *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
-        }
-      }
-    }
-    __syncthreads();   // the ring is reused by the next tile
-  }
-}
-
 // ---------------------------------------------------------------- bf16 MFMA, interleaved
 // Same tiles, ring and swizzle as above, with the memory work hidden under
 // the MFMAs by a rolling pipeline over 16-wide K steps.  Each step first
@@ -1583,26 +1369,15 @@ constexpr int kBM = 128, kBN = 128, kBK = 64;
 // groups average at least 1024 rows and its tiles fill the 256 compute
 // units, and the 128-row interleaved ring (5) otherwise.  nout: output
 // columns of the pass (F for gate/up, d for down).
-// FS_GEMM_TILE / FS_GEMM_TILE_DOWN (0-9) force a variant, for tuning.
 int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
-  static const int gu_env = [] {
-    const char* e = getenv("FS_GEMM_TILE");
-    return e ? atoi(e) : -1;
-  }();
-  static const int dn_env = [] {
-    const char* e = getenv("FS_GEMM_TILE_DOWN");
-    return e ? atoi(e) : -1;
-  }();
   if (down) {
     if (nout % 256 != 0) return 10;   // the only down variant for such widths
-    if (dn_env >= 0) return dn_env;
     const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 256);
     // 256-row tiles only for long groups (a dense shared expert): on routed
     // groups of about a thousand rows the 128-row kernel, which primes each
     // tile's first K blocks during the previous tile, is faster.
     return K < 2816 && max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
   }
-  if (gu_env >= 0 && gu_env != 10) return gu_env;   // 10 is down only
   const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 128);
   return max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 8 : 5;
 }
@@ -1637,14 +1412,6 @@ int64_t persistent_grid(int64_t max_rows, int G, int BM, int nn, int occ) {
 // One bf16 GEMM pass with the LDS-ring variant v.  NCOL output columns per
 // tile: BN / 2 for gate/up (a tile holds matching gate and up rows), BN for
 // down.
-template <int MODE, int BM, int BN, int BK, int ST, int WM, int WN, int OCC>
-void run_dma(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
-             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
-  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
-  const int64_t g = grid_for(m_total, G, BM, NOUT / NCOL);
-  launch_k(gemm_bf16_dma_kernel<MODE, BM, BN, BK, ST, WM, WN, OCC>,
-      (unsigned)g, 64 * WM * WN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
-}
 // K split of an interleaved-ring pass: `splits` slices of `kps` K blocks
 // with fp32 partials in P (splits == 1: no split).
 struct KSplit {
@@ -1688,30 +1455,23 @@ void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
   launch_k(gemm_bf16_rs_kernel<MODE, BM, BN, BK>,
       (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
 }
-// Variants 0-9 have BN = 256 and BK <= 64: they need NOUT % 128 == 0 for
-// gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
-// only) has 128 x 128 tiles for NOUT % 128 == 0.
-// (A K split applies to the interleaved variants 5 and 7 only.)
+// Variants 5, 7 and 8 have BN = 256 and BK = 64: they need NOUT % 128 == 0
+// for gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
+// only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to the
+// interleaved variants 5 and 7 only.)
 template <int MODE>
 void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
                int64_t m_total, const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc,
                hipStream_t s, const KSplit& sp = KSplit{}) {
 #define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
   switch (v) {
-    case 0: run_dma<MODE, 128, 256, 64, 3, 2, 2, 1>(FS_ARGS); break;
-    case 1: run_dma<MODE, 128, 256, 32, 6, 2, 2, 1>(FS_ARGS); break;
-    case 2: run_dma<MODE, 256, 256, 32, 4, 2, 4, 1>(FS_ARGS); break;
-    case 3: run_dma<MODE, 256, 256, 64, 2, 2, 4, 1>(FS_ARGS); break;
-    case 5: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS, sp); break;
-    case 6: run_il<MODE, 128, 256, 32, 3, 2>(FS_ARGS); break;
     case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS, sp); break;
     case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
-    case 9: run_il<MODE, 256, 256, 32, 4, 1>(FS_ARGS); break;
     case 10:
       // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
       if constexpr (MODE == MODE_DOWN) run_il<MODE, 128, 128, 64, 4, 1>(FS_ARGS);
       break;
-    default: run_dma<MODE, 128, 256, 32, 3, 2, 2, 2>(FS_ARGS); break;
+    default: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS, sp); break;   // 5
   }
 #undef FS_ARGS
 }
@@ -1732,12 +1492,8 @@ size_t stream_partial_bytes(int dtype, int64_t max_rows, int ffn, int d) {
 // weight tiles x slices) to fill the chip, at least two K blocks per slice,
 // and partials that fit the buffer above.
 int stream_splits(int64_t max_rows, int G, int nw, int K, size_t partial_bytes) {
-  static const int env = [] {
-    const char* e = getenv("FS_STREAM_SPLITS");
-    return e ? atoi(e) : -1;
-  }();
   const int64_t tiles = (int64_t)G * (nw / kStreamWrows);
-  int64_t s = env >= 1 ? env : cdiv64(kStreamWgs, tiles);
+  int64_t s = cdiv64(kStreamWgs, tiles);
   const int64_t by_k = (K / 64) / 2;
   if (s > by_k) s = by_k;
   const int64_t by_mem = (int64_t)(partial_bytes / ((size_t)(max_rows > 0 ? max_rows : 1) * nw * 4));
@@ -1745,26 +1501,15 @@ int stream_splits(int64_t max_rows, int G, int nw, int K, size_t partial_bytes) 
   return s < 1 ? 1 : (int)s;
 }
 
-// FS_GEMM_STREAM=0 never takes the streaming kernel, =2 takes it whenever
-// the groups average at most 64 rows (tuning); unset or 1: the rule below.
-int stream_mode() {
-  static const int mode = [] {
-    const char* e = getenv("FS_GEMM_STREAM");
-    return e ? atoi(e) : 1;
-  }();
-  return mode;
-}
-
 // The streaming kernel takes a pass when its groups average at most 64 rows
 // and the LDS-ring kernel's 128 x 256 tiles would not give every CU one.
 bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
-  const int mode = stream_mode();
-  if (mode == 0 || dtype != 1 || max_rows > kStreamMaxRows || max_rows > (int64_t)64 * G ||
-      ffn % 64 != 0 || d % 64 != 0)
+  if (dtype != 1 || max_rows > kStreamMaxRows || max_rows > (int64_t)64 * G || ffn % 64 != 0 ||
+      d % 64 != 0)
     return false;
   const int64_t ring_tiles =
       (int64_t)G * std::max<int64_t>(1, cdiv64(max_rows, (int64_t)128 * G)) * std::max(1, ffn / 128);
-  return mode == 2 || ring_tiles < 256;
+  return ring_tiles < 256;
 }
 
 // One FP8 GEMM pass, 128 x 256 tiles except where the bf16 rule takes the
@@ -1789,21 +1534,12 @@ void gemm_pass_f8(int v, const uint8_t* A, const int32_t* rows, const int32_t* g
 // within pbytes.  A pass with at least one tile per CU is not split: there
 // the fp32 partials and the reduction cost more than the balance gains
 // (weight-streaming decode passes slow down by a sixth when split).
-// FS_GEMM_SPLITS forces a count (tuning).
 int ring_splits(bool gateup, int BM, int64_t max_rows, int G, int KT, int NOUT, size_t pbytes) {
-  static const int env = [] {
-    const char* e = getenv("FS_GEMM_SPLITS");
-    return e ? atoi(e) : -1;
-  }();
   const int NCOL = gateup ? 128 : 256;
   const int64_t tiles =
       (int64_t)G * std::max<int64_t>(1, cdiv64(max_rows, (int64_t)BM * G)) * (NOUT / NCOL);
   const int64_t want = (int64_t)8 * num_cus();
-  int64_t sl;
-  if (env >= 1)
-    sl = env;
-  else
-    sl = tiles >= num_cus() ? 1 : std::min<int64_t>(8, cdiv64(want, tiles));
+  int64_t sl = tiles >= num_cus() ? 1 : std::min<int64_t>(8, cdiv64(want, tiles));
   sl = std::min<int64_t>(sl, KT / 4);
   const size_t per = (size_t)std::max<int64_t>(max_rows, 1) * (gateup ? 2 * NOUT : NOUT) * 4;
   while (sl > 1 && (size_t)sl * per > pbytes) --sl;
