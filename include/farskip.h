@@ -202,6 +202,28 @@ fs_status fs_dispatch_pack_fp8(const fs_moe_desc* desc, const int32_t* topk_ids,
                                int32_t* row_to_slot, uint8_t* send_codes, float* send_scales,
                                void* ws, size_t ws_bytes, fs_stream stream);
 
+/* Dispatch plan and pack for callers that cannot allocate memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments and results as fs_dispatch_pack without the
+ * workspace: the plan's scratch is a fixed 4 MiB device array inside the
+ * library, one per device, kept until the process ends; the call allocates
+ * and frees nothing.  The plan kernels overwrite every scratch word they
+ * read, so nothing carries over between calls.
+ *   Limit     ceil(N / 64) * E <= 262144 (e.g. 32768 tokens over 512
+ *             experts); larger shapes return FS_ERR_UNSUPPORTED before
+ *             anything is enqueued.
+ *   Device    The array of the current device is used; a non-NULL stream
+ *             must belong to that device (FS_ERR_INVALID otherwise).
+ *   Races     Every call on one device shares that device's array: calls
+ *             whose work overlaps on one device (other streams, other
+ *             threads) race and must be ordered by the caller.
+ *   Timing    No fs_profile timing windows are opened. */
+fs_status fs_dispatch_pack_noalloc(const fs_moe_desc* desc, const int32_t* topk_ids,
+                                   const void* x, int32_t* expert_counts,
+                                   int32_t* expert_offsets, int32_t* rank_offsets,
+                                   int32_t* slot_to_row, int32_t* row_to_slot, void* send,
+                                   fs_stream stream);
+
 /* Rows landing on this rank's experts after Dispatch (Section 2.1).  The
  * receive buffer holds, for every source rank s, that rank's whole send
  * buffer at rows [s*N*k, (s+1)*N*k).

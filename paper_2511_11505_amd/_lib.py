@@ -64,6 +64,8 @@ _SIGS = {
     "fs_dispatch_pack": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_dispatch_pack_fp8": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                     _sz, _vp]),
+    "fs_dispatch_pack_noalloc": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, _vp]),
     "fs_receive_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
     "fs_local_rows": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
     "fs_grouped_expert_ffn_gathered": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp,
@@ -182,6 +184,14 @@ def fs_dispatch_pack(desc, topk_ids, x, expert_counts, expert_offsets, rank_offs
     _check(load().fs_dispatch_pack(ctypes.byref(desc), ptr(topk_ids), ptr(x), ptr(expert_counts),
                                    ptr(expert_offsets), ptr(rank_offsets), ptr(slot_to_row),
                                    ptr(row_to_slot), ptr(send), wp, wb, stream_handle(stream)))
+
+
+def fs_dispatch_pack_noalloc(desc, topk_ids, x, expert_counts, expert_offsets, rank_offsets,
+                             slot_to_row, row_to_slot, send, stream=None):
+    _check(load().fs_dispatch_pack_noalloc(ctypes.byref(desc), ptr(topk_ids), ptr(x),
+                                           ptr(expert_counts), ptr(expert_offsets),
+                                           ptr(rank_offsets), ptr(slot_to_row), ptr(row_to_slot),
+                                           ptr(send), stream_handle(stream)))
 
 
 def fs_dispatch_pack_fp8(desc, topk_ids, x, expert_counts, expert_offsets, rank_offsets, slot_to_row,

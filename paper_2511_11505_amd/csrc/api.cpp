@@ -430,6 +430,56 @@ fs_status fs_dispatch_pack(const fs_moe_desc* desc, const int32_t* topk_ids, con
                         slot_to_row, row_to_slot, send, ws, S(stream));
 }
 
+fs_status fs_dispatch_pack_noalloc(const fs_moe_desc* desc, const int32_t* topk_ids,
+                                   const void* x, int32_t* expert_counts,
+                                   int32_t* expert_offsets, int32_t* rank_offsets,
+                                   int32_t* slot_to_row, int32_t* row_to_slot, void* send,
+                                   fs_stream stream) {
+  fs_status st = check_desc(desc);
+  if (st != FS_OK) return st;
+  if (desc->n_tokens == 0) return FS_OK;
+  NEED4(topk_ids, "topk_ids");
+  NEED4(expert_counts, "expert_counts");
+  NEED4(expert_offsets, "expert_offsets");
+  NEED4(rank_offsets, "rank_offsets");
+  NEED4(slot_to_row, "slot_to_row");
+  NEED4(row_to_slot, "row_to_slot");
+  OPT(send, "send");
+  if (send) NEED(x, "x");
+  const size_t need = fs::plan_ws_bytes(desc->n_tokens, desc->n_experts);
+  if (need > fs::kPlanScratchBytes)
+    return fail(FS_ERR_UNSUPPORTED,
+                "fs_dispatch_pack_noalloc: the plan needs " + std::to_string(need) +
+                    " bytes of scratch, more than its fixed " +
+                    std::to_string(fs::kPlanScratchBytes) +
+                    " (ceil(n_tokens / 64) * n_experts must be <= 262144); use fs_dispatch_pack");
+  hipStream_t s = S(stream);
+  if (s) {
+    int cur = 0;
+    hipDevice_t sdev = 0;
+    FS_HIP(hipGetDevice(&cur), "hipGetDevice");
+    FS_HIP(hipStreamGetDevice(s, &sdev), "hipStreamGetDevice");
+    if ((int)sdev != cur)
+      return fail(FS_ERR_INVALID, "fs_dispatch_pack_noalloc: the stream belongs to device " +
+                                      std::to_string((int)sdev) + ", not the current device " +
+                                      std::to_string(cur));
+  }
+  void* scratch = nullptr;
+  FS_HIP(fs::plan_scratch(&scratch), "plan scratch address");
+  // the plan kernels write every scratch word they later read, so the last
+  // call's contents need no clearing; no timing windows are opened (they
+  // may create events)
+  FS_HIP(fs::launch_plan(topk_ids, desc->n_tokens, desc->top_k, desc->n_experts, desc->ep_size,
+                         expert_counts, expert_offsets, rank_offsets, slot_to_row, row_to_slot,
+                         scratch, s),
+         "plan");
+  if (send)
+    FS_HIP(fs::launch_pack(desc->dtype, x, slot_to_row, desc->n_tokens, desc->top_k,
+                           desc->hidden, send, s),
+           "pack");
+  return FS_OK;
+}
+
 fs_status fs_receive_rows(const fs_moe_desc* desc, const int32_t* src_counts,
                           const int32_t* src_offsets, int32_t* group_rows, int32_t* group_offsets,
                           fs_stream stream) {

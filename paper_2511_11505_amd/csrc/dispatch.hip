@@ -16,8 +16,17 @@
 // rows of its own experts: a contiguous block of the plan's rows, read back
 // to token indices so the expert GEMM gathers them straight from x.
 
+#include <mutex>
+
 #include "common.hpp"
 #include "internal.hpp"
+
+// Plan workspace of the allocation-free dispatch entry point
+// (fs_dispatch_pack_noalloc): a fixed device array that every device holding
+// this library keeps until the process ends.  Host code never passes its
+// name to a kernel (on the host the name is a stand-in, not a device
+// address); it uses the per-device address plan_scratch() returns.
+static __device__ __align__(256) unsigned char scratch[fs::kPlanScratchBytes];
 
 namespace fs {
 namespace {
@@ -292,6 +301,27 @@ __global__ __launch_bounds__(256) void local_rows_kernel(const int32_t* __restri
 size_t plan_ws_bytes(int N, int E) {
   const size_t n_tiles = (size_t)(N + kTile - 1) / kTile;
   return n_tiles * E * (sizeof(uint64_t) + 2 * sizeof(int32_t));
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device with that device current and kept.
+hipError_t plan_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[kPlanScratchMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kPlanScratchMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* counts,

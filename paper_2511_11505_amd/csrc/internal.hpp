@@ -39,6 +39,12 @@ hipError_t launch_topk(const float* src, int n_partials, int N, int E, const flo
 
 // ---- dispatch (dispatch.hip)
 size_t plan_ws_bytes(int N, int E);
+// Fixed plan workspace of the allocation-free dispatch entry point: 4 MiB,
+// enough for ceil(N / 64) * E <= 262144 (e.g. 32768 tokens over 512
+// experts).  plan_scratch() gives its device address on the current device.
+constexpr size_t kPlanScratchBytes = (size_t)4 << 20;
+constexpr int kPlanScratchMaxDevices = 64;
+hipError_t plan_scratch(void** out);
 hipError_t launch_plan(const int32_t* ids, int N, int k, int E, int R, int32_t* counts,
                        int32_t* offsets, int32_t* rank_offsets, int32_t* slot_to_row,
                        int32_t* row_to_slot, void* ws, hipStream_t s);

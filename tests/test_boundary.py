@@ -134,6 +134,14 @@ def test_other_entry_point_checks():
            (FAKE, 1 << 30), stream=0)
     expect(L.FS_ERR_WORKSPACE, L.fs_dispatch_pack, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
            (FAKE, 8), stream=0)
+    # the allocation-free dispatch: pointer checks, and shapes beyond its
+    # fixed scratch rejected before any HIP call
+    expect(L.FS_ERR_INVALID, L.fs_dispatch_pack_noalloc, d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+           FAKE, stream=0)
+    big = desc("dsv2lite", n_experts=512, n_tokens=(262144 // 512) * 64 + 1)
+    msg = expect(L.FS_ERR_UNSUPPORTED, L.fs_dispatch_pack_noalloc, big, FAKE, FAKE, FAKE, FAKE, FAKE,
+                 FAKE, FAKE, FAKE, stream=0)
+    assert "scratch" in msg
     expect(L.FS_ERR_INVALID, L.fs_grouped_expert_ffn, d, 32, 2048, FAKE, None, None, 100, FAKE, FAKE,
            FAKE, (FAKE, 1 << 40), stream=0)
     expect(L.FS_ERR_UNSUPPORTED, L.fs_grouped_expert_ffn, d, 32, 100, FAKE, None, FAKE, 100, FAKE,
