@@ -154,7 +154,7 @@ struct Carve {
 };
 
 size_t router_bytes(const fs_moe_desc* d) {
-  return align256(fs::router_ws_bytes(d->n_tokens, d->hidden, d->n_experts));
+  return align256(fs::router_ws_bytes(d->dtype, d->n_tokens, d->hidden, d->n_experts));
 }
 size_t plan_bytes(const fs_moe_desc* d) { return align256(fs::plan_ws_bytes(d->n_tokens, d->n_experts)); }
 
@@ -290,7 +290,7 @@ static fs_status router_impl(const fs_moe_desc* d, const void* x, const void* w_
   if (!logits_in) {
     Carve c{reinterpret_cast<char*>(ws)};
     float* scratch_logits = reinterpret_cast<float*>(c.take((size_t)N * E * sizeof(float)));
-    const bool split = fs::router_split(N, D, E);
+    const bool split = fs::router_split(d->dtype, N, D, E);
     float* dst;
     if (split) {
       dst = reinterpret_cast<float*>(c.take((size_t)fs::router_slices(D) * N * E * sizeof(float)));

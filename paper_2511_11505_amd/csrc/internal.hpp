@@ -29,8 +29,8 @@ inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t 
 
 // ---- router (router.hip)
 int router_slices(int d);
-bool router_split(int N, int d, int E);
-size_t router_ws_bytes(int N, int d, int E);
+bool router_split(int dtype, int N, int d, int E);
+size_t router_ws_bytes(int dtype, int N, int d, int E);
 hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, int d, int E,
                                 bool split, float* out, hipStream_t s);
 hipError_t launch_topk(const float* src, int n_partials, int N, int E, const float* bias,

@@ -173,6 +173,141 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const T* __restrict_
   }
 }
 
+// bf16 logits on the fp32 matrix cores.  v_mfma_f32_32x32x1_2b_f32 adds, for
+// each of two 32 x 32 blocks, one product per output: d = c + a * b.  A
+// bf16 product is exact in fp32, so a chain of these over ascending k is the
+// same sequence of rounded adds as the vector kernel's fused multiply-adds,
+// and the logits are identical bit for bit (checked on the device against
+// a sequential fp32 sum); the matrix cores run fp32 at twice the rate of
+// unpacked vector FMAs.  Lane layout: for block b, lanes [32b, 32b+32) give
+// the rows (A) and the columns (B); accumulator element v of lane l is block
+// v / 16, row 8 ((v % 16) / 4) + 4 (l / 32) + v % 4, column l % 32.
+//
+// A workgroup of four waves computes (32 WT) tokens x (64 WE) experts, each
+// wave 32 tokens x 64 experts: A lane l holds token l % 32 of its rows (the
+// same token in both halves), B lane l expert l of its columns.  The token
+// and expert rows of a 64-wide K chunk are staged in LDS (128-byte rows,
+// 16-byte chunk c of row r at position c ^ ((r / 2) % 8), so the 32 or 64
+// rows one read touches fall in different banks) by coalesced loads one
+// chunk ahead in registers, double-buffered with one barrier per chunk; a
+// lane then reads its eight k of a step as one 16-byte LDS read.
+typedef float floatx32 __attribute__((ext_vector_type(32)));
+
+template <int WT, int WE, bool SPLIT>
+__global__ __launch_bounds__(256) void router_mfma_kernel(const bf16_t* __restrict__ x,
+                                                          const bf16_t* __restrict__ w, int N,
+                                                          int d, int E, float* __restrict__ out) {
+  constexpr bool split = SPLIT;
+  static_assert(WT * WE == 4, "four waves");
+  constexpr int BT = 32 * WT, BE = 64 * WE, ROWS = BT + BE;
+  constexpr int LPT = ROWS * 8 / 256;                  // 16-byte loads per thread per chunk
+  static_assert(ROWS * 8 % 256 == 0, "whole load rounds");
+  __shared__ __align__(16) unsigned char sm[2][ROWS * 128];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wt = wave % WT, we = wave / WT;
+  const int t0 = blockIdx.x * BT, e0 = blockIdx.y * BE;
+  const int S = (d + kRouterSlice - 1) / kRouterSlice;
+  const int s_begin = split ? (int)blockIdx.z : 0;
+  const int s_end = split ? s_begin + 1 : S;
+  const int k_begin = s_begin * kRouterSlice;
+  const int k_end = min(d, s_end * kRouterSlice);
+  const int nch = (k_end - k_begin) / 64;            // d % 128 == 0: whole chunks
+
+  // staged loads: chunk q = tid + 256 i is row q / 8, 16-byte piece q % 8;
+  // rows past N / E read the last valid row (their outputs are not stored)
+  const bf16_t* src[LPT];
+  int dst[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int q = tid + 256 * i, row = q / 8, pc = q % 8;
+    const bf16_t* base = row < BT ? x + (size_t)min(t0 + row, N - 1) * d
+                                  : w + (size_t)min(e0 + row - BT, E - 1) * d;
+    src[i] = base + k_begin + pc * 8;
+    dst[i] = row * 128 + ((pc ^ ((row >> 1) & 7)) << 4);
+  }
+  uint4 stg[LPT];
+  auto gload = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) stg[i] = ld16(src[i] + 64 * c);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) st16(sm[buf] + dst[i], stg[i]);
+  };
+  const int ra = wt * 32 + (lane & 31), rb = BT + we * 64 + lane;
+  const int offa = ra * 128, swa = (ra >> 1) & 7, offb = rb * 128, swb = (rb >> 1) & 7;
+
+  floatx32 part, tot;
+#pragma unroll
+  for (int v = 0; v < 32; ++v) part[v] = tot[v] = 0.f;
+  auto store_out = [&](float* o, const floatx32& val) {
+#pragma unroll
+    for (int v = 0; v < 32; ++v) {
+      const int j = v & 15;
+      const int t = t0 + wt * 32 + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+      const int e = e0 + we * 64 + 32 * (v >> 4) + (lane & 31);
+      if (t < N && e < E) o[(size_t)t * E + e] = val[v];
+    }
+  };
+
+  if (nch > 0) {
+    gload(0);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) gload(c + 1);
+    const unsigned char* sb = sm[c & 1];
+    // eight k per step; the next step's operands are read during this one
+    // (the scheduling barriers keep the compiler from hoisting every step's
+    // reads and conversions, which would take registers from occupancy)
+    uint4 ua = *reinterpret_cast<const uint4*>(sb + offa + (swa << 4));
+    uint4 ub = *reinterpret_cast<const uint4*>(sb + offb + (swb << 4));
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      uint4 na = ua, nb = ub;
+      if (ks < 7) {
+        na = *reinterpret_cast<const uint4*>(sb + offa + (((ks + 1) ^ swa) << 4));
+        nb = *reinterpret_cast<const uint4*>(sb + offb + (((ks + 1) ^ swb) << 4));
+      }
+      const uint32_t av[4] = {ua.x, ua.y, ua.z, ua.w}, bv[4] = {ub.x, ub.y, ub.z, ub.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        part = __builtin_amdgcn_mfma_f32_32x32x1f32(__uint_as_float(av[h] << 16),
+                                                    __uint_as_float(bv[h] << 16), part, 0, 0, 0);
+        part = __builtin_amdgcn_mfma_f32_32x32x1f32(__uint_as_float(av[h] & 0xFFFF0000u),
+                                                    __uint_as_float(bv[h] & 0xFFFF0000u), part,
+                                                    0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      ua = na;
+      ub = nb;
+    }
+    // end of a slice: fold its sum in (or emit it)
+    const int kn = k_begin + 64 * (c + 1);
+    if (kn % kRouterSlice == 0 || kn == k_end) {
+      if constexpr (SPLIT) {
+        store_out(out + (size_t)((kn - 1) / kRouterSlice) * N * E, part);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 32; ++v) tot[v] = tot[v] + part[v];
+      }
+#pragma unroll
+      for (int v = 0; v < 32; ++v) part[v] = 0.f;
+    }
+    if (c + 1 < nch) lstore((c + 1) & 1);
+    __syncthreads();
+  }
+  if constexpr (!SPLIT) store_out(out, tot);
+}
+
+// The matrix-core kernel serves bf16 routers with more than 16 experts and
+// more tokens than the decode-sized tiles of the vector kernel take (hidden
+// sizes are multiples of 128, so slices hold whole 64-element chunks).  At
+// 64 tokens its 32-token tiles give too few workgroups (DeepSeek-V3-shaped
+// decode: 19 us against 13 us on the vector kernel's 16-token tiles).
+bool use_mfma_router(int dtype, int N, int E) { return dtype == 1 && E > 16 && N > kRouterSmallN; }
+
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + expf(-z)); }
 
 // One wavefront per token, four tokens per workgroup.  EPL experts per lane:
@@ -359,15 +494,20 @@ hipError_t launch_logits_t(const T* x, const T* w, int N, int d, int E, bool spl
 
 int router_slices(int d) { return (d + kRouterSlice - 1) / kRouterSlice; }
 
-bool router_split(int N, int d, int E) {
+// Split the hidden dimension over workgroups (one 256-slice each, summed in
+// order by top-k) when the output tiles alone would not fill the chip: 512
+// tiles for the vector kernel, 4096 waves of 32 x 64 for the matrix-core one.
+bool router_split(int dtype, int N, int d, int E) {
+  if (router_slices(d) <= 1) return false;
+  if (use_mfma_router(dtype, N, E)) return cdiv64(N, 32) * cdiv64(E, 64) < 4096;
   const int64_t BT = E <= 16 ? 256 : (N <= kRouterSmallN ? 16 : 64), BE = E <= 16 ? 16 : 64;
   const int64_t tiles = cdiv64(N, BT) * cdiv64(E, BE);
-  return router_slices(d) > 1 && tiles < 512;
+  return tiles < 512;
 }
 
-size_t router_ws_bytes(int N, int d, int E) {
+size_t router_ws_bytes(int dtype, int N, int d, int E) {
   size_t b = (size_t)N * E * sizeof(float);  // logits when the caller keeps none
-  if (router_split(N, d, E)) b += (size_t)router_slices(d) * N * E * sizeof(float);
+  if (router_split(dtype, N, d, E)) b += (size_t)router_slices(d) * N * E * sizeof(float);
   return b;
 }
 
@@ -375,6 +515,29 @@ hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, 
                                 bool split, float* out, hipStream_t s) {
   if (dtype == 0)
     return launch_logits_t<float>((const float*)x, (const float*)w, N, d, E, split, out, s);
+  if (use_mfma_router(dtype, N, E)) {
+    // workgroup tile: 64 tokens x 128 experts, or 128 x 64 (measured on
+    // 4096 tokens over 256 experts: 64 x 128 192 us, 32 x 256 198 us)
+    const int z = split ? router_slices(d) : 1;
+#define FS_ROUTER_MFMA(WT, WE)                                                               \
+  do {                                                                                       \
+    const dim3 g((N + 32 * WT - 1) / (32 * WT), (E + 64 * WE - 1) / (64 * WE), z);           \
+    if (split)                                                                               \
+      launch_k(router_mfma_kernel<WT, WE, true>, g, 256, 0, s, (const bf16_t*)x,            \
+               (const bf16_t*)w, N, d, E, out);                                              \
+    else                                                                                     \
+      launch_k(router_mfma_kernel<WT, WE, false>, g, 256, 0, s, (const bf16_t*)x,           \
+               (const bf16_t*)w, N, d, E, out);                                              \
+  } while (0)
+    if (E > 128)
+      FS_ROUTER_MFMA(2, 2);
+    else if (E > 64)
+      FS_ROUTER_MFMA(2, 2);
+    else
+      FS_ROUTER_MFMA(4, 1);
+#undef FS_ROUTER_MFMA
+    return hipGetLastError();
+  }
   return launch_logits_t<bf16_t>((const bf16_t*)x, (const bf16_t*)w, N, d, E, split, out, s);
 }
 

@@ -64,11 +64,18 @@ def check_ids(cfg, ids_gpu, ids_ref, near):
     return int(near.sum())
 
 
-# router-only cases: 37 tokens take the 16-token tiles (three, one ragged)
-# over five slices of the hidden dimension
+# router-only cases: 37 tokens over five slices of the hidden dimension;
+# 160 experts (a ragged last 64-expert range) over 300 tokens (a ragged last
+# 32-token tile); 8190 tokens over 512 experts, enough output tiles to run
+# without splitting the hidden dimension, two slices of it (one ragged)
 ROUTER_EXTRA = {
     "dsv3_decode_m": CONFIGS["dsv3_decode"].scaled(n_tokens=37, hidden=1280, ffn=192,
                                                    ffn_shared=192, name="dsv3_decode_m"),
+    "e160": CONFIGS["dsv2lite"].scaled(n_tokens=300, hidden=640, n_experts=160, ffn=256,
+                                       ffn_shared=128, name="e160"),
+    "wide_unsplit": CONFIGS["dsv3_prefill"].scaled(n_tokens=8190, hidden=384, n_experts=512,
+                                                   ep_size=1, ffn=256, ffn_shared=128,
+                                                   name="wide_unsplit"),
 }
 
 
