@@ -33,7 +33,7 @@ Floating point is fp64 on the exact input values, as in ``moe.py``.
 
 import numpy as np
 
-from .moe import dense_linear, logits_routing_f32, route, route_given, silu
+from .moe import _given, dense_linear, logits_routing_f32, route, route_given, silu
 
 
 def expert_range(n_experts, ep_size, ep_rank):
@@ -162,7 +162,7 @@ def _route_all(cfg, o, lw, ids_given):
     ids, w, near, margin = route(z32, cfg.score, cfg.top_k, cfg.n_groups, cfg.topk_groups,
                                  cfg.norm_topk, cfg.routed_scale, lw.get("bias"))
     if ids_given is not None:
-        ids = np.asarray(ids_given, np.int32)
+        ids = np.asarray(_given(ids_given, cfg, z32, ids, lw.get("bias")), np.int32)
         w = route_given(z32, ids, cfg.score, cfg.norm_topk, cfg.routed_scale)
     return ids, w, dict(z32=z32, ids=ids, margin=margin)
 

@@ -61,7 +61,7 @@ def logits_routing_f32(x, w_router, slice_len=ROUTER_SLICE):
 # O2-O6: scores, group limit, top-k, weights  (Section 2.1, s())
 # --------------------------------------------------------------------------
 def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
-          routed_scale=1.0, bias=None, tau=1e-6):
+          routed_scale=1.0, bias=None, tau=1e-6, margins="kernel"):
     """Select top_k experts per token from fp32 logits.
 
     Returns (ids [N,k] int32 in descending key order, weights [N,k] fp64,
@@ -71,7 +71,17 @@ def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
     transcendental keys or rounded group sums is closer than ``tau``: either
     selection or slot order may then legitimately differ.  Softmax selection
     compares the fp32 logits themselves and is never flagged.
+
+    ``margins`` chooses the decisions the margin covers: "kernel" (the
+    above), "all" (every decision of either score: gaps between consecutive
+    selected keys, between the last selected and the first rejected key,
+    and the group decisions) or "set" (only the decisions that change which
+    experts and groups are selected: the last selected against the first
+    rejected key and group).  The last two serve logits that are themselves
+    perturbed, as a stacked layer's input carries roundings.
     """
+    if margins not in ("kernel", "all", "set"):
+        raise ValueError(margins)
     z = np.asarray(z32, np.float64)
     N, E = z.shape
     if score == "softmax":
@@ -81,7 +91,7 @@ def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
         ex = np.exp(z - zmax)
         base = ex / ex.sum(axis=1, keepdims=True)   # probabilities over all E
         keys = z.copy()
-        keys_rounded = False
+        keys_rounded = margins != "kernel"
     elif score == "sigmoid":
         with np.errstate(over="ignore"):
             base = 1.0 / (1.0 + np.exp(-z))
@@ -106,7 +116,7 @@ def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
         gs_sorted = np.take_along_axis(gscore, gorder, axis=1)
         if topk_groups < n_groups:
             margin = np.minimum(margin, gs_sorted[:, topk_groups - 1] - gs_sorted[:, topk_groups])
-        if topk_groups > 1:
+        if topk_groups > 1 and margins != "set":
             margin = np.minimum(margin, np.min(np.diff(-gs_sorted[:, :topk_groups], axis=1), axis=1))
 
     order = np.lexsort((idx_e, -keys), axis=1)
@@ -117,7 +127,7 @@ def route(z32, score, top_k, n_groups=1, topk_groups=1, norm_topk=False,
             nxt = ks[:, top_k]
             gap = ks[:, top_k - 1] - nxt
             margin = np.minimum(margin, np.where(np.isfinite(nxt), gap, np.inf))
-        if top_k > 1:
+        if top_k > 1 and margins != "set":
             margin = np.minimum(margin, np.min(ks[:, :top_k - 1] - ks[:, 1:top_k], axis=1))
     w = np.take_along_axis(base, ids, axis=1)
     if norm_topk:
@@ -262,15 +272,27 @@ def dense_linear(a, w):
 # --------------------------------------------------------------------------
 # The whole block on rank r (packed formulation, O1-O13)
 # --------------------------------------------------------------------------
+def _given(ids_given, cfg, z32, own, bias):
+    """The selection a caller substitutes: an [N, k] array, or a callable
+    taking (z32, own ids, set-decision margins) and returning one."""
+    if callable(ids_given):
+        _, _, _, margin = route(z32, cfg.score, cfg.top_k, cfg.n_groups, cfg.topk_groups,
+                                cfg.norm_topk, cfg.routed_scale, bias, margins="set")
+        return ids_given(z32, own, margin)
+    return ids_given
+
+
 def moe_block(cfg, x_all, w_router, bias, w_gate_up, w_down, sh_gate_up=None,
               sh_down=None, y_remote=None, ids_given=None):
     """Every step of the block on rank cfg.ep_rank, following the data flow
     router -> top-k -> plan -> pack -> all-to-all -> experts -> return ->
     combine.  For R > 1 the other ranks' routing and sends are computed here
-    too.  ids_given (optional, [N, k]) replaces this rank's own selection
-    (the weights still come from its logits): where rounding in an earlier
-    layer moved a near tie, a caller takes the selection the other side
-    made.  Returns a dict of every intermediate."""
+    too.  ids_given (optional) replaces this rank's own selection (the
+    weights still come from its logits): an [N, k] array, or a callable
+    (z32, own ids, margins of the set decisions) -> [N, k] ids, so that a
+    caller can take the other side's selection only where rounding in an
+    earlier layer may have moved a near tie.  Returns a dict of every
+    intermediate."""
     R, r, k, E = cfg.ep_size, cfg.ep_rank, cfg.top_k, cfg.n_experts
     E_loc, cap = cfg.n_local, cfg.cap
     src = []
@@ -280,7 +302,7 @@ def moe_block(cfg, x_all, w_router, bias, w_gate_up, w_down, sh_gate_up=None,
         ids, w, near, margin = route(z32, cfg.score, k, cfg.n_groups, cfg.topk_groups,
                                      cfg.norm_topk, cfg.routed_scale, bias)
         if s == r and ids_given is not None:
-            ids = np.asarray(ids_given, np.int32)
+            ids = np.asarray(_given(ids_given, cfg, z32, ids, bias), np.int32)
             w = route_given(z32, ids, cfg.score, cfg.norm_topk, cfg.routed_scale)
         plan = dispatch_plan(ids, E, R)
         send = pack(xs, plan["slot_to_row"], k)

@@ -75,6 +75,7 @@ class ReplicatedStack:
         # per-layer copies of the selections, kept when a schedule runs with
         # keep_ids=True (for checking routing against a reference)
         self.kept_ids = []
+        self.kept_logits = []
 
     def close(self):
         pass
@@ -97,11 +98,18 @@ class ReplicatedStack:
     def _routed(self, o, lw, stream, keep_ids=False):
         """This rank's routed partial sum on o into self.routed."""
         c = self.cfg
-        L.fs_router_topk(self.desc, o, lw["w_router"], lw.get("bias"), None, None, self.ids,
+        logits = None
+        if keep_ids:
+            if getattr(self, "logits", None) is None:
+                self.logits = torch.empty((c.n_tokens, c.n_experts), dtype=torch.float32,
+                                          device=self.ids.device)
+            logits = self.logits
+        L.fs_router_topk(self.desc, o, lw["w_router"], lw.get("bias"), None, logits, self.ids,
                          self.w, self.ws_router, stream=stream)
         if keep_ids:
             with torch.cuda.stream(stream):
                 self.kept_ids.append(self.ids.clone())
+                self.kept_logits.append(self.logits.clone())
         L.fs_dispatch_pack(self.desc, self.ids, None, self.counts, self.offsets, self.rank_offsets,
                            self.s2r, self.r2s, None, self.ws_plan, stream=stream)
         L.fs_local_rows(self.desc, self.offsets, self.rank_offsets, self.r2s, self.local_tokens,
@@ -121,6 +129,7 @@ class ReplicatedStack:
         With comm None the same order runs on one stream."""
         compute = compute or torch.cuda.current_stream()
         self.kept_ids = []
+        self.kept_logits = []
         side = comm or compute
         p = o = x
         routed_done = None
@@ -161,6 +170,7 @@ class ReplicatedStack:
         `compute`; returns the buffer holding o_{L-1}."""
         compute = compute or torch.cuda.current_stream()
         self.kept_ids = []
+        self.kept_logits = []
         o = x
         for lw in self.layers:
             self._attention(o, lw, compute)

@@ -118,6 +118,13 @@ def test_grouped_ffn_fp8_steps(counts, F, d, gather):
     xq_n, xs_n = np_u8(xq), xs.cpu().numpy()
     gq_n, gs_n = np_u8(gq).reshape(G, 2 * F, d), gs.cpu().numpy().reshape(G, 2 * F)
     dq_n, ds_n = np_u8(dq).reshape(G, d, F), ds.cpu().numpy().reshape(G, d)
+    # the codes the oracle is about to use are the oracle's own quantisation
+    # of the bf16 activations and weights, bit for bit
+    for got_c, got_s, src_t in ((xq_n, xs_n, x), (gq_n.reshape(-1, d), gs_n.reshape(-1), wgu),
+                                (dq_n.reshape(-1, F), ds_n.reshape(-1), wdn)):
+        want_c, want_s = of8.quantize_rows(src_t.float().cpu().numpy().reshape(got_c.shape))
+        assert np.array_equal(got_c, want_c)
+        assert np.array_equal(got_s.view(np.uint32), want_s.view(np.uint32))
     src = np.arange(M) if rows is None else rows.cpu().numpy()
     goff_n = goff.cpu().numpy()
     H_n, Hq_n, Hs_n, out_n = f64(H), np_u8(Hq), Hs.cpu().numpy(), f64(out)

@@ -549,3 +549,57 @@ def test_tokens_direct_hand_value():
                                    [[None, np.array([3.0, 3.0])]])
     want = 0.5 * 4.0 / (1.0 + math.exp(-2.0)) + 0.75
     assert np.allclose(got, [[want, want]], rtol=1e-15, atol=0)
+
+
+def test_route_margin_kinds():
+    # Softmax selection is never a near tie for the kernel (it compares the
+    # logits themselves), but a perturbed input can flip a close pair:
+    # "all" covers every decision, "set" only those that change which
+    # experts are selected.
+    z = np.array([[0.5, 0.5 + 2e-9, -1.0, 0.1], [2.0, 1.0, 0.0, -1.0],
+                  [3.0, 1.0, 1.0 - 1e-9, -1.0]])
+    _, _, near, margin = oracle.route(z, "softmax", 2)
+    assert not near.any() and np.all(np.isinf(margin))
+    ids, _, near, margin = oracle.route(z, "softmax", 2, margins="all")
+    assert near.tolist() == [True, False, True]
+    assert ids[0].tolist() == [1, 0]
+    # row 1: gaps 2 - 1 (slot order) and 1 - 0 (last kept vs first dropped)
+    assert margin[1] == 1.0
+    _, _, near, margin = oracle.route(z, "softmax", 2, margins="set")
+    # row 0: the close pair are both selected (only their order is close)
+    assert near.tolist() == [False, False, True]
+    assert margin[0] == 0.5 - 0.1 and margin[1] == 1.0
+    # sigmoid: "kernel" and "all" agree
+    a = oracle.route(z, "sigmoid", 2)[3]
+    b = oracle.route(z, "sigmoid", 2, margins="all")[3]
+    assert np.array_equal(a, b)
+    # groups: the group boundary counts for "set", the order of kept groups
+    # does not
+    zg = np.array([[1.0, 0.0, 1.0 + 1e-9, 0.0, -3.0, -3.0]])
+    m_all = oracle.route(zg, "softmax", 2, n_groups=3, topk_groups=2, margins="all")[3]
+    m_set = oracle.route(zg, "softmax", 2, n_groups=3, topk_groups=2, margins="set")[3]
+    assert m_all[0] < 1e-8 and m_set[0] == 1.0
+
+
+def test_block_selection_callback():
+    # A callable ids_given sees the logits, the oracle's own ids and the
+    # margins of its set decisions, and its result replaces the selection.
+    cfg = _tiny_cfg(score="sigmoid", n_groups=3, topk_groups=2, top_k=3)
+    x_all, wr, bias, gu, dn, _ = _tiny_inputs(cfg, rng(27))
+    own = oracle.moe_block(cfg, x_all, wr, bias, gu, dn)
+    seen = {}
+
+    def keep_own(z32, ids, margin):
+        seen.update(z32=z32, ids=ids, margin=margin)
+        return ids
+
+    same = oracle.moe_block(cfg, x_all, wr, bias, gu, dn, ids_given=keep_own)
+    assert np.array_equal(same["routed"], own["routed"])
+    assert np.array_equal(seen["ids"], own["me"]["ids"])
+    assert np.array_equal(seen["z32"], own["me"]["z32"])
+    m_set = oracle.route(seen["z32"], cfg.score, cfg.top_k, cfg.n_groups, cfg.topk_groups,
+                         cfg.norm_topk, cfg.routed_scale, bias, margins="set")[3]
+    assert np.array_equal(seen["margin"], m_set)
+    flipped = oracle.moe_block(cfg, x_all, wr, bias, gu, dn,
+                               ids_given=lambda z, ids, m: ids[:, ::-1].copy())
+    assert np.allclose(flipped["routed"], own["routed"], rtol=1e-12, atol=1e-12)
