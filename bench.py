@@ -260,7 +260,9 @@ def bench_layers(args, cfg, torch, L):
         "config": {"workload": f"{cfg.name}: {args.layers} stacked layers, two-window FarSkip "
                                f"schedule (Dispatch and Combine stand-in copies on a second stream)",
                    "layers": args.layers, "tokens": N, "hidden": cfg.hidden,
-                   "experts": cfg.n_experts, "top_k": cfg.top_k, "ep_size": cfg.ep_size},
+                   "experts": cfg.n_experts, "top_k": cfg.top_k, "ffn": cfg.ffn,
+                   "shared": cfg.n_shared, "ffn_shared": cfg.ffn_shared,
+                   "ep_size": cfg.ep_size, "dtype": cfg.dtype},
         "regular_ms_per_step": ms_rg,
         "speedup_vs_regular": ms_rg / ms_fs,
         "xgmi_model": {"copy_us_each": round(xgmi_us, 2),

@@ -20,7 +20,9 @@ sparser than DeepSeek-V3 (s = 32) has s/32 times the experts, each
 32/s times narrower, with the same 8 + 1 active experts: same parameters,
 fewer routed FLOPs.
 
-Pure arithmetic on the host; no GPU and no data.
+Pure arithmetic on the host; no GPU and no data.  ``measured_rates`` and
+``calibrated_machine`` take the rates from a bench.py record of one MI355X
+instead (``--bench FILE``).
 """
 
 from dataclasses import dataclass, replace
@@ -58,10 +60,12 @@ class Machine:
     attn_flops: float = 500e12
     allreduce_bw: float = 400e9
     gpus: int = 8
+    gate_flops: float = 0.0     # the router's rate; 0: the GEMM rate
 
     def scaled(self, compute=1.0, attention=1.0, comm=1.0):
         return replace(self, gemm_flops=self.gemm_flops * compute,
                        attn_flops=self.attn_flops * compute * attention,
+                       gate_flops=self.gate_flops * compute,
                        allreduce_bw=self.allreduce_bw * comm)
 
 
@@ -114,7 +118,7 @@ def layer_times(a, m, b):
     attn = proj / m.gpus / m.gemm_flops + core / m.gpus / m.attn_flops
     shared = a.n_shared * swiglu_flops(t, a.d, a.shared_ffn) / m.gpus / m.gemm_flops
     routed = a.active * swiglu_flops(t, a.d, a.ffn) / m.gpus / m.gemm_flops
-    gate = gemm_flops(t, a.d, a.experts) / m.gpus / m.gemm_flops
+    gate = gemm_flops(t, a.d, a.experts) / m.gpus / (m.gate_flops or m.gemm_flops)
     msg = allreduce_time(t * a.d * b.act_bytes, m)            # one [tokens, d] all-reduce
     return dict(attn=attn, shared=shared, routed=routed, gate=gate, attn_comm=msg, mlp_comm=msg)
 
@@ -160,14 +164,90 @@ def sweep(machine=Machine(), batch=Batch(), arch=Arch(), sparsities=SPARSITIES):
     return out
 
 
+# ---------------------------------------------------------------- calibration
+# Rates measured on one MI355X by bench.py replace the hypothetical
+# accelerator's: the routed SwiGLU experts' sustained TFLOP/s for the
+# model's GEMMs, the dense linear's (the attention stand-in's parts a and b)
+# for attention, and the router's.  The all-reduce bandwidth of an
+# 8 x MI355X node is not measurable on one GPU and stays a parameter.
+
+@dataclass(frozen=True)
+class Rates:
+    """Sustained TFLOP/s of the kernels a bench.py record timed."""
+    routed: float          # routed SwiGLU experts, gate/up + down
+    shared: float          # shared experts, gate/up + down (0 without)
+    dense: float           # dense d x d linear (attention stand-in)
+    router: float          # router logits
+
+
+def _record_shape(rec):
+    c = rec["config"]
+    N, d, E, k = c["tokens"], c["hidden"], c["experts"], c["top_k"]
+    # rows on this rank's experts: recorded by block lines; a stacked-layer
+    # line takes the balanced expectation N k (each of R ranks routes N
+    # tokens to k experts, a 1/R share of which is local)
+    rows = c.get("rows_local_experts", N * k)
+    return N, d, E, k, c["ffn"], c.get("shared", 0), c.get("ffn_shared", 0), rows
+
+
+def measured_rates(rec):
+    """Rates of a bench.py JSON record (a block line, or a stacked-layer
+    line of bench.py --layers), from its per-launch kernel times."""
+    N, d, E, k, F, S, Fs, rows = _record_shape(rec)
+    us = rec["kernels_us"]
+    tflops = lambda flops, t_us: flops / (t_us * 1e-6) / 1e12
+    routed = tflops(swiglu_flops(rows, d, F), us["gate_up"] + us["down"])
+    shared = (tflops(S * swiglu_flops(N, d, Fs), us["shared_gate_up"] + us["shared_down"])
+              if S and "shared_gate_up" in us else 0.0)
+    dense = tflops(gemm_flops(N, d, d), us["next_layer"]) if "next_layer" in us else routed
+    router = tflops(gemm_flops(N, d, E), us["router"])
+    return Rates(routed, shared, dense, router)
+
+
+STACK_KERNELS = ("router", "topk", "plan", "pack", "gate_up", "down", "combine",
+                 "shared_gate_up", "shared_down")
+
+
+def stack_layer_time(rec):
+    """Modelled time (s) of one stacked layer of bench.py --layers: the
+    attention stand-in's two dense linears and the block's kernels, in
+    sequence, with the Dispatch and Combine stand-in copies hidden (the
+    FarSkip schedule's windows, Eq. 9)."""
+    us = rec["kernels_us"]
+    t = sum(us.get(n, 0.0) for n in STACK_KERNELS) + 2 * us.get("next_layer", 0.0)
+    return t * 1e-6
+
+
+def calibrated_machine(rec, allreduce_bw, gpus=8):
+    """The App. B node with one MI355X's measured rates: GEMMs at the
+    routed experts' rate, attention at the dense linear's, the gate at the
+    router's."""
+    r = measured_rates(rec)
+    return Machine(gemm_flops=r.routed * 1e12, attn_flops=r.dense * 1e12,
+                   allreduce_bw=allreduce_bw, gpus=gpus, gate_flops=r.router * 1e12)
+
+
 def main():
     import argparse
+    import json
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gemm-tflops", type=float, default=600.0)
     ap.add_argument("--attn-tflops", type=float, default=500.0)
     ap.add_argument("--allreduce-gbs", type=float, default=400.0)
+    ap.add_argument("--bench", default=None,
+                    help="a bench.py JSON line (file): take the GEMM and attention rates from it")
     a = ap.parse_args()
     m = Machine(a.gemm_tflops * 1e12, a.attn_tflops * 1e12, a.allreduce_gbs * 1e9)
+    if a.bench:
+        rec = json.loads(open(a.bench).read().strip().splitlines()[-1])
+        r = measured_rates(rec)
+        m = calibrated_machine(rec, a.allreduce_gbs * 1e9)
+        print(f"rates from {a.bench}: routed {r.routed:.1f}, shared {r.shared:.1f}, dense "
+              f"{r.dense:.1f}, router {r.router:.1f} TFLOP/s; all-reduce {a.allreduce_gbs:.0f} GB/s")
+        if "layers" in rec["config"]:
+            per = rec["ms_per_step"] * 1e-3 / rec["config"]["layers"]
+            print(f"stacked layer: modelled {stack_layer_time(rec) * 1e6:.1f} us, measured "
+                  f"{per * 1e6:.1f} us")
     res = sweep(m)
     print("| scenario | " + " | ".join(f"{s}x" for s in SPARSITIES) + " |")
     print("|---|" + "---|" * len(SPARSITIES))
