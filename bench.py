@@ -490,8 +490,11 @@ def bench_block(args, cfg, torch, L, with_cpu):
     sh_gu = sh_dn = None
     if cfg.n_shared > 0:
         sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
+    # decode-sized routed passes (a few rows per local expert) stream the
+    # experts' weights in fragment order
+    fo = args.fp8 is None and cfg.dtype == "bf16" and cfg.cap <= 64 * cfg.n_local
     blk = fs.MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=dev,
-                      fp8=args.fp8)
+                      fp8=args.fp8, fragment_order=fo)
     M = cfg.cap
     if cfg.ep_size > 1:
         M = fs.prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias, wl.y_remote)
@@ -666,7 +669,8 @@ def bench_block(args, cfg, torch, L, with_cpu):
                                + (f", FP8 E4M3 experts ({args.fp8})" if fp8_routed else ""),
                    "tokens": N, "hidden": d, "experts": E, "top_k": k, "ffn": cfg.ffn,
                    "shared": cfg.n_shared, "ep_size": cfg.ep_size, "rows_local_experts": M,
-                   "second_stream": comm is not None, "next_layer": bool(args.overlap)},
+                   "second_stream": comm is not None, "next_layer": bool(args.overlap),
+                   "fragment_ordered_experts": fo},
         "roofline": roof,
         "grouped_gemm_frac_bf16_peak": None if roof is None else roof["mfma_frac"],
         "ffn": ffn,

@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 6
+#define FS_ABI_VERSION 7
 
 typedef enum {
   FS_OK = 0,
@@ -278,6 +278,37 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
                                 const void* w_gate_up, const void* w_down, void* out_rows,
                                 void* ws, size_t ws_bytes, fs_stream stream);
 
+/* Expert weights in MFMA fragment order, a load-time layout transform for
+ * weight streaming (decode: the MoE layer's experts, Section 2.1, whose
+ * weights each routed pass reads once from HBM; the paper's decode is
+ * memory-bound, Section 5.2).  n_mats row-major bf16 matrices [rows, cols]
+ * (rows % 32 == 0, cols % 16 == 0) are rewritten as [rows/32][cols/16]
+ * blocks of 1 KB: in block (g, c), the 16 bytes at lane l (0..63) are
+ * row 32 g + l % 32, columns 16 c + 8 (l / 32) .. + 7, the B operand layout
+ * of a 32 x 32 x 16 bf16 matrix instruction.  A block is one 1 KB load and
+ * a 32-row group's whole column range is contiguous.
+ *   src, dst   n_mats * rows * cols bf16 each, device, 16-byte aligned,
+ *              not overlapping
+ * FS_ERR_UNSUPPORTED for other dtypes or shapes. */
+fs_status fs_expert_weights_fragment_order(int32_t dtype, int64_t n_mats, int32_t rows,
+                                           int32_t cols, const void* src, void* dst,
+                                           fs_stream stream);
+
+/* fs_grouped_expert_ffn with fragment-ordered weights
+ * (fs_expert_weights_fragment_order of w_gate_up as n_groups matrices
+ * [2F, d] and of w_down as n_groups matrices [d, F]): the same rows,
+ * groups, outputs and workspace (FS_OP_GROUPED_FFN), bf16 only, ffn % 128
+ * == 0 and d % 256 == 0 (FS_ERR_UNSUPPORTED otherwise).  The weights
+ * stream from memory straight into the matrix units' registers, 64 rows
+ * per tile: meant for groups of few rows (decode), where the pass is
+ * bound by reading every weight once; larger groups are correct but re-read
+ * each weight panel once per 64 rows. */
+fs_status fs_grouped_expert_ffn_fo(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                   const void* in_rows, const int32_t* group_rows,
+                                   const int32_t* group_offsets, int64_t max_rows,
+                                   const void* w_gate_up_fo, const void* w_down_fo,
+                                   void* out_rows, void* ws, size_t ws_bytes, fs_stream stream);
+
 /* The grouped SwiGLU FFN of fs_grouped_expert_ffn with the input gathered
  * and the output in grouped order: row i of the grouped order reads
  * x[gather_rows[i]] and writes y[i].  Used with replicated activations,
@@ -407,6 +438,13 @@ typedef struct {
   const float* ss_gate_up;       /* [2 S F_s] */
   const uint8_t* ws_down_fp8;    /* [d, S F_s] */
   const float* ss_down;          /* [d] */
+  /* Fragment-ordered copies of w_gate_up and w_down
+   * (fs_expert_weights_fragment_order), or NULL.  When given (bf16, ffn %
+   * 128 == 0, d % 256 == 0), routed-expert passes whose groups average at
+   * most 64 rows (decode) stream them with fs_grouped_expert_ffn_fo's
+   * kernels; other passes read w_gate_up / w_down, which stay required. */
+  const void* w_gate_up_fo;      /* [E/R, 2F, d] in fragment order */
+  const void* w_down_fo;         /* [E/R, d, F] in fragment order */
 } fs_moe_weights;
 
 /* Caller-owned buffers of one block (device memory). */

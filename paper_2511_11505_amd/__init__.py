@@ -15,8 +15,9 @@ from ._lib import (  # noqa: F401
     FsError, make_desc, load, fs_abi_version, fs_workspace_size, fs_router_topk,
     fs_dispatch_pack, fs_dispatch_pack_fp8, fs_receive_rows, fs_grouped_expert_ffn, fs_combine_unpack,
     fs_local_rows, fs_grouped_expert_ffn_gathered, fs_combine_partial, fs_allreduce_standin,
-    fs_quantize_fp8, fs_grouped_expert_ffn_fp8,
+    fs_quantize_fp8, fs_grouped_expert_ffn_fp8, fs_expert_weights_fragment_order,
+    fs_grouped_expert_ffn_fo,
     fs_farskip_residual, fs_dense_linear, fs_block_sync_create, fs_block_sync_destroy,
     fs_moe_block_forward, fs_profile_enable, fs_profile_select, fs_profile_read, fs_profile_reset,
 )
-from .block import MoEBlock, fp8_row_views, prepare_remote_sources  # noqa: F401
+from .block import MoEBlock, fp8_row_views, fragment_ordered, prepare_remote_sources  # noqa: F401

@@ -32,6 +32,16 @@ def _quantize(w):
     return codes, scales
 
 
+def fragment_ordered(w):
+    """MFMA fragment-order copy of bf16 weight matrices [..., rows, cols]
+    (fs_expert_weights_fragment_order)."""
+    rows, cols = w.shape[-2], w.shape[-1]
+    out = torch.empty_like(w)
+    L.fs_expert_weights_fragment_order(L.FS_BF16, w.numel() // (rows * cols), rows, cols,
+                                       w.contiguous(), out)
+    return out
+
+
 def fp8_row_views(buf, rows, d):
     """Views of an FP8 row buffer of `rows` rows held in the device tensor
     buf (any dtype, contiguous): codes [rows, d] uint8 at byte 0, scales
@@ -45,9 +55,13 @@ def fp8_row_views(buf, rows, d):
 
 class MoEBlock:
     def __init__(self, cfg, w_router, sel_bias, w_gate_up, w_down, ws_gate_up=None, ws_down=None,
-                 max_recv_rows=None, device="cuda", with_comm=True, with_return=False, fp8=None):
+                 max_recv_rows=None, device="cuda", with_comm=True, with_return=False, fp8=None,
+                 fragment_order=False):
         """fp8: None (bf16 experts), "routed" (FP8 routed experts) or "all"
-        (FP8 routed and shared experts)."""
+        (FP8 routed and shared experts).  fragment_order: also keep the
+        routed experts' weights in MFMA fragment order (converted once, by
+        the library), which the block streams for passes of few rows per
+        expert (decode)."""
         if fp8 not in (None, "routed", "all"):
             raise ValueError(f"fp8 must be None, 'routed' or 'all', not {fp8!r}")
         self.cfg = cfg
@@ -84,6 +98,9 @@ class MoEBlock:
             if fp8 == "all" and ws_gate_up is not None:
                 q["ws_gate_up_fp8"], q["ss_gate_up"] = _quantize(ws_gate_up)
                 q["ws_down_fp8"], q["ss_down"] = _quantize(ws_down)
+        if fragment_order:
+            q["w_gate_up_fo"] = fragment_ordered(w_gate_up)
+            q["w_down_fo"] = fragment_ordered(w_down)
         self.fp8_weights = q
         self.weights_keep = (w_router, sel_bias, w_gate_up, w_down, ws_gate_up, ws_down)
         self.weights = L.fs_moe_weights(L.ptr(w_router), L.ptr(sel_bias), L.ptr(w_gate_up),

@@ -628,6 +628,54 @@ fs_status fs_grouped_expert_ffn(const fs_moe_desc* desc, int32_t n_groups, int32
   return FS_OK;
 }
 
+fs_status fs_expert_weights_fragment_order(int32_t dtype, int64_t n_mats, int32_t rows,
+                                           int32_t cols, const void* src, void* dst,
+                                           fs_stream stream) {
+  if (dtype != FS_BF16) return fail(FS_ERR_UNSUPPORTED, "fragment order is for bf16 weights");
+  if (n_mats < 0 || rows <= 0 || cols <= 0) return fail(FS_ERR_INVALID, "bad matrix shape");
+  if (rows % 32 != 0 || cols % 16 != 0)
+    return fail(FS_ERR_UNSUPPORTED, "fragment order needs rows % 32 == 0 and cols % 16 == 0");
+  if (n_mats == 0) return FS_OK;
+  NEED(src, "src");
+  NEED(dst, "dst");
+  const size_t bytes = (size_t)n_mats * rows * cols * 2;
+  const char *a = static_cast<const char*>(src), *b = static_cast<const char*>(dst);
+  if (a < b + bytes && b < a + bytes) return fail(FS_ERR_INVALID, "src and dst overlap");
+  FS_HIP(fs::launch_fragment_order(src, n_mats, rows, cols, dst, S(stream)), "fragment_order");
+  return FS_OK;
+}
+
+static bool fo_shape_ok(const fs_moe_desc* d, int32_t ffn) {
+  return d->dtype == FS_BF16 && ffn % 128 == 0 && d->hidden % 256 == 0;
+}
+
+fs_status fs_grouped_expert_ffn_fo(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                   const void* in_rows, const int32_t* group_rows,
+                                   const int32_t* group_offsets, int64_t max_rows,
+                                   const void* w_gate_up_fo, const void* w_down_fo,
+                                   void* out_rows, void* ws, size_t ws_bytes, fs_stream stream) {
+  fs_status st = ffn_checks(desc, n_groups, ffn, group_offsets, max_rows);
+  if (st != FS_OK) return st;
+  if (!fo_shape_ok(desc, ffn))
+    return fail(FS_ERR_UNSUPPORTED, "fragment-ordered experts need bf16, ffn % 128 == 0 and "
+                                    "hidden % 256 == 0");
+  if (max_rows == 0) return FS_OK;
+  NEED(in_rows, "in_rows");
+  OPT4(group_rows, "group_rows");
+  OPT4(group_offsets, "group_offsets");
+  NEED(w_gate_up_fo, "w_gate_up_fo");
+  NEED(w_down_fo, "w_down_fo");
+  NEED(out_rows, "out_rows");
+  if (ws_bytes < fs::ffn_ws_bytes(desc->dtype, max_rows, ffn, desc->hidden))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN)");
+  NEED(ws, "ws");
+  FS_HIP(fs::launch_grouped_ffn_fo(n_groups, ffn, desc->hidden, in_rows, group_rows, group_rows,
+                                   group_offsets, max_rows, w_gate_up_fo, w_down_fo, out_rows, ws,
+                                   S(stream), group_offsets ? FS_K_GATE_UP : FS_K_SHARED_GATE_UP),
+         "grouped_ffn_fo");
+  return FS_OK;
+}
+
 // ---- combine + residual
 fs_status fs_combine_unpack(const fs_moe_desc* desc, const void* y_ret,
                             const int32_t* slot_to_row, const float* topk_w,
@@ -990,6 +1038,13 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
                                         max_recv_rows, wt->w_gate_up_fp8, wt->s_gate_up,
                                         wt->w_down_fp8, wt->s_down, b->y, ws_ffn, sc, FS_K_GATE_UP),
              "grouped_ffn_fp8");
+    } else if (wt->w_gate_up_fo && wt->w_down_fo && fo_shape_ok(desc, desc->ffn) &&
+               max_recv_rows <= (int64_t)64 * E_loc) {
+      // groups of few rows (decode): stream the fragment-ordered weights
+      FS_HIP(fs::launch_grouped_ffn_fo(E_loc, desc->ffn, D, in_rows, rows, rows, goff,
+                                       max_recv_rows, wt->w_gate_up_fo, wt->w_down_fo, b->y,
+                                       ws_ffn, sc, FS_K_GATE_UP),
+             "grouped_ffn_fo");
     } else {
       FS_HIP(fs::launch_grouped_ffn(desc->dtype, E_loc, desc->ffn, D, in_rows, rows, rows, goff,
                                     max_recv_rows, wt->w_gate_up, wt->w_down, b->y, ws_ffn, sc,

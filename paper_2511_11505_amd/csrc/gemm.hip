@@ -1071,6 +1071,237 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_rs_kernel(
   }
 }
 
+// ---------------------------------------------------------------- bf16 MFMA, fragment-ordered weights
+// Expert weights stored in MFMA fragment order (one 1 KB block per 32 rows x
+// 16 k: lane l's 16 bytes are row l % 32, k 8 (l / 32) .. + 7, the B operand
+// of v_mfma_f32_32x32x16_bf16) stream from HBM straight into registers: a
+// load instruction reads 1 KB contiguously and a wave reads one 32-row
+// group's whole K range in address order, so the weights never pass
+// through LDS.  Only the activation rows (64 per tile, gathered) are staged,
+// by direct global->LDS DMAs in a three-slot ring.  For groups of few rows
+// (decode), where the pass streams every active expert's weights once and is
+// bound by HBM.
+//
+// Tile: 64 rows x (gate/up: 128 H columns, wave w the gate group and the up
+// group of columns 32 w .. 32 w + 31; down: 256 output columns, wave w two
+// 32-column groups).  Weight blocks of 64 k go two blocks ahead of the
+// MFMAs (three register slots of 32 VGPRs), activation blocks two ahead.
+// The persistent grid walks (group, n-tile, m-tile; m fastest) in eight
+// contiguous XCD ranges, as the LDS-ring kernels do: m-tiles of one weight
+// panel run together under one L2.
+constexpr int kFoBM = 64;
+
+__device__ __forceinline__ const bf16_t* fo_group(const bf16_t* Wg, int K, int grp) {
+  return Wg + (size_t)grp * (K / 16) * 512;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
+    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ Bfo,
+    int K, int NOUT, bf16_t* __restrict__ C, int ldc) {
+  constexpr int BM = kFoBM, NT = 256, TM = BM / 32, KS = 4, NST = 3;
+  constexpr int ROWB = 128, ASTAGE = BM * ROWB;
+  constexpr int ALD = BM * ROWB / 1024 / 4;          // 1 KB DMAs per wave per block
+  constexpr int NB = 2 * KS;                         // weight loads per wave per block
+  constexpr int NCOL = (MODE == MODE_GATEUP) ? 128 : 256;
+  __shared__ int s_goff[kMaxGroups + 1];
+  __shared__ int s_tpre[kMaxGroups + 1];
+  __shared__ int s_wtot[NT / 64];
+  __shared__ __align__(1024) unsigned char ring[NST * ASTAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
+
+  const int nn = NOUT / NCOL;
+  const int64_t total = (int64_t)nn * s_tpre[G];
+  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
+  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
+  const int64_t stride = gridDim.x / kXcd;
+  const int KT = K / 64;
+  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
+  const int drow = lane / 8, dpos = lane % 8;
+  const unsigned ring_lds = lds_addr(ring);
+  const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+  int aoff[TM], asw[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = i * 32 + (lane & 31);
+    aoff[i] = r * ROWB;
+    asw[i] = (r >> 1) & 7;
+  }
+  int ghint = 0;
+
+  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
+    const int64_t L = xcd_base + j;
+    if (L >= total) break;
+    const int g = find_group_from(s_tpre, G, nn, L, ghint);
+    ghint = g;
+    const int Tg = s_tpre[g + 1] - s_tpre[g];
+    const int local = (int)(L - (int64_t)nn * s_tpre[g]);
+    const int nt = local / Tg;
+    const int m0 = (local - nt * Tg) * BM, n0 = nt * NCOL;
+    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
+    const bf16_t* Bg = Bfo + (size_t)g * bstride;
+    // activation rows of this wave's DMAs (rows past the group's end load
+    // its last row; their results are not stored)
+    const bf16_t* asrc[ALD];
+#pragma unroll
+    for (int i = 0; i < ALD; ++i) {
+      const int r = (wave * ALD + i) * 8 + drow;
+      int m = m0 + r;
+      if (m >= rows_g) m = rows_g - 1;
+      const int grow = row_base + m;
+      const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
+      asrc[i] = A + sr * K + ((dpos ^ ((r >> 1) & 7)) * 8);
+    }
+    // this wave's two 32-row weight groups
+    const bf16_t* bsrc[2];
+    if (MODE == MODE_GATEUP) {
+      bsrc[0] = fo_group(Bg, K, n0 / 32 + wave) + lane * 8;
+      bsrc[1] = fo_group(Bg, K, (NOUT + n0) / 32 + wave) + lane * 8;
+    } else {
+      bsrc[0] = fo_group(Bg, K, n0 / 32 + 2 * wave) + lane * 8;
+      bsrc[1] = fo_group(Bg, K, n0 / 32 + 2 * wave + 1) + lane * 8;
+    }
+    auto dA = [&](int kt, int i) __attribute__((always_inline)) {
+      dma16_at(asrc[i] + (size_t)kt * 64,
+               ring_lds + (unsigned)((kt % NST) * ASTAGE) + (wave_u * ALD + i) * 1024u);
+    };
+    floatx16 acc[TM][2];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.f;
+    bf16x8 Bf[3][NB];
+    bf16x8 Fa[2][TM];
+    auto gB = [&](int slot, int kt, int q) __attribute__((always_inline)) {
+      Bf[slot][q] = *reinterpret_cast<const bf16x8*>(bsrc[q & 1] + ((size_t)kt * KS + (q >> 1)) * 512);
+    };
+    auto rA = [&](int buf, int kt, int ks, int i) __attribute__((always_inline)) {
+      const unsigned char* sl = ring + (kt % NST) * ASTAGE;
+      const int c = ks * 2 + (lane >> 5);
+      Fa[buf][i] = *reinterpret_cast<const bf16x8*>(sl + aoff[i] + ((c ^ asw[i]) << 4));
+    };
+    // prologue: activation blocks 0 and 1, weight blocks 0 and 1
+#pragma unroll
+    for (int i = 0; i < ALD; ++i) dA(0, i);
+#pragma unroll
+    for (int q = 0; q < NB; ++q) gB(0, 0, q);
+    if (KT > 1) {
+#pragma unroll
+      for (int i = 0; i < ALD; ++i) dA(1, i);
+#pragma unroll
+      for (int q = 0; q < NB; ++q) gB(1, 1, q);
+    }
+    wait_vmcnt<0>();
+    barrier_nofence();
+#pragma unroll
+    for (int i = 0; i < TM; ++i) rA(0, 0, 0, i);
+    // block kt: weights from slot kt % 3; issues the DMAs of activation block
+    // kt + 2 (step 0) and the loads of weight block kt + 2 (steps 0..2).  The
+    // last step waits for activation block kt + 1: after its DMAs, only this
+    // block's DMAs and weight loads may still be in flight.
+    auto block = [&](int kt, auto SLOT, auto N1, auto N2) __attribute__((always_inline)) {
+      constexpr int sl = decltype(SLOT)::value;
+      constexpr int s2 = (sl + 2) % 3;
+      const bool n1 = bool(N1), n2 = bool(N2);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int cb = ks & 1;
+#pragma unroll
+        for (int q = 0; q < TM * 2; ++q) {
+          const int i = q >> 1, t = q & 1;
+          acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fa[cb][i], Bf[sl][2 * ks + t],
+                                                              acc[i][t], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (ks == KS - 1 && q == 0 && n1) {
+            wait_lgkm0();
+            if (n2)
+              wait_vmcnt<ALD + NB>();
+            else
+              wait_vmcnt<0>();
+            barrier_nofence();
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if (q < TM) {
+            if (ks < KS - 1)
+              rA(cb ^ 1, kt, ks + 1, q);
+            else if (n1)
+              rA(cb ^ 1, kt + 1, 0, q);
+          }
+          if (ks == 0 && n2 && q < ALD) dA(kt + 2, q);
+          if (ks < 3 && n2) {
+            // weight loads 3 ks .. 3 ks + 2 of block kt + 2, after the last MFMAs
+            const int qq = 3 * ks + (q - (TM * 2 - 3));
+            if (q >= TM * 2 - 3 && qq < NB) gB(s2, kt + 2, qq);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using T = std::true_type;
+    int kt = 0;
+    for (; kt + 5 <= KT; kt += 3) {
+      block(kt, I0{}, T{}, T{});
+      block(kt + 1, I1{}, T{}, T{});
+      block(kt + 2, I2{}, T{}, T{});
+    }
+    // the last one to four blocks
+    block(kt, I0{}, kt + 1 < KT, kt + 2 < KT);
+    if (kt + 1 < KT) block(kt + 1, I1{}, kt + 2 < KT, kt + 3 < KT);
+    if (kt + 2 < KT) block(kt + 2, I2{}, kt + 3 < KT, false);
+    if (kt + 3 < KT) block(kt + 3, I0{}, false, false);
+
+    // epilogue: accumulator element v of lane l is row 8 (v / 4) + 4 (l / 32)
+    // + v % 4, column l % 32 of its 32 x 32 block; 32 lanes store 64
+    // contiguous bytes of a row
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        if (m < rows_g) {
+          const int grow = row_base + m;
+          if (MODE == MODE_GATEUP) {
+            C[(int64_t)grow * ldc + n0 + 32 * wave + (lane & 31)] =
+                f2bf(swiglu_bf16_epi(acc[i][0][v], acc[i][1][v]));
+          } else {
+            const int64_t orow = rows ? (int64_t)rows[grow] : (int64_t)grow;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+              C[orow * ldc + n0 + 64 * wave + 32 * t + (lane & 31)] = f2bf(acc[i][t][v]);
+          }
+        }
+      }
+    // the next item's prologue refills ring slots slower waves may still read
+    __syncthreads();
+  }
+}
+
+// Fragment order of row-major [rows, cols] matrices (rows % 32 == 0,
+// cols % 16 == 0): one thread per 16-byte piece of the destination.
+__global__ __launch_bounds__(256) void fragment_order_kernel(const bf16_t* __restrict__ src,
+                                                             int64_t n_mats, int rows, int cols,
+                                                             bf16_t* __restrict__ dst) {
+  const int64_t per = (int64_t)rows * cols / 8;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_mats * per) return;
+  const int64_t mat = i / per, r = i % per;
+  const int lane = (int)(r % 64);
+  const int64_t chunk = r / 64;
+  const int ks = (int)(chunk % (cols / 16));
+  const int64_t ng = chunk / (cols / 16);
+  const int64_t row = ng * 32 + lane % 32;
+  const int col = ks * 16 + (lane / 32) * 8;
+  reinterpret_cast<uint4*>(dst)[i] =
+      *reinterpret_cast<const uint4*>(src + (mat * rows + row) * cols + col);
+}
+
 // ---------------------------------------------------------------- bf16 MFMA, weight streaming
 // For groups of few rows (decode), where the GEMM reads each weight once and
 // is bound by HBM: one wave per workgroup owns 64 weight rows of one group
@@ -1731,6 +1962,41 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
         H, rows_out, goff, G, max_rows, (const float*)w_down, ffn, d, (float*)out, d);
     if (profile) prof_end(pd, s);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_fragment_order(const void* src, int64_t n_mats, int rows, int cols, void* dst,
+                                 hipStream_t s) {
+  const int64_t n = n_mats * rows * (int64_t)cols / 8;
+  if (n == 0) return hipSuccess;
+  launch_k(fragment_order_kernel, (unsigned)cdiv64(n, 256), 256, 0, s, (const bf16_t*)src, n_mats,
+           rows, cols, (bf16_t*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_ffn_fo(int G, int ffn, int d, const void* in, const int32_t* rows_in,
+                                 const int32_t* rows_out, const int32_t* goff, int64_t max_rows,
+                                 const void* w_gate_up_fo, const void* w_down_fo, void* out,
+                                 void* ws, hipStream_t s, int prof_gate_up) {
+  if (max_rows <= 0) return hipSuccess;
+  const bool profile = prof_gate_up >= 0;
+  bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+  // one workgroup per CU at most (streaming from HBM gains nothing from a
+  // second: measured on 26 experts x 4096 x 7168, 208 workgroups stream at
+  // 5.9 TB/s, 416 at 5.4)
+  auto grid = [&](int ncol, int nout) {
+    int64_t g = grid_for(max_rows, G, kFoBM, nout / ncol);
+    const int64_t cap = (int64_t)num_cus() / kXcd * kXcd;
+    return (unsigned)(g < cap ? g : cap);
+  };
+  if (profile) prof_begin(prof_gate_up, s);
+  launch_k(gemm_bf16_fo_kernel<MODE_GATEUP>, grid(128, ffn), 256, 0, s, (const bf16_t*)in,
+           rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up_fo, d, ffn, H, ffn);
+  if (profile) prof_end(prof_gate_up, s);
+  if (profile) prof_begin(prof_gate_up + 1, s);
+  launch_k(gemm_bf16_fo_kernel<MODE_DOWN>, grid(256, d), 256, 0, s, (const bf16_t*)H, rows_out,
+           goff, G, max_rows, (const bf16_t*)w_down_fo, ffn, d, (bf16_t*)out, d);
+  if (profile) prof_end(prof_gate_up + 1, s);
   return hipGetLastError();
 }
 

@@ -88,6 +88,16 @@ hipError_t launch_grouped_ffn_fp8(int n_groups, int ffn, int d, const uint8_t* x
                                   void* ws, hipStream_t s, int prof_gate_up);
 hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a, const void* w,
                                void* out, hipStream_t s);
+// Expert weights in MFMA fragment order: n_mats row-major [rows, cols] bf16
+// matrices (rows % 32 == 0, cols % 16 == 0) to [rows/32][cols/16][64][8].
+hipError_t launch_fragment_order(const void* src, int64_t n_mats, int rows, int cols, void* dst,
+                                 hipStream_t s);
+// The grouped SwiGLU FFN on fragment-ordered weights (bf16; ffn % 128 == 0,
+// d % 256 == 0); the workspace is that of launch_grouped_ffn.
+hipError_t launch_grouped_ffn_fo(int G, int ffn, int d, const void* in, const int32_t* rows_in,
+                                 const int32_t* rows_out, const int32_t* goff, int64_t max_rows,
+                                 const void* w_gate_up_fo, const void* w_down_fo, void* out,
+                                 void* ws, hipStream_t s, int prof_gate_up);
 
 // ---- combine and residual (elementwise.hip)
 // row_range (device, 2 ints) or NULL: only plan rows in [row_range[0],

@@ -71,7 +71,7 @@ def expect(status, fn, *args, **kw):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("abi_version", 7, L.FS_ERR_INVALID),
+    ("abi_version", L.FS_ABI_VERSION + 1, L.FS_ERR_INVALID),
     ("n_tokens", -1, L.FS_ERR_INVALID),
     ("hidden", 0, L.FS_ERR_INVALID),
     ("hidden", 7168 + 64, L.FS_ERR_UNSUPPORTED),
@@ -144,6 +144,17 @@ def test_other_entry_point_checks():
     assert "scratch" in msg
     expect(L.FS_ERR_INVALID, L.fs_grouped_expert_ffn, d, 32, 2048, FAKE, None, None, 100, FAKE, FAKE,
            FAKE, (FAKE, 1 << 40), stream=0)
+    # fragment order: bf16 only, whole 32-row x 16-column blocks, no overlap
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_expert_weights_fragment_order, L.FS_F32, 2, 64, 64, FAKE,
+           FAKE + (1 << 20), stream=0)
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_expert_weights_fragment_order, L.FS_BF16, 2, 48, 64, FAKE,
+           FAKE + (1 << 20), stream=0)
+    expect(L.FS_ERR_INVALID, L.fs_expert_weights_fragment_order, L.FS_BF16, 2, 64, 64, FAKE,
+           FAKE + 4096, stream=0)
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_grouped_expert_ffn_fo, desc("tiny"), 8, 512, FAKE, None,
+           FAKE, 100, FAKE, FAKE, FAKE, (FAKE, 1 << 40), stream=0)
+    expect(L.FS_ERR_WORKSPACE, L.fs_grouped_expert_ffn_fo, d, 32, 2048, FAKE, None, FAKE, 100,
+           FAKE, FAKE, FAKE, (FAKE, 64), stream=0)
     expect(L.FS_ERR_UNSUPPORTED, L.fs_grouped_expert_ffn, d, 32, 100, FAKE, None, FAKE, 100, FAKE,
            FAKE, FAKE, (FAKE, 1 << 40), stream=0)
     expect(L.FS_ERR_WORKSPACE, L.fs_grouped_expert_ffn, d, 32, 2048, FAKE, None, FAKE, 100, FAKE,

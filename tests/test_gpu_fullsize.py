@@ -103,15 +103,20 @@ def expert_input_tokens(cfg, blk, wl, plan, e_local):
     return src, tok, y
 
 
-@pytest.mark.parametrize("name", ["tiny", "dsv2lite", "scout", "dsv3_prefill", "dsv3_decode"])
-def test_fullsize_block(name):
+@pytest.mark.parametrize("name,fo", [("tiny", False), ("dsv2lite", False), ("scout", False),
+                                     ("dsv3_prefill", False), ("dsv3_decode", False),
+                                     ("dsv3_decode", True)])
+def test_fullsize_block(name, fo):
+    """fo: the block also holds fragment-ordered expert weights, which its
+    routed passes stream at decode sizes."""
     cfg = CONFIGS[name]
-    print(f"\n[fullsize {name}] start", flush=True)
+    print(f"\n[fullsize {name}{' fragment-ordered' if fo else ''}] start", flush=True)
     wl = make_workload(cfg, DEV)
     sh_gu = sh_dn = None
     if cfg.n_shared > 0:
         sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
-    blk = MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=DEV)
+    blk = MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=DEV,
+                   fragment_order=fo)
     if cfg.ep_size > 1:
         blk.set_max_recv_rows(prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias, wl.y_remote))
     comm = torch.cuda.Stream()

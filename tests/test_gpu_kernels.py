@@ -9,6 +9,7 @@ import torch
 
 import oracle
 from paper_2511_11505_amd import _lib as L
+from paper_2511_11505_amd.block import fragment_ordered
 from tests._util import TOL, f64, rel_err
 from workloads import CONFIGS, make_workload
 from workloads.generate import synthetic_topk_ids
@@ -391,3 +392,50 @@ def test_profile_select_times_only_the_selected_kernels():
         L.fs_profile_enable(False)
         L.fs_profile_select(None)
         L.fs_profile_reset()
+
+
+def test_fragment_order_layout():
+    # block (g, c) of a matrix holds, at lane l, row 32 g + l % 32 and
+    # columns 16 c + 8 (l / 32) .. + 7: a plain reshape of the row-major
+    # matrix, checked bit for bit
+    gen = torch.Generator(device=DEV).manual_seed(5)
+    w = torch.randn((3, 96, 48), generator=gen, device=DEV).to(torch.bfloat16)
+    fo = fragment_ordered(w)
+    torch.cuda.synchronize()
+    a = w.view(torch.int16).cpu().numpy().reshape(3, 3, 32, 3, 2, 8)   # [m][g][r][c][h][e]
+    want = a.transpose(0, 1, 3, 4, 2, 5).reshape(-1)                   # [m][g][c][h][r][e]
+    assert np.array_equal(fo.view(torch.int16).cpu().numpy().reshape(-1), want)
+
+
+@pytest.mark.parametrize("counts,d,F,gather", [
+    ([0, 1, 64, 65, 130], 768, 256, True),      # empty, single-row, one and three 64-row tiles
+    ([37], 512, 128, False),                    # one group
+    ([3, 0, 5, 9, 1, 0, 2, 7], 256, 384, True),   # many small groups, K of 4 blocks (tail)
+    ([20, 113, 0, 61, 2], 1024, 640, True),     # K rings of 16 and 10 blocks (ragged tails)
+])
+def test_grouped_ffn_fragment_order(counts, d, F, gather):
+    """The grouped SwiGLU FFN on fragment-ordered weights (weights streamed
+    straight into the matrix units' registers), element by element against
+    the oracle; rows outside the groups are never written."""
+    counts = np.array(counts)
+    G, M = len(counts), int(counts.sum())
+    goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    gen = torch.Generator(device=DEV).manual_seed(d * 3 + F)
+    n_src = M + 13
+    X = torch.randn((n_src, d), generator=gen, device=DEV).to(torch.bfloat16)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(torch.bfloat16)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(torch.bfloat16)
+    rows = torch.randperm(n_src, generator=gen, device=DEV)[:M].to(torch.int32) if gather else None
+    out = torch.full((n_src, d), float("nan"), device=DEV).to(torch.bfloat16)
+    desc = L.make_desc(CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16"))
+    L.fs_grouped_expert_ffn_fo(desc, G, F, X, rows, torch.from_numpy(goff).to(DEV), M,
+                               fragment_ordered(wgu), fragment_ordered(wd), out,
+                               ws_for(desc, L.FS_OP_GROUPED_FFN, M, F))
+    torch.cuda.synchronize()
+    Xn, gun, dnn, outn = f64(X), f64(wgu), f64(wd), f64(out)
+    rr = rows.cpu().numpy() if gather else np.arange(M)
+    for gi in range(G):
+        sel = rr[goff[gi]:goff[gi + 1]]
+        if len(sel):
+            assert rel_err(outn[sel], oracle.swiglu(Xn[sel], gun[gi], dnn[gi])) <= TOL["bf16"], f"group {gi}"
+    assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
