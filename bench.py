@@ -239,6 +239,26 @@ def bench_layers(args, cfg, torch, L):
     ms_fs, k_fs = timed(lambda: st.farskip(x, compute=compute, comm=comm))
     ms_rg, k_rg = timed(lambda: st.regular(x, compute=compute))
     us = lambda k, name: k[name]["us_per_launch"] if name in k else 0.0
+    link = None
+    if args.link_gbs > 0:
+        # both schedules again, every stand-in copy paced at the time the
+        # all-to-all of its buffer takes on 8 GPUs joined by 7 links each
+        with L.standin_link(7, args.link_gbs * 1e9, args.link_wgs):
+            ms_fs_l, k_fs_l = timed(lambda: st.farskip(x, compute=compute, comm=comm))
+            ms_rg_l, k_rg_l = timed(lambda: st.regular(x, compute=compute))
+        link = {"links": 7, "link_gbs": args.link_gbs, "workgroups": args.link_wgs,
+                "copy_model_us_each": round(cfg.cap * cfg.hidden * cfg.elem_bytes / 8
+                                            / (args.link_gbs * 1e9) * 1e6, 2),
+                "farskip_ms_per_step": ms_fs_l, "regular_ms_per_step": ms_rg_l,
+                "speedup_vs_regular": ms_rg_l / ms_fs_l,
+                "farskip_copy_us": {n: round(us(k_fs_l, n), 2) for n in ("dispatch_copy", "combine_copy")},
+                "regular_copy_us": {n: round(us(k_rg_l, n), 2) for n in ("dispatch_copy", "combine_copy")},
+                "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs_l.items()},
+                "note": "both schedules measured with each Dispatch and Combine stand-in copy "
+                        "run on link_wgs workgroups and paced to the time the all-to-all of its "
+                        "buffer takes on a node of 8 GPUs (1/8 of the buffer per link at "
+                        "link_gbs, all links at once); the link rate is emulated, the overlap, "
+                        "the copies' CU and HBM use and the schedule are measured"}
     per_layer = ms_fs * 1e3 / args.layers
     gate = sum(us(k_fs, n) for n in ("router", "topk", "plan", "pack"))
     routed = us(k_fs, "gate_up") + us(k_fs, "down")
@@ -271,6 +291,7 @@ def bench_layers(args, cfg, torch, L):
                        "farskip_copies_fit_window": 2 * xgmi_us <= per_layer - routed - gate,
                        "note": "regular schedule with its measured blocking copies replaced by "
                                "all-to-all time on an 8-GPU xGMI node (model, not a measurement)"},
+        "link_emulated": link,
         "eq9_per_layer_us": {"dispatch_plus_combine": round(comm_us, 2),
                              "layer": round(per_layer, 2), "routed_experts": round(routed, 2),
                              "gate": round(gate, 2),
@@ -331,13 +352,40 @@ def bench_replicated(args, cfg, torch, L):
 
     ms_fs, k_fs = timed(lambda: st.farskip(x, compute=compute, comm=comm))
     if args.farskip_only:
-        print(json.dumps({"schedule": "farskip", "ms_per_step": ms_fs,
-                          "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()}}),
-              flush=True)
+        line = {"schedule": "farskip", "ms_per_step": ms_fs,
+                "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs.items()}}
+        if args.link_gbs > 0:
+            # then with the link-paced all-reduce stand-ins
+            with L.standin_link(7, args.link_gbs * 1e9, args.link_wgs):
+                ms_l, k_l = timed(lambda: st.farskip(x, compute=compute, comm=comm))
+            line["link_emulated"] = {"ms_per_step": ms_l, "kernels_us": {
+                k2: round(v["us_per_launch"], 2) for k2, v in k_l.items()}}
+        print(json.dumps(line), flush=True)
         return
     ms_serial, _ = timed(lambda: st.farskip(x, compute=compute, comm=None))
     ms_rg, k_rg = timed(lambda: st.regular(x, compute=compute))
     us = lambda k, name: k[name]["us_per_launch"] if name in k else 0.0
+    link = None
+    if args.link_gbs > 0:
+        # both schedules again, every all-reduce stand-in paced at the time
+        # a ring all-reduce of its message takes over the 7 links of each
+        # of 8 GPUs
+        with L.standin_link(7, args.link_gbs * 1e9, args.link_wgs):
+            ms_fs_l, k_fs_l = timed(lambda: st.farskip(x, compute=compute, comm=comm))
+            ms_rg_l, k_rg_l = timed(lambda: st.regular(x, compute=compute))
+        link = {"links": 7, "link_gbs": args.link_gbs, "workgroups": args.link_wgs,
+                "allreduce_model_us": round(2 * cfg.n_tokens * cfg.hidden * cfg.elem_bytes / 8
+                                            / (args.link_gbs * 1e9) * 1e6, 2),
+                "farskip_ms_per_step": ms_fs_l, "regular_ms_per_step": ms_rg_l,
+                "speedup_vs_regular": ms_rg_l / ms_fs_l,
+                "farskip_copy_us": round(us(k_fs_l, "allreduce_copy"), 2),
+                "regular_copy_us": round(us(k_rg_l, "allreduce_copy"), 2),
+                "kernels_us": {k2: round(v["us_per_launch"], 2) for k2, v in k_fs_l.items()},
+                "note": "both schedules measured with each all-reduce stand-in copy run on "
+                        "link_wgs workgroups and paced to the time a ring all-reduce of the "
+                        "message takes over every link of a node of 8 GPUs (link_gbs per "
+                        "direction); the link rate is emulated, the overlap, the copies' CU "
+                        "and HBM use and the schedule are measured"}
     N, d, F, es = cfg.n_tokens, cfg.hidden, cfg.ffn, cfg.elem_bytes
     per_layer = ms_fs * 1e3 / args.layers
     attention = 2 * us(k_fs, "next_layer")
@@ -400,6 +448,7 @@ def bench_replicated(args, cfg, torch, L):
             "allreduce_copy": round(copy, 2),
             "note": "the attention + shared all-reduce hides behind the routed experts, "
                     "the routed all-reduce behind the next attention"},
+        "link_emulated": link,
         "allreduce_model": {"message_bytes": msg_bytes, "at_400GBs_bus": m400,
                             "at_7_xgmi_links": mlinks,
                             "note": "measured times with each stand-in copy replaced by a ring "
@@ -438,8 +487,14 @@ def main():
     ap.add_argument("--fp8", choices=("routed", "all"), default=None,
                     help="run the routed (or routed and shared) experts in FP8 E4M3")
     ap.add_argument("--farskip-only", action="store_true",
-                    help="replicated-activation workloads: time only the two-stream FarSkip schedule "
-                         "(for kernel traces)")
+                    help="replicated-activation workloads: time only the two-stream FarSkip schedule, "
+                         "with HBM-speed and then link-paced copies (for kernel traces)")
+    ap.add_argument("--link-gbs", type=float, default=153.0,
+                    help="stacked-layer runs: also time both schedules with every stand-in copy "
+                         "paced at the time its collective takes on a node of 8 GPUs joined by "
+                         "links of this many GB/s per direction (0: skip)")
+    ap.add_argument("--link-wgs", type=int, default=128,
+                    help="workgroups of each link-paced stand-in copy")
     ap.add_argument("--overlap", action="store_true",
                     help="run the next-layer stand-in (d x d linear) between BEGIN and FINISH and "
                          "compare with a serial run")

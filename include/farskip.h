@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 7
+#define FS_ABI_VERSION 8
 
 typedef enum {
   FS_OK = 0,
@@ -398,12 +398,34 @@ fs_status fs_combine_partial(const fs_moe_desc* desc, const void* y_local,
 
 /* One-GPU stand-in for the all-reduce of an [N, d] dtype partial sum over
  * the R ranks (Section 4.2): with one participant the sum is the partial
- * itself, so out = partial as a device-to-device copy on `stream` (the
- * traffic and the stream placement of the collective; on a node RCCL's
- * all-reduce takes its place).  out == partial is an in-place no-op; other
- * overlaps are FS_ERR_INVALID. */
+ * itself, so out = partial as a stand-in copy on `stream` (the traffic and
+ * the stream placement of the collective, and with fs_standin_link its
+ * duration; on a node RCCL's all-reduce takes its place).  out == partial
+ * is an in-place no-op; other overlaps are FS_ERR_INVALID. */
 fs_status fs_allreduce_standin(const fs_moe_desc* desc, void* out, const void* partial,
                                fs_stream stream);
+
+/* Link model of the one-GPU stand-in copies: the Dispatch and Combine
+ * copies of fs_moe_block_forward (the all-to-alls of Section 2.1) and
+ * fs_allreduce_standin (the all-reduces of Section 4.2).  Process-wide;
+ * applies to copies enqueued after the call.
+ *   links == 0 (the default): each stand-in copy is a device-to-device copy
+ *     at HBM speed (the arguments after links are ignored).
+ *   links > 0: each runs as a copy kernel on `workgroups` workgroups that
+ *     takes the time the collective would take on a node of links + 1 GPUs,
+ *     every pair joined by one link of link_bytes_per_s per direction:
+ *     B / ((links + 1) * link_bytes_per_s) for an all-to-all of a B-byte
+ *     send buffer (each peer's share on its own link, all links at once),
+ *     twice that for a ring all-reduce of B bytes over every link.  Byte b
+ *     of the buffer is read no earlier than b / rate after the kernel
+ *     starts, so the copy takes HBM bandwidth and CUs as a transfer at that
+ *     rate would; it takes longer when the workgroups cannot keep up.
+ * The bytes copied are the same either way.  links in [0, 1023];
+ * link_bytes_per_s in [1e9, 1e15] and workgroups in [1, 4096] when links > 0;
+ * else FS_ERR_INVALID and the setting is unchanged.  No GPU work. */
+fs_status fs_standin_link(int32_t links, double link_bytes_per_s, int32_t workgroups);
+/* The current link model (links 0: HBM-speed copies). */
+fs_status fs_standin_link_get(int32_t* links, double* link_bytes_per_s, int32_t* workgroups);
 
 /* FarSkip residual add (Eq. 7): out = residual + deferred (+ extra), in
  * fp32 with one rounding.  out may equal residual (in place).  [N, d]
@@ -481,8 +503,8 @@ fs_status fs_block_sync_destroy(fs_block_sync* sync);
 /* One FarSkip MoE block forward (Section 3 connectivity, Section 4.1
  * schedule), in phases that let the caller place other work between them.
  *   FS_PHASE_GATE on `compute`: router + top-k, plan + pack; then the
- *     Dispatch stand-in: on `comm` (after an event), a device-to-device copy
- *     of the whole send buffer into receive slot r.
+ *     Dispatch stand-in: on `comm` (after an event), a stand-in copy
+ *     (fs_standin_link) of the whole send buffer into receive slot r.
  *   FS_PHASE_SHARED on `compute`: the shared experts on residual_in and
  *     partial_out = residual_in + shared_out (Eq. 8b: the next layer's input
  *     without the routed output).

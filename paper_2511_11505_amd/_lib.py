@@ -22,7 +22,7 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
  FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_QUANTIZE, FS_K_COUNT) = range(15)
-FS_ABI_VERSION = 7
+FS_ABI_VERSION = 8
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -81,6 +81,9 @@ _SIGS = {
                                          _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fs_combine_partial": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
     "fs_allreduce_standin": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp]),
+    "fs_standin_link": (_i32, [_i32, ctypes.c_double, _i32]),
+    "fs_standin_link_get": (_i32, [ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(_i32)]),
     "fs_farskip_residual": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp]),
     "fs_block_sync_create": (_i32, [ctypes.POINTER(_vp)]),
     "fs_block_sync_destroy": (_i32, [_vp]),
@@ -282,6 +285,33 @@ def fs_combine_partial(desc, y_local, slot_to_row, rank_offsets, topk_w, partial
 def fs_allreduce_standin(desc, out, partial, stream=None):
     _check(load().fs_allreduce_standin(ctypes.byref(desc), ptr(out), ptr(partial),
                                        stream_handle(stream)))
+
+
+def fs_standin_link(links, link_bytes_per_s=0.0, workgroups=0):
+    _check(load().fs_standin_link(int(links), float(link_bytes_per_s), int(workgroups)))
+
+
+def fs_standin_link_get():
+    n, b, w = _i32(), ctypes.c_double(), _i32()
+    _check(load().fs_standin_link_get(ctypes.byref(n), ctypes.byref(b), ctypes.byref(w)))
+    return n.value, b.value, w.value
+
+
+class standin_link:
+    """Context manager: the stand-in copies inside follow a node of
+    links + 1 GPUs joined by links of link_bytes_per_s per direction
+    (fs_standin_link); the previous setting comes back on exit."""
+
+    def __init__(self, links=7, link_bytes_per_s=153e9, workgroups=128):
+        self.args = (links, link_bytes_per_s, workgroups)
+
+    def __enter__(self):
+        self.prev = fs_standin_link_get()
+        fs_standin_link(*self.args)
+        return self
+
+    def __exit__(self, *exc):
+        fs_standin_link(*self.prev)
 
 
 def fs_farskip_residual(desc, out, residual, deferred, extra=None, stream=None):

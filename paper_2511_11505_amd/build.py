@@ -24,7 +24,8 @@ COMMON = [
 # The router's fixed fp32 reduction order needs products and sums rounded
 # separately for fp32 inputs: no contraction in that file.
 PER_FILE = {"router.hip": ["-ffp-contract=off"]}
-SOURCES = ["api.cpp", "router.hip", "dispatch.hip", "gemm.hip", "elementwise.hip", "fp8.hip"]
+SOURCES = ["api.cpp", "router.hip", "dispatch.hip", "gemm.hip", "elementwise.hip", "fp8.hip",
+           "standin.hip"]
 
 
 def _compile(src):

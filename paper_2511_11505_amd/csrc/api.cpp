@@ -185,6 +185,32 @@ size_t block_bytes(const fs_moe_desc* d, int64_t max_rows, bool fp8_routed, bool
   return b;
 }
 
+// Link model of the stand-in collectives (fs_standin_link); links == 0:
+// device-to-device copies at HBM speed.
+struct LinkModel {
+  int links = 0;
+  double bytes_per_s = 0.0;
+  int workgroups = 0;
+};
+std::mutex g_link_mu;
+LinkModel g_link;
+
+LinkModel link_model() {
+  std::lock_guard<std::mutex> g(g_link_mu);
+  return g_link;
+}
+
+// One stand-in copy of a collective moving `bytes` per GPU: `factor` 1 for
+// an all-to-all (each of the links + 1 GPUs' shares crosses its own link,
+// all links at once: bytes / ((links + 1) rate)), 2 for a ring all-reduce
+// over every link (2 (n - 1) / n bytes out of each GPU over n - 1 links).
+hipError_t standin_copy(void* dst, const void* src, size_t bytes, double factor, hipStream_t s) {
+  const LinkModel m = link_model();
+  if (m.links == 0) return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s);
+  const double seconds = factor * (double)bytes / ((double)(m.links + 1) * m.bytes_per_s);
+  return fs::launch_paced_copy(dst, src, bytes, seconds, m.workgroups, s);
+}
+
 }  // namespace
 
 namespace fs {
@@ -736,8 +762,31 @@ fs_status fs_allreduce_standin(const fs_moe_desc* desc, void* out, const void* p
   hipStream_t s = S(stream);
   if (o == p) return FS_OK;
   fs::prof_begin(FS_K_ALLREDUCE_COPY, s);
-  FS_HIP(hipMemcpyAsync(out, partial, bytes, hipMemcpyDeviceToDevice, s), "hipMemcpyAsync");
+  FS_HIP(standin_copy(out, partial, bytes, 2.0, s), "allreduce stand-in copy");
   fs::prof_end(FS_K_ALLREDUCE_COPY, s);
+  return FS_OK;
+}
+
+fs_status fs_standin_link(int32_t links, double link_bytes_per_s, int32_t workgroups) {
+  if (links < 0 || links > 1023) return fail(FS_ERR_INVALID, "links must be in [0, 1023]");
+  if (links > 0) {
+    if (!(link_bytes_per_s >= 1e9 && link_bytes_per_s <= 1e15))
+      return fail(FS_ERR_INVALID, "link_bytes_per_s must be in [1e9, 1e15]");
+    if (workgroups < 1 || workgroups > 4096)
+      return fail(FS_ERR_INVALID, "workgroups must be in [1, 4096]");
+  }
+  std::lock_guard<std::mutex> g(g_link_mu);
+  g_link = links > 0 ? LinkModel{links, link_bytes_per_s, workgroups} : LinkModel{};
+  return FS_OK;
+}
+
+fs_status fs_standin_link_get(int32_t* links, double* link_bytes_per_s, int32_t* workgroups) {
+  if (!links || !link_bytes_per_s || !workgroups)
+    return fail(FS_ERR_INVALID, "outputs must not be NULL");
+  const LinkModel m = link_model();
+  *links = m.links;
+  *link_bytes_per_s = m.bytes_per_s;
+  *workgroups = m.workgroups;
   return FS_OK;
 }
 
@@ -941,15 +990,12 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
   auto dispatch_copy = [&](hipStream_t st) -> fs_status {
     fs::prof_begin(FS_K_DISPATCH_COPY, st);
     if (fp8_routed) {
-      FS_HIP(hipMemcpyAsync(recv_codes + (size_t)r * cap * D, send_codes, (size_t)cap * D,
-                            hipMemcpyDeviceToDevice, st),
-             "hipMemcpyAsync");
-      FS_HIP(hipMemcpyAsync(recv_scales + (size_t)r * cap, send_scales, (size_t)cap * 4,
-                            hipMemcpyDeviceToDevice, st),
-             "hipMemcpyAsync");
+      FS_HIP(standin_copy(recv_codes + (size_t)r * cap * D, send_codes, (size_t)cap * D, 1.0, st),
+             "dispatch stand-in copy");
+      FS_HIP(standin_copy(recv_scales + (size_t)r * cap, send_scales, (size_t)cap * 4, 1.0, st),
+             "dispatch stand-in copy");
     } else {
-      FS_HIP(hipMemcpyAsync(recv_slot, b->send, slot_bytes, hipMemcpyDeviceToDevice, st),
-             "hipMemcpyAsync");
+      FS_HIP(standin_copy(recv_slot, b->send, slot_bytes, 1.0, st), "dispatch stand-in copy");
     }
     fs::prof_end(FS_K_DISPATCH_COPY, st);
     return FS_OK;
@@ -1058,15 +1104,13 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
         FS_HIP(hipEventRecord(sync->computed, sc), "hipEventRecord");
         FS_HIP(hipStreamWaitEvent(sm, sync->computed, 0), "hipStreamWaitEvent");
         fs::prof_begin(FS_K_COMBINE_COPY, sm);
-        FS_HIP(hipMemcpyAsync(b->ret, y_slot, slot_bytes, hipMemcpyDeviceToDevice, sm),
-               "hipMemcpyAsync");
+        FS_HIP(standin_copy(b->ret, y_slot, slot_bytes, 1.0, sm), "combine stand-in copy");
         fs::prof_end(FS_K_COMBINE_COPY, sm);
         FS_HIP(hipEventRecord(sync->returned, sm), "hipEventRecord");
         sync->have_return = true;
       } else {
         fs::prof_begin(FS_K_COMBINE_COPY, sc);
-        FS_HIP(hipMemcpyAsync(b->ret, y_slot, slot_bytes, hipMemcpyDeviceToDevice, sc),
-               "hipMemcpyAsync");
+        FS_HIP(standin_copy(b->ret, y_slot, slot_bytes, 1.0, sc), "combine stand-in copy");
         fs::prof_end(FS_K_COMBINE_COPY, sc);
       }
     }

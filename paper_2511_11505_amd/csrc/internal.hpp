@@ -109,4 +109,11 @@ hipError_t launch_combine(int dtype, const void* y_ret, const int32_t* slot_to_r
 hipError_t launch_residual(int dtype, void* out, const void* a, const void* b, const void* c,
                            int64_t n_elems, hipStream_t s);
 
+// ---- stand-in collectives (standin.hip)
+// Copy `bytes` from src to dst with `workgroups` workgroups, taking at least
+// `seconds` (0: unpaced); see the kernel's comment for the schedule.
+// Pointers and bytes must be multiples of 4 (else hipErrorInvalidValue).
+hipError_t launch_paced_copy(void* dst, const void* src, size_t bytes, double seconds,
+                             int workgroups, hipStream_t s);
+
 }  // namespace fs

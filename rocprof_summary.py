@@ -16,7 +16,9 @@ each way; the copy dispatches taken are those reading the most.
 With --overlap, it instead reports, for every copy dispatched on the stream
 that carries the largest copies (the Dispatch stand-in), the fraction of the
 copy's interval during which a kernel of another stream runs:
-|copy ∩ (∪ compute kernels)| / |copy|.
+|copy ∩ (∪ compute kernels)| / |copy|; --copy-kernel selects the copies by
+kernel name (the HBM-speed blit by default, paced_copy for the link-paced
+stand-in copies).
 
 With --mfma PMC_DIR (a `rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES
 SQ_INSTS_VALU_MFMA_MOPS_BF16` run), it reports per kernel the fraction of
@@ -90,10 +92,10 @@ def window_report(trace_dir, substring, start, count):
           f"{sum(d) / len(d):.2f} us (min {min(d):.2f}, max {max(d):.2f})")
 
 
-def overlap_report(trace_dir, min_us, skip):
+def overlap_report(trace_dir, min_us, skip, copy_kernel="copyBuffer"):
     rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
     span = lambda r: (int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
-    copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+    copies = [r for r in rows if copy_kernel in r["Kernel_Name"]]
     longest = max(span(r)[1] - span(r)[0] for r in copies)
     streams = {r["Stream_Id"] for r in copies if span(r)[1] - span(r)[0] >= 0.5 * longest}
     if len(streams) != 1:
@@ -196,6 +198,9 @@ def main():
     ap.add_argument("--min-us", type=float, default=1.0)
     ap.add_argument("--overlap", action="store_true")
     ap.add_argument("--skip", type=int, default=0, help="--overlap: leading copies to skip (warm-up)")
+    ap.add_argument("--copy-kernel", default="copyBuffer",
+                    help="--overlap: kernel-name substring of the copies (paced_copy: the "
+                         "link-paced stand-in copies)")
     ap.add_argument("--mfma")
     ap.add_argument("--memory", action="append", default=[],
                     help="counter-run directories for the GEMM memory-pipeline table")
@@ -212,7 +217,7 @@ def main():
     keep = (lambda k: True) if a.all_kernels else (lambda k: not k.startswith("torch:"))
     scales, kib = {}, {}
     if a.overlap:
-        overlap_report(a.trace_dir, a.min_us, a.skip)
+        overlap_report(a.trace_dir, a.min_us, a.skip, a.copy_kernel)
         return
     if a.mfma:
         mfma_report(a.trace_dir, a.mfma, a.min_us)

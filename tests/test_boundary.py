@@ -193,3 +193,22 @@ def test_empty_batch_is_a_noop():
     d = desc(n_tokens=0)
     L.fs_router_topk(d, None, None, None, None, None, None, None, None, stream=0)
     L.fs_combine_unpack(d, None, None, None, None, None, None, stream=0)
+
+
+def test_standin_link_setting():
+    # process-wide link model of the stand-in copies: set, read back,
+    # rejected arguments leave it unchanged, links 0 restores HBM copies
+    assert L.fs_standin_link_get() == (0, 0.0, 0)
+    L.fs_standin_link(7, 153e9, 64)
+    assert L.fs_standin_link_get() == (7, 153e9, 64)
+    for args in [(-1, 153e9, 64), (1024, 153e9, 64), (7, 5e8, 64), (7, 2e15, 64), (7, float("nan"), 64),
+                 (7, 153e9, 0), (7, 153e9, 4097)]:
+        with pytest.raises(L.FsError) as e:
+            L.fs_standin_link(*args)
+        assert e.value.status == L.FS_ERR_INVALID
+        assert L.fs_standin_link_get() == (7, 153e9, 64)
+    with L.standin_link(3, 50e9, 8):
+        assert L.fs_standin_link_get() == (3, 50e9, 8)
+    assert L.fs_standin_link_get() == (7, 153e9, 64)
+    L.fs_standin_link(0, -1.0, -5)          # links 0 ignores the rest
+    assert L.fs_standin_link_get() == (0, 0.0, 0)

@@ -195,6 +195,12 @@ def test_replicated_stack_matches_oracle(name, n_layers):
     fs_serial = st.farskip(x, comm=None).clone()
     torch.cuda.synchronize()
     assert torch.equal(fs, fs_serial)
+    # the all-reduce stand-ins paced at the modelled link time copy the same bytes
+    with L.standin_link(7, 153e9, 64):
+        fs_link = st.farskip(x, comm=comm).clone()
+        rg_link = st.regular(x).clone()
+        torch.cuda.synchronize()
+    assert torch.equal(fs, fs_link)
     near = []
     want_fs, _ = ar.farskip_ar_stack(cfg, f64(x), ol,
                                      ids_given=choosers(cfg, ids_fs, z_fs, ol, near))
@@ -207,6 +213,7 @@ def test_replicated_stack_matches_oracle(name, n_layers):
     want_rg, _ = ar.regular_ar_stack(cfg, f64(x), ol,
                                      ids_given=choosers(cfg, ids_rg, z_rg, ol, near))
     assert rel_err(f64(rg), want_rg) <= tol
+    assert torch.equal(rg, rg_link)
     print(f"[replicated {name}] (near-tie tokens, max logit difference / rms) per layer, "
           f"FarSkip then regular: {near}")
     assert rel_err(f64(fs), want_rg) > 2 * rel_err(f64(fs), want_fs)

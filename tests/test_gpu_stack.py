@@ -31,6 +31,7 @@ import pytest
 import torch
 
 import oracle
+from paper_2511_11505_amd import _lib as L
 from paper_2511_11505_amd.stack import LayerStack
 from tests._util import TOL, f64, rel_err
 from tests.test_gpu_fullsize import check_valid_choice
@@ -110,6 +111,13 @@ def test_stack_matches_oracle(name, n_layers):
     torch.cuda.synchronize()
     # the two-stream schedule computes exactly what the one-stream order does
     assert torch.equal(fs, fs_serial)
+    # so do both schedules with the Dispatch and Combine stand-ins paced at
+    # the modelled link time
+    with L.standin_link(7, 153e9, 64):
+        fs_link = st.farskip(x, comm=comm).clone()
+        rg_link = st.regular(x).clone()
+        torch.cuda.synchronize()
+    assert torch.equal(fs, fs_link)
     near = []
     want_fs, _ = oracle.farskip_stack(cfg, f64(x), ol,
                                       ids_given=choosers(cfg, ids_fs, z_fs, ol, near))
@@ -121,6 +129,7 @@ def test_stack_matches_oracle(name, n_layers):
     want_rg, _ = oracle.regular_stack(cfg, f64(x), ol,
                                       ids_given=choosers(cfg, ids_rg, z_rg, ol, near))
     assert rel_err(f64(rg), want_rg) <= tol
+    assert torch.equal(rg, rg_link)
     print(f"[stack {name}] (near-tie tokens, max logit difference / rms) per layer, FarSkip "
           f"then regular: {near}")
     # each schedule computes its own connectivity, not the other one: the
