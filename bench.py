@@ -495,6 +495,8 @@ def main():
                          "links of this many GB/s per direction (0: skip)")
     ap.add_argument("--link-wgs", type=int, default=128,
                     help="workgroups of each link-paced stand-in copy")
+    ap.add_argument("--vendor-reference", action="store_true",
+                    help="also time the block's GEMM passes as plain hipBLASLt GEMMs (context)")
     ap.add_argument("--overlap", action="store_true",
                     help="run the next-layer stand-in (d x d linear) between BEGIN and FINISH and "
                          "compare with a serial run")
@@ -527,9 +529,94 @@ def main():
             r2 = bench_block(args, CONFIGS[name], torch, L, with_cpu=False)
             res["workloads"][name] = {key: r2[key] for key in (
                 "value", "unit", "ms_per_step", "config", "roofline", "ffn", "permute_frac_hbm",
-                "step_roofline_frac", "block_roofline_frac", "kernels_us") if key in r2}
+                "step_roofline_frac", "block_roofline_frac", "kernels_us", "vendor_reference")
+                if key in r2}
             torch.cuda.empty_cache()
     print(json.dumps(res), flush=True)
+
+
+def vendor_reference(cfg, blk, wl, kernels, torch):
+    """The block's four GEMM passes as plain hipBLASLt GEMMs (torch.matmul),
+    for context: the routed passes as one GEMM per local expert with the
+    block's own row counts, the shared passes as one dense GEMM each.  They
+    do less than the library's passes (no row gather or scatter, no SwiGLU
+    epilogue), on random inputs of the same shapes and distribution."""
+    dev = "cuda:0"
+    d, F, E_loc = cfg.hidden, cfg.ffn, cfg.n_local
+    lo = cfg.ep_rank * E_loc
+    counts = blk.t["src_counts"][:, lo:lo + E_loc].sum(0).tolist()
+    dt = torch.bfloat16
+    g = torch.Generator(device=dev).manual_seed(7)
+    xs = [torch.randn((n, d), generator=g, device=dev, dtype=torch.float32).to(dt) for n in counts]
+    hs = [torch.randn((n, F), generator=g, device=dev, dtype=torch.float32).to(dt) for n in counts]
+
+    def timed(fn, reps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3
+
+    def routed(inputs, w):
+        for e, xe in enumerate(inputs):
+            if xe.shape[0]:
+                torch.matmul(xe, w[e].t())
+    M = sum(counts)
+    ref = {"gate_up": timed(lambda: routed(xs, wl.w_gate_up)),
+           "down": timed(lambda: routed(hs, wl.w_down))}
+    flops = {"gate_up": 2.0 * M * d * 2 * F, "down": 2.0 * M * F * d}
+    if cfg.n_shared > 0 and blk.weights_keep[4] is not None:
+        sh_gu, sh_dn = blk.weights_keep[4], blk.weights_keep[5]
+        Fs = sh_dn.shape[1]
+        x = torch.randn((cfg.n_tokens, d), generator=g, device=dev, dtype=torch.float32).to(dt)
+        h = torch.randn((cfg.n_tokens, Fs), generator=g, device=dev, dtype=torch.float32).to(dt)
+        ref["shared_gate_up"] = timed(lambda: torch.matmul(x, sh_gu.t()))
+        ref["shared_down"] = timed(lambda: torch.matmul(h, sh_dn.t()))
+        # the library's shared FFN alone (in the block it runs beside the
+        # Dispatch stand-in copy)
+        from paper_2511_11505_amd import _lib as L
+        ws = torch.empty((max(L.fs_workspace_size(blk.desc, L.FS_OP_GROUPED_FFN, cfg.n_tokens, Fs), 256),),
+                         dtype=torch.uint8, device=dev)
+        y = torch.empty((cfg.n_tokens, d), dtype=dt, device=dev)
+        run = lambda: L.fs_grouped_expert_ffn(blk.desc, 1, Fs, x, None, None, cfg.n_tokens, sh_gu,
+                                              sh_dn, y, ws)
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        L.fs_profile_reset()
+        L.fs_profile_select([L.FS_K_SHARED_GATE_UP, L.FS_K_SHARED_DOWN])
+        L.fs_profile_enable(True)
+        for _ in range(10):
+            run()
+        torch.cuda.synchronize()
+        L.fs_profile_enable(False)
+        alone = kernel_table(L)
+        L.fs_profile_reset()
+        L.fs_profile_select(None)
+        flops["shared_gate_up"] = 2.0 * cfg.n_tokens * d * 2 * Fs
+        flops["shared_down"] = 2.0 * cfg.n_tokens * Fs * d
+    else:
+        alone = {}
+    out = {}
+    frac = lambda k, us: round(flops[k] / us / 1e6 / PEAK_BF16_TFLOPS, 4)
+    for k, us in ref.items():
+        ours = kernels.get(k, {}).get("us_per_launch")
+        out[k] = {"hipblaslt_us": round(us, 2), "hipblaslt_frac": frac(k, us),
+                  "ours_us": round(ours, 2) if ours else None,
+                  "ours_frac": frac(k, ours) if ours else None}
+        if k in alone:
+            out[k]["ours_alone_us"] = round(alone[k]["us_per_launch"], 2)
+            out[k]["ours_alone_frac"] = frac(k, alone[k]["us_per_launch"])
+    return {"passes": out, "note": "hipBLASLt (torch.matmul) on the same GEMM shapes: routed passes as "
+            "one GEMM per local expert with the block's row counts, shared passes dense; plain GEMMs "
+            "without the library's gather, scatter and SwiGLU epilogue; fractions of the 2.5 PFLOP/s "
+            "bf16 peak; ours_us inside the block step, ours_alone_us the library's shared FFN "
+            "(fs_grouped_expert_ffn, one group) run alone"}
 
 
 def bench_block(args, cfg, torch, L, with_cpu):
@@ -742,6 +829,8 @@ def bench_block(args, cfg, torch, L, with_cpu):
     if fp8_routed:
         res["grouped_gemm_frac_bf16_peak"] = None
         res["grouped_gemm_frac_fp8_peak"] = None if roof is None else roof["mfma_frac"]
+    if getattr(args, "vendor_reference", False) and cfg.dtype == "bf16" and not fp8_routed:
+        res["vendor_reference"] = vendor_reference(cfg, blk, wl, kernels, torch)
     if with_cpu and not fp8_routed:
         try:
             res["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_sample)
