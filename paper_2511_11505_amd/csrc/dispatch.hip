@@ -55,49 +55,82 @@ __global__ __launch_bounds__(64) void plan_hist_kernel(const int32_t* __restrict
   }
 }
 
-// One workgroup of 512 threads; thread e owns expert e (E <= 512).  Writes,
-// per tile, the number of earlier tiles' slots on each expert
+// One workgroup of 512 threads (E <= 512).  Expert e gets P = 512 / EP
+// threads (EP: E rounded up to a power of two), each summing one contiguous
+// chunk of the tiles' counts, so a few experts still spread their tiles over
+// the whole workgroup; the chunk sums are scanned per expert in LDS.
+// Writes, per tile, the number of earlier tiles' slots on each expert
 // (tile_base[tile][e]), the counts, the exclusive offsets and rank offsets.
-// Tile counts are read 16 at a time so the loads overlap.
+// All sums are integer, so any grouping gives the same values.
 __global__ __launch_bounds__(512) void plan_scan_kernel(const int32_t* __restrict__ hist,
                                                         int n_tiles, int E, int R,
                                                         int32_t* __restrict__ tile_base,
                                                         int32_t* __restrict__ counts,
                                                         int32_t* __restrict__ offsets,
                                                         int32_t* __restrict__ rank_offsets) {
+  __shared__ int32_t part[512];
   __shared__ int32_t sc[512];
-  const int e = threadIdx.x;
-  int run = 0;
+  const int tid = threadIdx.x;
+  int EP = 1;
+  while (EP < E) EP <<= 1;
+  const int P = 512 / EP;
+  const int e = tid % EP, c = tid / EP;
+  const int tpc = (n_tiles + P - 1) / P;
+  const int ta = min(n_tiles, c * tpc), tb = min(n_tiles, ta + tpc);
+  // 1. this chunk's sum (loads sixteen at a time so they overlap)
+  int sum = 0;
   if (e < E) {
-    for (int t0 = 0; t0 < n_tiles; t0 += 16) {
+    for (int t0 = ta; t0 < tb; t0 += 16) {
       int h[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) h[i] = (t0 + i < n_tiles) ? hist[(size_t)(t0 + i) * E + e] : 0;
+      for (int i = 0; i < 16; ++i) h[i] = (t0 + i < tb) ? hist[(size_t)(t0 + i) * E + e] : 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sum += h[i];
+    }
+  }
+  part[tid] = sum;
+  __syncthreads();
+  // 2. inclusive scan of the chunk sums of each expert (stride EP in part)
+  for (int o = 1; o < P; o <<= 1) {
+    const int v = (c >= o) ? part[tid - o * EP] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  // 3. the per-tile bases of this chunk (its counts again, now from L2)
+  if (e < E) {
+    int run = part[tid] - sum;
+    for (int t0 = ta; t0 < tb; t0 += 16) {
+      int h[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) h[i] = (t0 + i < tb) ? hist[(size_t)(t0 + i) * E + e] : 0;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        if (t0 + i < n_tiles) tile_base[(size_t)(t0 + i) * E + e] = run;
+        if (t0 + i < tb) tile_base[(size_t)(t0 + i) * E + e] = run;
         run += h[i];
       }
     }
   }
-  sc[e] = (e < E) ? run : 0;
+  // 4. expert totals (the last chunk's inclusive sums) and their scan
+  const int run = (tid < E) ? part[(P - 1) * EP + tid] : 0;
+  sc[tid] = run;
   __syncthreads();
   for (int o = 1; o < 512; o <<= 1) {
-    const int v = (e >= o) ? sc[e - o] : 0;
+    const int v = (tid >= o) ? sc[tid - o] : 0;
     __syncthreads();
-    sc[e] += v;
+    sc[tid] += v;
     __syncthreads();
   }
-  const int incl = sc[e];
-  if (e < E) {
-    counts[e] = run;
-    offsets[e] = incl - run;
+  const int incl = sc[tid];
+  if (tid < E) {
+    counts[tid] = run;
+    offsets[tid] = incl - run;
   }
-  if (e == E - 1) offsets[E] = incl;
+  if (tid == E - 1) offsets[E] = incl;
   // rank_offsets[r] = offsets[r * E / R]
-  if (e <= R) {
-    const int ge = e * (E / R);
-    rank_offsets[e] = (ge == 0) ? 0 : sc[ge - 1];
+  if (tid <= R) {
+    const int ge = tid * (E / R);
+    rank_offsets[tid] = (ge == 0) ? 0 : sc[ge - 1];
   }
 }
 

@@ -190,7 +190,9 @@ __global__ __launch_bounds__(256) void router_logits_kernel(const T* __restrict_
 // 16-byte chunk c of row r at position c ^ ((r / 2) % 8), so the 32 or 64
 // rows one read touches fall in different banks) by coalesced loads one
 // chunk ahead in registers, double-buffered with one barrier per chunk; a
-// lane then reads its eight k of a step as one 16-byte LDS read.
+// lane then reads its eight k of a step as one 16-byte LDS read.  (One
+// buffer and two barriers per chunk measured no faster: registers, not
+// LDS, bound its residency.)
 typedef float floatx32 __attribute__((ext_vector_type(32)));
 
 template <int WT, int WE, bool SPLIT>
@@ -301,12 +303,133 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(const bf16_t* __restri
   if constexpr (!SPLIT) store_out(out, tot);
 }
 
-// The matrix-core kernel serves bf16 routers with more than 16 experts and
-// more tokens than the decode-sized tiles of the vector kernel take (hidden
-// sizes are multiples of 128, so slices hold whole 64-element chunks).  At
-// 64 tokens its 32-token tiles give too few workgroups (DeepSeek-V3-shaped
-// decode: 19 us against 13 us on the vector kernel's 16-token tiles).
-bool use_mfma_router(int dtype, int N, int E) { return dtype == 1 && E > 16 && N > kRouterSmallN; }
+// Routers of at most 16 experts on v_mfma_f32_16x16x1_4b_f32: four
+// 16 x 16 blocks, each adding one product per output (d = c + a * b), so a
+// chain over ascending k is the same sequence of rounded adds as above (bit
+// for bit, checked on the device).  Lane layout: for block b, lanes
+// [16b, 16b+16) give the rows (A) and the columns (B); accumulator element
+// v of lane l is block v / 4, row 4 (l / 16) + v % 4, column l % 16.  A lane
+// l holds token l of its wave's 64 (block b: tokens 16b .. 16b+15) and B
+// lane l expert l % 16 (the same 16 experts in every block), so one
+// instruction covers 64 tokens x 16 experts with no padding column.  A
+// workgroup of four waves computes 256 tokens; swizzle and slice order are
+// those of router_mfma_kernel, with one LDS staging buffer (the next chunk
+// waits in registers), so that four workgroups fit a CU.
+template <bool SPLIT>
+__global__ __launch_bounds__(256) void router_mfma16_kernel(const bf16_t* __restrict__ x,
+                                                            const bf16_t* __restrict__ w, int N,
+                                                            int d, int E, float* __restrict__ out) {
+  constexpr int BT = 256, BE = 16, ROWS = BT + BE;
+  constexpr int PIECES = ROWS * 8;                     // 16-byte pieces per chunk
+  constexpr int LPT = (PIECES + 255) / 256;            // loads per thread (the last partial)
+  __shared__ __align__(16) unsigned char sm[ROWS * 128];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * BT;
+  const int S = (d + kRouterSlice - 1) / kRouterSlice;
+  const int s_begin = SPLIT ? (int)blockIdx.z : 0;
+  const int s_end = SPLIT ? s_begin + 1 : S;
+  const int k_begin = s_begin * kRouterSlice;
+  const int k_end = min(d, s_end * kRouterSlice);
+  const int nch = (k_end - k_begin) / 64;            // d % 128 == 0: whole chunks
+
+  // staged loads: piece q = tid + 256 i is row q / 8, 16-byte piece q % 8;
+  // token rows past N and expert rows past E read the last valid row
+  const bf16_t* src[LPT];
+  int dst[LPT];
+  bool live[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int q = tid + 256 * i, row = min(q / 8, ROWS - 1), pc = q % 8;
+    live[i] = q < PIECES;
+    const bf16_t* base = row < BT ? x + (size_t)min(t0 + row, N - 1) * d
+                                  : w + (size_t)min(row - BT, E - 1) * d;
+    src[i] = base + k_begin + pc * 8;
+    dst[i] = row * 128 + ((pc ^ ((row >> 1) & 7)) << 4);
+  }
+  uint4 stg[LPT];
+  auto gload = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i)
+      if (live[i]) stg[i] = ld16(src[i] + 64 * c);
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i)
+      if (live[i]) st16(sm + dst[i], stg[i]);
+  };
+  const int ra = wave * 64 + lane, rb = BT + (lane & 15);
+  const int offa = ra * 128, swa = (ra >> 1) & 7, offb = rb * 128, swb = (rb >> 1) & 7;
+
+  floatx16 part, tot;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) part[v] = tot[v] = 0.f;
+  auto store_out = [&](float* o, const floatx16& val) {
+    const int e = lane & 15;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int t = t0 + wave * 64 + 16 * (v >> 2) + 4 * (lane >> 4) + (v & 3);
+      if (t < N && e < E) o[(size_t)t * E + e] = val[v];
+    }
+  };
+
+  if (nch > 0) {
+    gload(0);
+    lstore();
+  }
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) gload(c + 1);
+    const unsigned char* sb = sm;
+    uint4 ua = *reinterpret_cast<const uint4*>(sb + offa + (swa << 4));
+    uint4 ub = *reinterpret_cast<const uint4*>(sb + offb + (swb << 4));
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      uint4 na = ua, nb = ub;
+      if (ks < 7) {
+        na = *reinterpret_cast<const uint4*>(sb + offa + (((ks + 1) ^ swa) << 4));
+        nb = *reinterpret_cast<const uint4*>(sb + offb + (((ks + 1) ^ swb) << 4));
+      }
+      const uint32_t av[4] = {ua.x, ua.y, ua.z, ua.w}, bv[4] = {ub.x, ub.y, ub.z, ub.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        part = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(av[h] << 16),
+                                                    __uint_as_float(bv[h] << 16), part, 0, 0, 0);
+        part = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(av[h] & 0xFFFF0000u),
+                                                    __uint_as_float(bv[h] & 0xFFFF0000u), part,
+                                                    0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      ua = na;
+      ub = nb;
+    }
+    // end of a slice: fold its sum in (or emit it)
+    const int kn = k_begin + 64 * (c + 1);
+    if (kn % kRouterSlice == 0 || kn == k_end) {
+      if constexpr (SPLIT) {
+        store_out(out + (size_t)((kn - 1) / kRouterSlice) * N * E, part);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) tot[v] = tot[v] + part[v];
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) part[v] = 0.f;
+    }
+    // one staging buffer (34 KB, for more resident workgroups): every wave
+    // has read it before the next chunk overwrites it
+    __syncthreads();
+    if (c + 1 < nch) lstore();
+    __syncthreads();
+  }
+  if constexpr (!SPLIT) store_out(out, tot);
+}
+
+// The matrix-core kernels serve bf16 routers with more tokens than the
+// decode-sized tiles of the vector kernel take (hidden sizes are multiples
+// of 128, so slices hold whole 64-element chunks): router_mfma16_kernel up
+// to 16 experts, router_mfma_kernel above.  At 64 tokens the 32-token tiles
+// give too few workgroups (DeepSeek-V3-shaped decode: 19 us against 13 us on
+// the vector kernel's 16-token tiles).
+bool use_mfma_router(int dtype, int N, int E) { return dtype == 1 && N > kRouterSmallN; }
 
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + expf(-z)); }
 
@@ -496,9 +619,11 @@ int router_slices(int d) { return (d + kRouterSlice - 1) / kRouterSlice; }
 
 // Split the hidden dimension over workgroups (one 256-slice each, summed in
 // order by top-k) when the output tiles alone would not fill the chip: 512
-// tiles for the vector kernel, 4096 waves of 32 x 64 for the matrix-core one.
+// tiles for the vector kernel and the 16-expert matrix-core one, 4096 waves
+// of 32 x 64 for the wider matrix-core one.
 bool router_split(int dtype, int N, int d, int E) {
   if (router_slices(d) <= 1) return false;
+  if (use_mfma_router(dtype, N, E) && E <= 16) return cdiv64(N, 256) < 512;
   if (use_mfma_router(dtype, N, E)) return cdiv64(N, 32) * cdiv64(E, 64) < 4096;
   const int64_t BT = E <= 16 ? 256 : (N <= kRouterSmallN ? 16 : 64), BE = E <= 16 ? 16 : 64;
   const int64_t tiles = cdiv64(N, BT) * cdiv64(E, BE);
@@ -515,6 +640,16 @@ hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, 
                                 bool split, float* out, hipStream_t s) {
   if (dtype == 0)
     return launch_logits_t<float>((const float*)x, (const float*)w, N, d, E, split, out, s);
+  if (use_mfma_router(dtype, N, E) && E <= 16) {
+    const dim3 g((N + 255) / 256, 1, split ? router_slices(d) : 1);
+    if (split)
+      launch_k(router_mfma16_kernel<true>, g, 256, 0, s, (const bf16_t*)x, (const bf16_t*)w, N, d,
+               E, out);
+    else
+      launch_k(router_mfma16_kernel<false>, g, 256, 0, s, (const bf16_t*)x, (const bf16_t*)w, N, d,
+               E, out);
+    return hipGetLastError();
+  }
   if (use_mfma_router(dtype, N, E)) {
     // workgroup tile: 64 tokens x 128 experts, or 128 x 64 (measured on
     // 4096 tokens over 256 experts: 64 x 128 192 us, 32 x 256 198 us)

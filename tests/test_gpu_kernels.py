@@ -68,7 +68,7 @@ def check_ids(cfg, ids_gpu, ids_ref, near):
 # router-only cases: 37 tokens over five slices of the hidden dimension;
 # 160 experts (a ragged last 64-expert range) over 300 tokens (a ragged last
 # 32-token tile); 8190 tokens over 512 experts, enough output tiles to run
-# without splitting the hidden dimension, two slices of it (one ragged)
+# without splitting the hidden dimension, two slices of it (one ragged);
 ROUTER_EXTRA = {
     "dsv3_decode_m": CONFIGS["dsv3_decode"].scaled(n_tokens=37, hidden=1280, ffn=192,
                                                    ffn_shared=192, name="dsv3_decode_m"),
@@ -77,6 +77,17 @@ ROUTER_EXTRA = {
     "wide_unsplit": CONFIGS["dsv3_prefill"].scaled(n_tokens=8190, hidden=384, n_experts=512,
                                                    ep_size=1, ffn=256, ffn_shared=128,
                                                    name="wide_unsplit"),
+    # the 16-expert matrix-core kernel: one slice (no split; 700 tokens, a
+    # ragged third 256-token tile); 6 experts (padded expert rows) over 4.5
+    # slices (the last one 128 wide), one slice per workgroup
+    "e16_unsplit": CONFIGS["scout"].scaled(n_tokens=700, hidden=256, ffn=256, ffn_shared=256,
+                                           name="e16_unsplit"),
+    "e6_split": CONFIGS["dsv2lite"].scaled(n_tokens=1100, hidden=1152, n_experts=6, top_k=2,
+                                           ffn=256, ffn_shared=128, name="e6_split"),
+    # enough tiles x slices for two slices per workgroup: 9 tiles x 58
+    # slices (the last 128 wide), workgroup 28 taking slices 56 and 57
+    "e16_two_slices": CONFIGS["scout"].scaled(n_tokens=2148, hidden=14720, ffn=256,
+                                              ffn_shared=256, name="e16_two_slices"),
 }
 
 
