@@ -1114,9 +1114,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
 
   const int nn = NOUT / NCOL;
   const int64_t total = (int64_t)nn * s_tpre[G];
+  // as many workgroups as give every one the same number of tiles (within
+  // one per XCD range): the tile count is known only here, and a part-full
+  // last round streams no faster than a full one
+  const int64_t rounds = (total + gridDim.x - 1) / gridDim.x;
+  int64_t eff = rounds > 0 ? (total + rounds - 1) / rounds : (int64_t)gridDim.x;
+  eff = (eff + kXcd - 1) / kXcd * kXcd;
+  if (eff > (int64_t)gridDim.x) eff = gridDim.x;
+  if ((int64_t)blockIdx.x >= eff) return;   // a whole workgroup, before any barrier below
   const int64_t per_xcd = (total + kXcd - 1) / kXcd;
   const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
-  const int64_t stride = gridDim.x / kXcd;
+  const int64_t stride = eff / kXcd;
   const int KT = K / 64;
   const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
   const int drow = lane / 8, dpos = lane % 8;
