@@ -634,7 +634,7 @@ def bench_block(args, cfg, torch, L, with_cpu):
         sh_gu, sh_dn = merge_shared(wl.sh_gate_up, wl.sh_down)
     # decode-sized routed passes (a few rows per local expert) stream the
     # experts' weights in fragment order
-    fo = args.fp8 is None and cfg.dtype == "bf16" and cfg.cap <= 64 * cfg.n_local
+    fo = cfg.dtype == "bf16" and cfg.cap <= 64 * cfg.n_local
     blk = fs.MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn, device=dev,
                       fp8=args.fp8, fragment_order=fo)
     M = cfg.cap

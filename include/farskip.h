@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FS_ABI_VERSION 8
+#define FS_ABI_VERSION 9
 
 typedef enum {
   FS_OK = 0,
@@ -309,6 +309,37 @@ fs_status fs_grouped_expert_ffn_fo(const fs_moe_desc* desc, int32_t n_groups, in
                                    const void* w_gate_up_fo, const void* w_down_fo,
                                    void* out_rows, void* ws, size_t ws_bytes, fs_stream stream);
 
+/* FP8 fragment order: n_mats row-major E4M3 code matrices [rows, cols]
+ * (rows % 32 == 0, cols % 64 == 0; fs_quantize_fp8 codes) rewritten as
+ * [rows/32][cols/64] fragments of 2 KB, each two 1 KB halves: in fragment
+ * (g, c), half h, the 16 bytes at lane l (0..63) are row 32 g + l % 32,
+ * columns 64 c + 32 (l / 32) + 16 h .. + 15 (lane l's 32 bytes are the B
+ * operand of a 32 x 32 x 64 FP8 matrix instruction).  Same purpose as
+ * fs_expert_weights_fragment_order: weight streaming in decode (Section
+ * 5.2), here for the FP8 experts the paper's inference runs use.
+ *   src, dst   n_mats * rows * cols bytes each, device, 16-byte aligned,
+ *              not overlapping
+ * FS_ERR_UNSUPPORTED for other shapes. */
+fs_status fs_expert_weights_fragment_order_fp8(int64_t n_mats, int32_t rows, int32_t cols,
+                                               const uint8_t* src, uint8_t* dst,
+                                               fs_stream stream);
+
+/* fs_grouped_expert_ffn_fp8 with FP8-fragment-ordered weight codes
+ * (fs_expert_weights_fragment_order_fp8 of w_gate_up as n_groups matrices
+ * [2F, d] and of w_down as n_groups matrices [d, F]; the row scales are
+ * unchanged): the same operands, groups, outputs and workspace
+ * (FS_OP_GROUPED_FFN_FP8), ffn % 128 == 0 and d % 256 == 0.  The MFMAs see
+ * the operands of fs_grouped_expert_ffn_fp8's kernel, so a pass that kernel
+ * runs without splitting K gives the same bits.  Meant for groups of few
+ * rows (decode). */
+fs_status fs_grouped_expert_ffn_fp8_fo(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                       const uint8_t* x_codes, const float* x_scales,
+                                       const int32_t* group_rows, const int32_t* group_offsets,
+                                       int64_t max_rows, const uint8_t* w_gate_up_fo,
+                                       const float* s_gate_up, const uint8_t* w_down_fo,
+                                       const float* s_down, void* out_rows, void* ws,
+                                       size_t ws_bytes, fs_stream stream);
+
 /* The grouped SwiGLU FFN of fs_grouped_expert_ffn with the input gathered
  * and the output in grouped order: row i of the grouped order reads
  * x[gather_rows[i]] and writes y[i].  Used with replicated activations,
@@ -467,6 +498,13 @@ typedef struct {
    * kernels; other passes read w_gate_up / w_down, which stay required. */
   const void* w_gate_up_fo;      /* [E/R, 2F, d] in fragment order */
   const void* w_down_fo;         /* [E/R, d, F] in fragment order */
+  /* FP8-fragment-ordered copies of w_gate_up_fp8 and w_down_fp8
+   * (fs_expert_weights_fragment_order_fp8), or NULL: with FP8 routed
+   * experts, passes whose groups average at most 64 rows stream them with
+   * fs_grouped_expert_ffn_fp8_fo's kernels; the FP8 fields above stay
+   * required. */
+  const uint8_t* w_gate_up_fp8_fo; /* [E/R, 2F, d] codes in FP8 fragment order */
+  const uint8_t* w_down_fp8_fo;    /* [E/R, d, F] */
 } fs_moe_weights;
 
 /* Caller-owned buffers of one block (device memory). */

@@ -16,8 +16,10 @@ from ._lib import (  # noqa: F401
     fs_dispatch_pack, fs_dispatch_pack_fp8, fs_receive_rows, fs_grouped_expert_ffn, fs_combine_unpack,
     fs_local_rows, fs_grouped_expert_ffn_gathered, fs_combine_partial, fs_allreduce_standin,
     fs_quantize_fp8, fs_grouped_expert_ffn_fp8, fs_expert_weights_fragment_order,
-    fs_grouped_expert_ffn_fo, fs_standin_link, fs_standin_link_get, standin_link,
+    fs_grouped_expert_ffn_fo, fs_grouped_expert_ffn_fp8_fo, fs_expert_weights_fragment_order_fp8,
+    fs_standin_link, fs_standin_link_get, standin_link,
     fs_farskip_residual, fs_dense_linear, fs_block_sync_create, fs_block_sync_destroy,
     fs_moe_block_forward, fs_profile_enable, fs_profile_select, fs_profile_read, fs_profile_reset,
 )
-from .block import MoEBlock, fp8_row_views, fragment_ordered, prepare_remote_sources  # noqa: F401
+from .block import (MoEBlock, fp8_row_views, fragment_ordered, fragment_ordered_fp8,  # noqa: F401
+                    prepare_remote_sources)

@@ -22,7 +22,7 @@ FS_SOFTMAX, FS_SIGMOID = 0, 1
 (FS_K_ROUTER, FS_K_TOPK, FS_K_PLAN, FS_K_PACK, FS_K_GATE_UP, FS_K_DOWN,
  FS_K_COMBINE, FS_K_SHARED_GATE_UP, FS_K_SHARED_DOWN, FS_K_DISPATCH_COPY, FS_K_DENSE,
  FS_K_COMBINE_COPY, FS_K_ALLREDUCE_COPY, FS_K_QUANTIZE, FS_K_COUNT) = range(15)
-FS_ABI_VERSION = 8
+FS_ABI_VERSION = 9
 
 _i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
 
@@ -46,7 +46,8 @@ class fs_moe_weights(ctypes.Structure):
                 ("ws_gate_up", _vp), ("ws_down", _vp),
                 ("w_gate_up_fp8", _vp), ("s_gate_up", _vp), ("w_down_fp8", _vp), ("s_down", _vp),
                 ("ws_gate_up_fp8", _vp), ("ss_gate_up", _vp), ("ws_down_fp8", _vp),
-                ("ss_down", _vp), ("w_gate_up_fo", _vp), ("w_down_fo", _vp)]
+                ("ss_down", _vp), ("w_gate_up_fo", _vp), ("w_down_fo", _vp),
+                ("w_gate_up_fp8_fo", _vp), ("w_down_fp8_fo", _vp)]
 
 
 class fs_block_buffers(ctypes.Structure):
@@ -79,6 +80,9 @@ _SIGS = {
     "fs_quantize_fp8": (_i32, [_i32, _i64, _i32, _vp, _vp, _vp, _vp]),
     "fs_grouped_expert_ffn_fp8": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp, _vp,
                                          _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "fs_grouped_expert_ffn_fp8_fo": (_i32, [ctypes.POINTER(fs_moe_desc), _i32, _i32, _vp, _vp, _vp,
+                                            _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "fs_expert_weights_fragment_order_fp8": (_i32, [_i64, _i32, _i32, _vp, _vp, _vp]),
     "fs_combine_partial": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp, _vp, _vp, _vp]),
     "fs_allreduce_standin": (_i32, [ctypes.POINTER(fs_moe_desc), _vp, _vp, _vp]),
     "fs_standin_link": (_i32, [_i32, ctypes.c_double, _i32]),
@@ -274,6 +278,22 @@ def fs_grouped_expert_ffn_fp8(desc, n_groups, ffn, x_codes, x_scales, group_rows
                                             max_rows, ptr(w_gate_up), ptr(s_gate_up), ptr(w_down),
                                             ptr(s_down), ptr(out_rows), wp, wb,
                                             stream_handle(stream)))
+
+
+def fs_grouped_expert_ffn_fp8_fo(desc, n_groups, ffn, x_codes, x_scales, group_rows, group_offsets,
+                                 max_rows, w_gate_up_fo, s_gate_up, w_down_fo, s_down, out_rows, ws,
+                                 stream=None):
+    wp, wb = _ws(ws)
+    _check(load().fs_grouped_expert_ffn_fp8_fo(ctypes.byref(desc), n_groups, ffn, ptr(x_codes),
+                                               ptr(x_scales), ptr(group_rows), ptr(group_offsets),
+                                               max_rows, ptr(w_gate_up_fo), ptr(s_gate_up),
+                                               ptr(w_down_fo), ptr(s_down), ptr(out_rows), wp, wb,
+                                               stream_handle(stream)))
+
+
+def fs_expert_weights_fragment_order_fp8(n_mats, rows, cols, src, dst, stream=None):
+    _check(load().fs_expert_weights_fragment_order_fp8(n_mats, rows, cols, ptr(src), ptr(dst),
+                                                       stream_handle(stream)))
 
 
 def fs_combine_partial(desc, y_local, slot_to_row, rank_offsets, topk_w, partial_out, stream=None):

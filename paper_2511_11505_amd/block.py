@@ -42,6 +42,16 @@ def fragment_ordered(w):
     return out
 
 
+def fragment_ordered_fp8(codes):
+    """FP8 fragment-order copy of E4M3 code matrices [..., rows, cols]
+    (fs_expert_weights_fragment_order_fp8)."""
+    rows, cols = codes.shape[-2], codes.shape[-1]
+    out = torch.empty_like(codes)
+    L.fs_expert_weights_fragment_order_fp8(codes.numel() // (rows * cols), rows, cols,
+                                           codes.contiguous(), out)
+    return out
+
+
 def fp8_row_views(buf, rows, d):
     """Views of an FP8 row buffer of `rows` rows held in the device tensor
     buf (any dtype, contiguous): codes [rows, d] uint8 at byte 0, scales
@@ -59,9 +69,9 @@ class MoEBlock:
                  fragment_order=False):
         """fp8: None (bf16 experts), "routed" (FP8 routed experts) or "all"
         (FP8 routed and shared experts).  fragment_order: also keep the
-        routed experts' weights in MFMA fragment order (converted once, by
-        the library), which the block streams for passes of few rows per
-        expert (decode)."""
+        routed experts' weights (and with fp8 their codes) in MFMA fragment
+        order (converted once, by the library), which the block streams for
+        passes of few rows per expert (decode)."""
         if fp8 not in (None, "routed", "all"):
             raise ValueError(f"fp8 must be None, 'routed' or 'all', not {fp8!r}")
         self.cfg = cfg
@@ -98,7 +108,10 @@ class MoEBlock:
             if fp8 == "all" and ws_gate_up is not None:
                 q["ws_gate_up_fp8"], q["ss_gate_up"] = _quantize(ws_gate_up)
                 q["ws_down_fp8"], q["ss_down"] = _quantize(ws_down)
-        if fragment_order:
+        if fragment_order and fp8:
+            q["w_gate_up_fp8_fo"] = fragment_ordered_fp8(q["w_gate_up_fp8"])
+            q["w_down_fp8_fo"] = fragment_ordered_fp8(q["w_down_fp8"])
+        elif fragment_order:
             q["w_gate_up_fo"] = fragment_ordered(w_gate_up)
             q["w_down_fo"] = fragment_ordered(w_down)
         self.fp8_weights = q

@@ -675,6 +675,56 @@ static bool fo_shape_ok(const fs_moe_desc* d, int32_t ffn) {
   return d->dtype == FS_BF16 && ffn % 128 == 0 && d->hidden % 256 == 0;
 }
 
+fs_status fs_expert_weights_fragment_order_fp8(int64_t n_mats, int32_t rows, int32_t cols,
+                                               const uint8_t* src, uint8_t* dst,
+                                               fs_stream stream) {
+  if (n_mats < 0 || rows <= 0 || cols <= 0) return fail(FS_ERR_INVALID, "bad matrix shape");
+  if (rows % 32 != 0 || cols % 64 != 0)
+    return fail(FS_ERR_UNSUPPORTED, "FP8 fragment order needs rows % 32 == 0 and cols % 64 == 0");
+  if (n_mats == 0) return FS_OK;
+  NEED(src, "src");
+  NEED(dst, "dst");
+  const size_t bytes = (size_t)n_mats * rows * cols;
+  const char *a = reinterpret_cast<const char*>(src), *b = reinterpret_cast<const char*>(dst);
+  if (a < b + bytes && b < a + bytes) return fail(FS_ERR_INVALID, "src and dst overlap");
+  FS_HIP(fs::launch_fragment_order_fp8(src, n_mats, rows, cols, dst, S(stream)),
+         "fragment_order_fp8");
+  return FS_OK;
+}
+
+fs_status fs_grouped_expert_ffn_fp8_fo(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
+                                       const uint8_t* x_codes, const float* x_scales,
+                                       const int32_t* group_rows, const int32_t* group_offsets,
+                                       int64_t max_rows, const uint8_t* w_gate_up_fo,
+                                       const float* s_gate_up, const uint8_t* w_down_fo,
+                                       const float* s_down, void* out_rows, void* ws,
+                                       size_t ws_bytes, fs_stream stream) {
+  fs_status st = ffn_checks(desc, n_groups, ffn, group_offsets, max_rows);
+  if (st != FS_OK) return st;
+  if (!fo_shape_ok(desc, ffn))
+    return fail(FS_ERR_UNSUPPORTED, "FP8 fragment-ordered experts write bf16 rows and need "
+                                    "ffn % 128 == 0 and hidden % 256 == 0");
+  if (max_rows == 0) return FS_OK;
+  NEED(x_codes, "x_codes");
+  NEED4(x_scales, "x_scales");
+  OPT4(group_rows, "group_rows");
+  OPT4(group_offsets, "group_offsets");
+  NEED(w_gate_up_fo, "w_gate_up_fo");
+  NEED4(s_gate_up, "s_gate_up");
+  NEED(w_down_fo, "w_down_fo");
+  NEED4(s_down, "s_down");
+  NEED(out_rows, "out_rows");
+  if (ws_bytes < fs::ffn_fp8_ws_bytes(max_rows, ffn, desc->hidden))
+    return fail(FS_ERR_WORKSPACE, "workspace smaller than fs_workspace_size(FS_OP_GROUPED_FFN_FP8)");
+  NEED(ws, "ws");
+  FS_HIP(fs::launch_grouped_ffn_fo_fp8(n_groups, ffn, desc->hidden, x_codes, x_scales, group_rows,
+                                       group_rows, group_offsets, max_rows, w_gate_up_fo,
+                                       s_gate_up, w_down_fo, s_down, out_rows, ws, S(stream),
+                                       group_offsets ? FS_K_GATE_UP : FS_K_SHARED_GATE_UP),
+         "grouped_ffn_fp8_fo");
+  return FS_OK;
+}
+
 fs_status fs_grouped_expert_ffn_fo(const fs_moe_desc* desc, int32_t n_groups, int32_t ffn,
                                    const void* in_rows, const int32_t* group_rows,
                                    const int32_t* group_offsets, int64_t max_rows,
@@ -932,9 +982,13 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       NEED4(wt->s_gate_up, "weights->s_gate_up");
       NEED(wt->w_down_fp8, "weights->w_down_fp8");
       NEED4(wt->s_down, "weights->s_down");
+      OPT(wt->w_gate_up_fp8_fo, "weights->w_gate_up_fp8_fo");
+      OPT(wt->w_down_fp8_fo, "weights->w_down_fp8_fo");
     } else {
       NEED(wt->w_gate_up, "weights->w_gate_up");
       NEED(wt->w_down, "weights->w_down");
+      OPT(wt->w_gate_up_fo, "weights->w_gate_up_fo");
+      OPT(wt->w_down_fo, "weights->w_down_fo");
     }
     NEED(b->y, "buffers->y");
     if (R > 1) {
@@ -1080,10 +1134,21 @@ fs_status fs_moe_block_forward(const fs_moe_desc* desc, int32_t phase,
       // the outputs go back to their receive rows
       const uint8_t* xq = b->recv ? recv_codes : send_codes;
       const float* xs = b->recv ? recv_scales : send_scales;
-      FS_HIP(fs::launch_grouped_ffn_fp8(E_loc, desc->ffn, D, xq, xs, rows, rows, goff,
-                                        max_recv_rows, wt->w_gate_up_fp8, wt->s_gate_up,
-                                        wt->w_down_fp8, wt->s_down, b->y, ws_ffn, sc, FS_K_GATE_UP),
-             "grouped_ffn_fp8");
+      if (wt->w_gate_up_fp8_fo && wt->w_down_fp8_fo && fo_shape_ok(desc, desc->ffn) &&
+          max_recv_rows <= (int64_t)64 * E_loc) {
+        // groups of few rows (decode): stream the FP8-fragment-ordered codes
+        FS_HIP(fs::launch_grouped_ffn_fo_fp8(E_loc, desc->ffn, D, xq, xs, rows, rows, goff,
+                                             max_recv_rows, wt->w_gate_up_fp8_fo, wt->s_gate_up,
+                                             wt->w_down_fp8_fo, wt->s_down, b->y, ws_ffn, sc,
+                                             FS_K_GATE_UP),
+               "grouped_ffn_fp8_fo");
+      } else {
+        FS_HIP(fs::launch_grouped_ffn_fp8(E_loc, desc->ffn, D, xq, xs, rows, rows, goff,
+                                          max_recv_rows, wt->w_gate_up_fp8, wt->s_gate_up,
+                                          wt->w_down_fp8, wt->s_down, b->y, ws_ffn, sc,
+                                          FS_K_GATE_UP),
+               "grouped_ffn_fp8");
+      }
     } else if (wt->w_gate_up_fo && wt->w_down_fo && fo_shape_ok(desc, desc->ffn) &&
                max_recv_rows <= (int64_t)64 * E_loc) {
       // groups of few rows (decode): stream the fragment-ordered weights

@@ -1089,21 +1089,42 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_rs_kernel(
 // The persistent grid walks (group, n-tile, m-tile; m fastest) in eight
 // contiguous XCD ranges, as the LDS-ring kernels do: m-tiles of one weight
 // panel run together under one L2.
+//
+// F8: E4M3 codes on v_mfma_scale_f32_32x32x64_f8f6f4 (unit block scales).
+// A fragment is 32 rows x 64 k (2 KB), lane l's 32 bytes being row l % 32,
+// k 32 (l / 32) .. + 31 of the step (the lane split of the LDS-ring FP8
+// kernel, so the MFMAs see the same operands); stored as two 1 KB halves,
+// half h holding bytes 16 h .. 16 h + 15 of every lane's 32, so each load
+// still reads 1 KB contiguously.  A block is 128 k (a staged activation row
+// is still 128 bytes) in two steps; a block's weight bytes, loads and MFMA
+// time equal bf16's.  The epilogue applies the row scales of the
+// activations and the column scales of the weights, as the LDS-ring kernel
+// does.
 constexpr int kFoBM = 64;
 
-__device__ __forceinline__ const bf16_t* fo_group(const bf16_t* Wg, int K, int grp) {
-  return Wg + (size_t)grp * (K / 16) * 512;
+// One 32-row weight group: 32 rows x K of 1- or 2-byte elements.
+template <typename TE>
+__device__ __forceinline__ const TE* fo_group(const TE* Wg, int K, int grp) {
+  return Wg + (size_t)grp * 32 * K;
 }
 
-template <int MODE>
+template <int MODE, bool F8 = false>
 __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
-    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ Bfo,
-    int K, int NOUT, bf16_t* __restrict__ C, int ldc) {
-  constexpr int BM = kFoBM, NT = 256, TM = BM / 32, KS = 4, NST = 3;
+    const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
+    const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ Bfo, int K, int NOUT,
+    bf16_t* __restrict__ C, int ldc, const float* __restrict__ sA, const float* __restrict__ sB) {
+  using TE = typename std::conditional<F8, uint8_t, bf16_t>::type;
+  using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
+  constexpr int BM = kFoBM, NT = 256, TM = BM / 32, NST = 3;
+  constexpr int KB = F8 ? 128 : 64;                  // K elements per block (128 bytes)
+  constexpr int KS = F8 ? 2 : 4;                     // MFMA steps per block
+  constexpr int CE = F8 ? 16 : 8;                    // elements per 16 bytes
   constexpr int ROWB = 128, ASTAGE = BM * ROWB;
   constexpr int ALD = BM * ROWB / 1024 / 4;          // 1 KB DMAs per wave per block
-  constexpr int NB = 2 * KS;                         // weight loads per wave per block
+  constexpr int NB = 8;                              // 1 KB weight loads per wave per block
+  constexpr int LPS = F8 ? 4 : 3;                    // weight loads issued per step
+  constexpr int WAITN = ALD + (NB < LPS * (KS - 1) ? NB : LPS * (KS - 1));
   constexpr int NCOL = (MODE == MODE_GATEUP) ? 128 : 256;
   __shared__ int s_goff[kMaxGroups + 1];
   __shared__ int s_tpre[kMaxGroups + 1];
@@ -1125,7 +1146,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
   const int64_t per_xcd = (total + kXcd - 1) / kXcd;
   const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
   const int64_t stride = eff / kXcd;
-  const int KT = K / 64;
+  const int KT = K / KB;
   const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
   const int drow = lane / 8, dpos = lane % 8;
   const unsigned ring_lds = lds_addr(ring);
@@ -1149,10 +1170,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
     const int nt = local / Tg;
     const int m0 = (local - nt * Tg) * BM, n0 = nt * NCOL;
     const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
-    const bf16_t* Bg = Bfo + (size_t)g * bstride;
+    const TE* Bg = Bfo + (size_t)g * bstride;
     // activation rows of this wave's DMAs (rows past the group's end load
     // its last row; their results are not stored)
-    const bf16_t* asrc[ALD];
+    const TE* asrc[ALD];
 #pragma unroll
     for (int i = 0; i < ALD; ++i) {
       const int r = (wave * ALD + i) * 8 + drow;
@@ -1160,19 +1181,19 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
       if (m >= rows_g) m = rows_g - 1;
       const int grow = row_base + m;
       const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      asrc[i] = A + sr * K + ((dpos ^ ((r >> 1) & 7)) * 8);
+      asrc[i] = A + sr * K + ((dpos ^ ((r >> 1) & 7)) * CE);
     }
     // this wave's two 32-row weight groups
-    const bf16_t* bsrc[2];
+    const TE* bsrc[2];
     if (MODE == MODE_GATEUP) {
-      bsrc[0] = fo_group(Bg, K, n0 / 32 + wave) + lane * 8;
-      bsrc[1] = fo_group(Bg, K, (NOUT + n0) / 32 + wave) + lane * 8;
+      bsrc[0] = fo_group(Bg, K, n0 / 32 + wave) + lane * CE;
+      bsrc[1] = fo_group(Bg, K, (NOUT + n0) / 32 + wave) + lane * CE;
     } else {
-      bsrc[0] = fo_group(Bg, K, n0 / 32 + 2 * wave) + lane * 8;
-      bsrc[1] = fo_group(Bg, K, n0 / 32 + 2 * wave + 1) + lane * 8;
+      bsrc[0] = fo_group(Bg, K, n0 / 32 + 2 * wave) + lane * CE;
+      bsrc[1] = fo_group(Bg, K, n0 / 32 + 2 * wave + 1) + lane * CE;
     }
     auto dA = [&](int kt, int i) __attribute__((always_inline)) {
-      dma16_at(asrc[i] + (size_t)kt * 64,
+      dma16_at(asrc[i] + (size_t)kt * KB,
                ring_lds + (unsigned)((kt % NST) * ASTAGE) + (wave_u * ALD + i) * 1024u);
     };
     floatx16 acc[TM][2];
@@ -1182,15 +1203,34 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.f;
-    bf16x8 Bf[3][NB];
-    bf16x8 Fa[2][TM];
+    // weight load q of a block: group q & 1; bf16 step q >> 1; F8 step
+    // q >> 2, half (q >> 1) & 1 (1 KB pieces of the group, in address order)
+    int4 Bf[3][NB];
+    FragT Fa[2][TM];
     auto gB = [&](int slot, int kt, int q) __attribute__((always_inline)) {
-      Bf[slot][q] = *reinterpret_cast<const bf16x8*>(bsrc[q & 1] + ((size_t)kt * KS + (q >> 1)) * 512);
+      const size_t piece = F8 ? ((size_t)kt * KS + (q >> 2)) * 2 + ((q >> 1) & 1)
+                              : (size_t)kt * KS + (q >> 1);
+      Bf[slot][q] = *reinterpret_cast<const int4*>(bsrc[q & 1] + piece * (1024 / sizeof(TE)));
+    };
+    auto bfrag = [&](int slot, int ks, int t) __attribute__((always_inline)) {
+      if constexpr (F8) {
+        const int4 lo = Bf[slot][(ks << 2) | t], hi = Bf[slot][(ks << 2) | 2 | t];
+        return int32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      } else {
+        return __builtin_bit_cast(bf16x8, Bf[slot][2 * ks + t]);
+      }
     };
     auto rA = [&](int buf, int kt, int ks, int i) __attribute__((always_inline)) {
       const unsigned char* sl = ring + (kt % NST) * ASTAGE;
-      const int c = ks * 2 + (lane >> 5);
-      Fa[buf][i] = *reinterpret_cast<const bf16x8*>(sl + aoff[i] + ((c ^ asw[i]) << 4));
+      if constexpr (F8) {
+        const int c = ks * 4 + 2 * (lane >> 5);
+        const int4 lo = *reinterpret_cast<const int4*>(sl + aoff[i] + ((c ^ asw[i]) << 4));
+        const int4 hi = *reinterpret_cast<const int4*>(sl + aoff[i] + (((c + 1) ^ asw[i]) << 4));
+        Fa[buf][i] = int32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      } else {
+        const int c = ks * 2 + (lane >> 5);
+        Fa[buf][i] = *reinterpret_cast<const bf16x8*>(sl + aoff[i] + ((c ^ asw[i]) << 4));
+      }
     };
     // prologue: activation blocks 0 and 1, weight blocks 0 and 1
 #pragma unroll
@@ -1208,9 +1248,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
 #pragma unroll
     for (int i = 0; i < TM; ++i) rA(0, 0, 0, i);
     // block kt: weights from slot kt % 3; issues the DMAs of activation block
-    // kt + 2 (step 0) and the loads of weight block kt + 2 (steps 0..2).  The
-    // last step waits for activation block kt + 1: after its DMAs, only this
-    // block's DMAs and weight loads may still be in flight.
+    // kt + 2 (step 0) and the loads of weight block kt + 2 (LPS per step,
+    // after the step's last MFMAs).  The last step waits for activation
+    // block kt + 1: after its DMAs, only the WAITN loads of block kt + 2
+    // issued before the wait may still be in flight.
     auto block = [&](int kt, auto SLOT, auto N1, auto N2) __attribute__((always_inline)) {
       constexpr int sl = decltype(SLOT)::value;
       constexpr int s2 = (sl + 2) % 3;
@@ -1221,13 +1262,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
 #pragma unroll
         for (int q = 0; q < TM * 2; ++q) {
           const int i = q >> 1, t = q & 1;
-          acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fa[cb][i], Bf[sl][2 * ks + t],
-                                                              acc[i][t], 0, 0, 0);
+          if constexpr (F8)
+            acc[i][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                Fa[cb][i], bfrag(sl, ks, t), acc[i][t], 0, 0, 0, 127, 0, 127);
+          else
+            acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fa[cb][i], bfrag(sl, ks, t),
+                                                                acc[i][t], 0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
           if (ks == KS - 1 && q == 0 && n1) {
             wait_lgkm0();
             if (n2)
-              wait_vmcnt<ALD + NB>();
+              wait_vmcnt<WAITN>();
             else
               wait_vmcnt<0>();
             barrier_nofence();
@@ -1240,10 +1285,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
               rA(cb ^ 1, kt + 1, 0, q);
           }
           if (ks == 0 && n2 && q < ALD) dA(kt + 2, q);
-          if (ks < 3 && n2) {
-            // weight loads 3 ks .. 3 ks + 2 of block kt + 2, after the last MFMAs
-            const int qq = 3 * ks + (q - (TM * 2 - 3));
-            if (q >= TM * 2 - 3 && qq < NB) gB(s2, kt + 2, qq);
+          if (ks * LPS < NB && n2) {
+            // weight loads LPS ks .. LPS ks + LPS - 1 of block kt + 2, after
+            // the step's last MFMAs
+            const int qq = LPS * ks + (q - (TM * 2 - LPS));
+            if (q >= TM * 2 - LPS && qq < NB) gB(s2, kt + 2, qq);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -1267,7 +1313,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
 
     // epilogue: accumulator element v of lane l is row 8 (v / 4) + 4 (l / 32)
     // + v % 4, column l % 32 of its 32 x 32 block; 32 lanes store 64
-    // contiguous bytes of a row
+    // contiguous bytes of a row.  F8: y = acc * row scale * column scale.
+    float sbc[2] = {1.f, 1.f};
+    if constexpr (F8) {
+      const float* sBg = sB + (size_t)g * ((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT);
+      if (MODE == MODE_GATEUP) {
+        sbc[0] = sBg[n0 + 32 * wave + (lane & 31)];
+        sbc[1] = sBg[NOUT + n0 + 32 * wave + (lane & 31)];
+      } else {
+        sbc[0] = sBg[n0 + 64 * wave + (lane & 31)];
+        sbc[1] = sBg[n0 + 64 * wave + 32 + (lane & 31)];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -1275,14 +1332,19 @@ __global__ __launch_bounds__(256) void gemm_bf16_fo_kernel(
         const int m = m0 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
         if (m < rows_g) {
           const int grow = row_base + m;
+          float y0 = acc[i][0][v], y1 = acc[i][1][v];
+          if constexpr (F8) {
+            const float sa =
+                sA[(MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow];
+            y0 = y0 * sa * sbc[0];
+            y1 = y1 * sa * sbc[1];
+          }
           if (MODE == MODE_GATEUP) {
-            C[(int64_t)grow * ldc + n0 + 32 * wave + (lane & 31)] =
-                f2bf(swiglu_bf16_epi(acc[i][0][v], acc[i][1][v]));
+            C[(int64_t)grow * ldc + n0 + 32 * wave + (lane & 31)] = f2bf(swiglu_bf16_epi(y0, y1));
           } else {
             const int64_t orow = rows ? (int64_t)rows[grow] : (int64_t)grow;
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-              C[orow * ldc + n0 + 64 * wave + 32 * t + (lane & 31)] = f2bf(acc[i][t][v]);
+            C[orow * ldc + n0 + 64 * wave + (lane & 31)] = f2bf(y0);
+            C[orow * ldc + n0 + 64 * wave + 32 + (lane & 31)] = f2bf(y1);
           }
         }
       }
@@ -1306,6 +1368,28 @@ __global__ __launch_bounds__(256) void fragment_order_kernel(const bf16_t* __res
   const int64_t ng = chunk / (cols / 16);
   const int64_t row = ng * 32 + lane % 32;
   const int col = ks * 16 + (lane / 32) * 8;
+  reinterpret_cast<uint4*>(dst)[i] =
+      *reinterpret_cast<const uint4*>(src + (mat * rows + row) * cols + col);
+}
+
+// FP8 fragment order of row-major [rows, cols] E4M3 code matrices (rows % 32
+// == 0, cols % 64 == 0): [rows / 32][cols / 64][2][64][16 bytes], half h of
+// lane l holding row l % 32, bytes 32 (l / 32) + 16 h .. + 15 of its 64-byte
+// step.  One thread per 16-byte piece of the destination.
+__global__ __launch_bounds__(256) void fragment_order_fp8_kernel(const uint8_t* __restrict__ src,
+                                                                 int64_t n_mats, int rows,
+                                                                 int cols,
+                                                                 uint8_t* __restrict__ dst) {
+  const int64_t per = (int64_t)rows * cols / 16;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_mats * per) return;
+  const int64_t mat = i / per, r = i % per;
+  const int lane = (int)(r % 64), half = (int)((r / 64) % 2);
+  const int64_t frag = r / 128;
+  const int ks = (int)(frag % (cols / 64));
+  const int64_t ng = frag / (cols / 64);
+  const int64_t row = ng * 32 + lane % 32;
+  const int col = ks * 64 + (lane / 32) * 32 + 16 * half;
   reinterpret_cast<uint4*>(dst)[i] =
       *reinterpret_cast<const uint4*>(src + (mat * rows + row) * cols + col);
 }
@@ -1999,11 +2083,54 @@ hipError_t launch_grouped_ffn_fo(int G, int ffn, int d, const void* in, const in
   };
   if (profile) prof_begin(prof_gate_up, s);
   launch_k(gemm_bf16_fo_kernel<MODE_GATEUP>, grid(128, ffn), 256, 0, s, (const bf16_t*)in,
-           rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up_fo, d, ffn, H, ffn);
+           rows_in, goff, G, max_rows, (const bf16_t*)w_gate_up_fo, d, ffn, H, ffn,
+           (const float*)nullptr, (const float*)nullptr);
   if (profile) prof_end(prof_gate_up, s);
   if (profile) prof_begin(prof_gate_up + 1, s);
   launch_k(gemm_bf16_fo_kernel<MODE_DOWN>, grid(256, d), 256, 0, s, (const bf16_t*)H, rows_out,
-           goff, G, max_rows, (const bf16_t*)w_down_fo, ffn, d, (bf16_t*)out, d);
+           goff, G, max_rows, (const bf16_t*)w_down_fo, ffn, d, (bf16_t*)out, d,
+           (const float*)nullptr, (const float*)nullptr);
+  if (profile) prof_end(prof_gate_up + 1, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fragment_order_fp8(const uint8_t* src, int64_t n_mats, int rows, int cols,
+                                     uint8_t* dst, hipStream_t s) {
+  const int64_t n = n_mats * rows * (int64_t)cols / 16;
+  if (n == 0) return hipSuccess;
+  launch_k(fragment_order_fp8_kernel, (unsigned)cdiv64(n, 256), 256, 0, s, src, n_mats, rows, cols,
+           dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_ffn_fo_fp8(int G, int ffn, int d, const uint8_t* x, const float* x_scale,
+                                     const int32_t* rows_in, const int32_t* rows_out,
+                                     const int32_t* goff, int64_t max_rows,
+                                     const uint8_t* w_gate_up_fo, const float* s_gate_up,
+                                     const uint8_t* w_down_fo, const float* s_down, void* out,
+                                     void* ws, hipStream_t s, int prof_gate_up) {
+  if (max_rows <= 0) return hipSuccess;
+  const bool profile = prof_gate_up >= 0;
+  // the workspace of launch_grouped_ffn_fp8: H, then its codes and scales
+  const size_t h = (size_t)max_rows * ffn;
+  bf16_t* H = reinterpret_cast<bf16_t*>(ws);
+  uint8_t* Hq = reinterpret_cast<uint8_t*>(ws) + (h * 2 + 255) / 256 * 256;
+  float* Hs = reinterpret_cast<float*>(Hq + (h + 255) / 256 * 256);
+  auto grid = [&](int ncol, int nout) {
+    int64_t g = grid_for(max_rows, G, kFoBM, nout / ncol);
+    const int64_t cap = (int64_t)num_cus() / kXcd * kXcd;
+    return (unsigned)(g < cap ? g : cap);
+  };
+  if (profile) prof_begin(prof_gate_up, s);
+  launch_k(gemm_bf16_fo_kernel<MODE_GATEUP, true>, grid(128, ffn), 256, 0, s, x, rows_in, goff, G,
+           max_rows, w_gate_up_fo, d, ffn, H, ffn, x_scale, s_gate_up);
+  if (profile) prof_end(prof_gate_up, s);
+  if (profile) prof_begin(prof_gate_up + 1, s);
+  hipError_t e = launch_quantize_fp8(1, H, max_rows, ffn, goff ? goff + G : nullptr, Hq, Hs, s);
+  if (e != hipSuccess) return e;
+  launch_k(gemm_bf16_fo_kernel<MODE_DOWN, true>, grid(256, d), 256, 0, s, (const uint8_t*)Hq,
+           rows_out, goff, G, max_rows, w_down_fo, ffn, d, (bf16_t*)out, d, (const float*)Hs,
+           s_down);
   if (profile) prof_end(prof_gate_up + 1, s);
   return hipGetLastError();
 }

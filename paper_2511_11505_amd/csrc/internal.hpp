@@ -92,6 +92,18 @@ hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a,
 // matrices (rows % 32 == 0, cols % 16 == 0) to [rows/32][cols/16][64][8].
 hipError_t launch_fragment_order(const void* src, int64_t n_mats, int rows, int cols, void* dst,
                                  hipStream_t s);
+// FP8 fragment order of n_mats row-major [rows, cols] E4M3 code matrices
+// (rows % 32 == 0, cols % 64 == 0).
+hipError_t launch_fragment_order_fp8(const uint8_t* src, int64_t n_mats, int rows, int cols,
+                                     uint8_t* dst, hipStream_t s);
+// The FP8 grouped SwiGLU FFN on FP8-fragment-ordered weights (ffn % 128 == 0,
+// d % 256 == 0); operands and workspace as launch_grouped_ffn_fp8.
+hipError_t launch_grouped_ffn_fo_fp8(int G, int ffn, int d, const uint8_t* x, const float* x_scale,
+                                     const int32_t* rows_in, const int32_t* rows_out,
+                                     const int32_t* goff, int64_t max_rows,
+                                     const uint8_t* w_gate_up_fo, const float* s_gate_up,
+                                     const uint8_t* w_down_fo, const float* s_down, void* out,
+                                     void* ws, hipStream_t s, int prof_gate_up);
 // The grouped SwiGLU FFN on fragment-ordered weights (bf16; ffn % 128 == 0,
 // d % 256 == 0); the workspace is that of launch_grouped_ffn.
 hipError_t launch_grouped_ffn_fo(int G, int ffn, int d, const void* in, const int32_t* rows_in,

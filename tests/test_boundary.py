@@ -155,6 +155,20 @@ def test_other_entry_point_checks():
            FAKE, 100, FAKE, FAKE, FAKE, (FAKE, 1 << 40), stream=0)
     expect(L.FS_ERR_WORKSPACE, L.fs_grouped_expert_ffn_fo, d, 32, 2048, FAKE, None, FAKE, 100,
            FAKE, FAKE, FAKE, (FAKE, 64), stream=0)
+    # FP8 fragment order: whole 32-row x 64-byte fragments, no overlap; its
+    # FFN: the FP8 FFN's shapes and workspace
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_expert_weights_fragment_order_fp8, 2, 64, 96, FAKE,
+           FAKE + (1 << 20), stream=0)
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_expert_weights_fragment_order_fp8, 2, 48, 128, FAKE,
+           FAKE + (1 << 20), stream=0)
+    expect(L.FS_ERR_INVALID, L.fs_expert_weights_fragment_order_fp8, 2, 64, 128, FAKE,
+           FAKE + 4096, stream=0)
+    expect(L.FS_ERR_INVALID, L.fs_expert_weights_fragment_order_fp8, -1, 64, 128, FAKE,
+           FAKE + (1 << 20), stream=0)
+    expect(L.FS_ERR_UNSUPPORTED, L.fs_grouped_expert_ffn_fp8_fo, d, 32, 100, FAKE, FAKE, None, FAKE,
+           100, FAKE, FAKE, FAKE, FAKE, FAKE, (FAKE, 1 << 40), stream=0)
+    expect(L.FS_ERR_WORKSPACE, L.fs_grouped_expert_ffn_fp8_fo, d, 32, 2048, FAKE, FAKE, None, FAKE,
+           100, FAKE, FAKE, FAKE, FAKE, FAKE, (FAKE, 64), stream=0)
     expect(L.FS_ERR_UNSUPPORTED, L.fs_grouped_expert_ffn, d, 32, 100, FAKE, None, FAKE, 100, FAKE,
            FAKE, FAKE, (FAKE, 1 << 40), stream=0)
     expect(L.FS_ERR_WORKSPACE, L.fs_grouped_expert_ffn, d, 32, 2048, FAKE, None, FAKE, 100, FAKE,

@@ -90,14 +90,35 @@ def ffn_case(G, F, d, counts, gather, seed):
 # case but one has few tiles and long K, so both passes split K; the last
 # has more tiles than workgroups with two-block K rings (the ring runs on
 # from tile to tile)
-@pytest.mark.parametrize("counts,F,d,gather", [([0, 1, 64, 65, 130], 256, 512, True),
-                                               ([37], 128, 256, False),
-                                               ([3, 0, 5, 300, 1, 0, 2, 7], 384, 768, True),
-                                               ([513, 700], 512, 1024, False),
-                                               ([2304], 4096, 256, False),
-                                               ([100, 0, 170, 50], 1024, 2048, True),
-                                               ([12000, 0, 9001, 1, 8000, 11111], 256, 256, True)])
-def test_grouped_ffn_fp8_steps(counts, F, d, gather):
+FFN_CASES = [([0, 1, 64, 65, 130], 256, 512, True),
+             ([37], 128, 256, False),
+             ([3, 0, 5, 300, 1, 0, 2, 7], 384, 768, True),
+             ([513, 700], 512, 1024, False),
+             ([2304], 4096, 256, False),
+             ([100, 0, 170, 50], 1024, 2048, True),
+             ([12000, 0, 9001, 1, 8000, 11111], 256, 256, True)]
+# the FP8 fragment-order kernels (weights streamed into registers) on the
+# cases of a few rows per group, and one dense group (36 row tiles)
+FO_CASES = [c for i, c in enumerate(FFN_CASES) if i in (0, 1, 2, 4, 5)]
+
+
+def test_fragment_order_fp8_layout():
+    # fragment (g, c), half h of a code matrix holds, at lane l, row
+    # 32 g + l % 32 and columns 64 c + 32 (l / 32) + 16 h .. + 15: a plain
+    # reshape of the row-major matrix, checked bit for bit
+    from paper_2511_11505_amd import fragment_ordered_fp8
+    gen = torch.Generator(device=DEV).manual_seed(6)
+    w = torch.randint(0, 256, (3, 96, 192), generator=gen, device=DEV, dtype=torch.int32).to(torch.uint8)
+    fo = fragment_ordered_fp8(w)
+    torch.cuda.synchronize()
+    a = np_u8(w).reshape(3, 3, 32, 3, 2, 2, 16)        # [m][g][r][c][l/32][h][byte]
+    want = a.transpose(0, 1, 3, 5, 4, 2, 6).reshape(-1)  # [m][g][c][h][l/32][r][byte]
+    assert np.array_equal(np_u8(fo).reshape(-1), want)
+
+
+@pytest.mark.parametrize("counts,F,d,gather,fo", [c + (False,) for c in FFN_CASES]
+                         + [c + (True,) for c in FO_CASES])
+def test_grouped_ffn_fp8_steps(counts, F, d, gather, fo):
     G = len(counts)
     x, wgu, wdn, goff, rows, M = ffn_case(G, F, d, counts, gather, seed=sum(counts) + F)
     cfg = CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16")
@@ -108,8 +129,14 @@ def test_grouped_ffn_fp8_steps(counts, F, d, gather):
     out = torch.full((x.shape[0], d), float("nan"), dtype=torch.bfloat16, device=DEV)
     ws_bytes = L.fs_workspace_size(desc, L.FS_OP_GROUPED_FFN_FP8, M, F)
     ws = torch.empty((ws_bytes,), dtype=torch.uint8, device=DEV)
-    L.fs_grouped_expert_ffn_fp8(desc, G, F, xq, xs, rows, goff, M, gq.reshape(G, 2 * F, d), gs,
-                                dq.reshape(G, d, F), ds, out, ws)
+    if fo:
+        from paper_2511_11505_amd import fragment_ordered_fp8
+        L.fs_grouped_expert_ffn_fp8_fo(desc, G, F, xq, xs, rows, goff, M,
+                                       fragment_ordered_fp8(gq.reshape(G, 2 * F, d)), gs,
+                                       fragment_ordered_fp8(dq.reshape(G, d, F)), ds, out, ws)
+    else:
+        L.fs_grouped_expert_ffn_fp8(desc, G, F, xq, xs, rows, goff, M, gq.reshape(G, 2 * F, d), gs,
+                                    dq.reshape(G, d, F), ds, out, ws)
     torch.cuda.synchronize()
     a = lambda n: (n + 255) // 256 * 256
     H = ws[: M * F * 2].view(torch.bfloat16).reshape(M, F)
@@ -199,8 +226,8 @@ FP8_BLOCKS = {
 }
 
 
-@pytest.mark.parametrize("name", list(FP8_BLOCKS))
-def test_block_fp8_chain(name):
+@pytest.mark.parametrize("name,fo", [(n, False) for n in FP8_BLOCKS] + [("dsv3_decode_f8s", True)])
+def test_block_fp8_chain(name, fo):
     # The block with FP8 experts: (a) gate and plan equal the bf16 block's
     # bit for bit, and its send and receive rows (FP8 dispatch) are the
     # codes and scales of the bf16 block's rows; (b) the local expert rows and the shared output
@@ -220,7 +247,7 @@ def test_block_fp8_chain(name):
     blocks, outs = {}, {}
     for mode in (None, "all"):
         blk = MoEBlock(cfg, wl.w_router, wl.bias, wl.w_gate_up, wl.w_down, sh_gu, sh_dn,
-                       device=DEV, fp8=mode)
+                       device=DEV, fp8=mode, fragment_order=fo)
         if cfg.ep_size > 1:
             blk.set_max_recv_rows(prepare_remote_sources(blk, wl.x_all, wl.w_router, wl.bias,
                                                          wl.y_remote))
@@ -254,9 +281,15 @@ def test_block_fp8_chain(name):
     desc = b8.desc
     ws = torch.empty((L.fs_workspace_size(desc, L.FS_OP_GROUPED_FFN_FP8, b8.max_recv_rows, cfg.ffn),),
                      dtype=torch.uint8, device=DEV)
-    L.fs_grouped_expert_ffn_fp8(desc, E_loc, cfg.ffn, xq, xs, rows, goff, b8.max_recv_rows,
-                                q["w_gate_up_fp8"], q["s_gate_up"], q["w_down_fp8"], q["s_down"],
-                                y_ref, ws)
+    if fo:
+        # the block streams the FP8-fragment-ordered codes (decode)
+        L.fs_grouped_expert_ffn_fp8_fo(desc, E_loc, cfg.ffn, xq, xs, rows, goff, b8.max_recv_rows,
+                                       q["w_gate_up_fp8_fo"], q["s_gate_up"], q["w_down_fp8_fo"],
+                                       q["s_down"], y_ref, ws)
+    else:
+        L.fs_grouped_expert_ffn_fp8(desc, E_loc, cfg.ffn, xq, xs, rows, goff, b8.max_recv_rows,
+                                    q["w_gate_up_fp8"], q["s_gate_up"], q["w_down_fp8"], q["s_down"],
+                                    y_ref, ws)
     x = wl.x
     xq_s, xs_s = quantize(x)
     sh_ref = torch.empty_like(x)
