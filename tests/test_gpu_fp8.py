@@ -99,7 +99,11 @@ FFN_CASES = [([0, 1, 64, 65, 130], 256, 512, True),
              ([12000, 0, 9001, 1, 8000, 11111], 256, 256, True)]
 # the FP8 fragment-order kernels (weights streamed into registers) on the
 # cases of a few rows per group, and one dense group (36 row tiles)
-FO_CASES = [c for i, c in enumerate(FFN_CASES) if i in (0, 1, 2, 4, 5)]
+FO_CASES = [c for i, c in enumerate(FFN_CASES) if i in (0, 1, 2, 4, 5)] + [
+    # 320 tiles per pass, two per workgroup, K of 8 and 4 blocks; then a
+    # down pass of K = 2 blocks
+    ([100] * 40, 512, 1024, True),
+    ([100] * 40, 256, 1024, True)]
 
 
 def test_fragment_order_fp8_layout():

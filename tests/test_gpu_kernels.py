@@ -423,6 +423,8 @@ def test_fragment_order_layout():
     ([37], 512, 128, False),                    # one group
     ([3, 0, 5, 9, 1, 0, 2, 7], 256, 384, True),   # many small groups, K of 4 blocks (tail)
     ([20, 113, 0, 61, 2], 1024, 640, True),     # K rings of 16 and 10 blocks (ragged tails)
+    # 320 tiles per pass: workgroups take two (K of 16 and 8 blocks)
+    ([100] * 40, 1024, 512, True),
 ])
 def test_grouped_ffn_fragment_order(counts, d, F, gather):
     """The grouped SwiGLU FFN on fragment-ordered weights (weights streamed
