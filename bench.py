@@ -48,8 +48,6 @@ def measured_traffic(cfg_name):
     src = os.path.join(ROOT, rec["source"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
         return None
-    if os.environ.get("FS_GEMM_TILE") not in (None, "", str(rec.get("tile", ""))):
-        return None
     return rec["hbm_bytes_per_launch"]
 
 

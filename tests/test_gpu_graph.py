@@ -7,6 +7,7 @@ import pytest
 import torch
 
 from paper_2511_11505_amd import MoEBlock, prepare_remote_sources
+from paper_2511_11505_amd import _lib as L
 from paper_2511_11505_amd.stack import LayerStack
 from tests.test_gpu_kernels import SMALL
 from workloads import make_workload
@@ -65,7 +66,11 @@ def test_block_graph_replays_equal_eager(name):
     blk.close()
 
 
-def test_stack_graph_replays_equal_eager():
+@pytest.mark.parametrize("link", [False, True])
+def test_stack_graph_replays_equal_eager(link):
+    # link: the Dispatch and Combine stand-ins captured as link-paced copy
+    # kernels (fs_standin_link), whose pacing starts from each replay's own
+    # clock
     cfg = SMALL["dsv2lite_s"]
     layers = stack_layers(cfg, 2, DEV)
     st = LayerStack(cfg, layers, device=DEV, merge_shared=merge_shared)
@@ -76,9 +81,10 @@ def test_stack_graph_replays_equal_eager():
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        with torch.cuda.graph(g):
-            res = st.farskip(x, compute=torch.cuda.current_stream(), comm=comm)
+    with L.standin_link(*((7, 153e9, 32) if link else (0,))):
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g):
+                res = st.farskip(x, compute=torch.cuda.current_stream(), comm=comm)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     for i in range(3):
