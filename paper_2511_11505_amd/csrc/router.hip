@@ -651,8 +651,10 @@ hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, 
     return hipGetLastError();
   }
   if (use_mfma_router(dtype, N, E)) {
-    // workgroup tile: 64 tokens x 128 experts, or 128 x 64 (measured on
-    // 4096 tokens over 256 experts: 64 x 128 192 us, 32 x 256 198 us)
+    // workgroup tile: 64 tokens x 128 experts, or 128 x 64 where 64-wide
+    // expert tiles pad less (measured on 4096 tokens over 256 experts:
+    // 64 x 128 192 us, 32 x 256 198 us; over 160 experts, d 5120: 128 x 64
+    // 96 us against 122 us for 64 x 128, which pads 160 to 256)
     const int z = split ? router_slices(d) : 1;
 #define FS_ROUTER_MFMA(WT, WE)                                                               \
   do {                                                                                       \
@@ -664,9 +666,7 @@ hipError_t launch_router_logits(int dtype, const void* x, const void* w, int N, 
       launch_k(router_mfma_kernel<WT, WE, false>, g, 256, 0, s, (const bf16_t*)x,           \
                (const bf16_t*)w, N, d, E, out);                                              \
   } while (0)
-    if (E > 128)
-      FS_ROUTER_MFMA(2, 2);
-    else if (E > 64)
+    if (E > 64 && cdiv64(E, 128) * 128 <= cdiv64(E, 64) * 64)
       FS_ROUTER_MFMA(2, 2);
     else
       FS_ROUTER_MFMA(4, 1);
