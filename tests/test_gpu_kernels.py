@@ -154,10 +154,12 @@ def plan_gpu(cfg, ids, x):
                                            (64, 64, 6, 1, "bf16"), (65, 64, 6, 8, "bf16"),
                                            (512, 512, 32, 4, "bf16"), (1000, 256, 8, 8, "bf16"),
                                            (777, 512, 32, 4, "f32"), (4096, 16, 1, 1, "bf16"),
-                                           (4200, 256, 4, 8, "bf16")])
+                                           (4200, 256, 4, 8, "bf16"), (4096, 256, 8, 8, "bf16"),
+                                           (8192, 16, 1, 1, "bf16"), (20000, 64, 8, 8, "bf16")])
 def test_plan_pack_bitexact(N, E, k, R, dtype):
-    # up to 512 tokens (eight 64-token tiles) the plan runs in one
-    # workgroup, beyond in three kernels
+    # up to tiles x slots = 2^23 the plan runs in one workgroup per 64-token
+    # tile that counts every slot (4096 x 8: 2^21), beyond (20000 x 8) in
+    # three kernels
     cfg = CONFIGS["tiny"].scaled(n_tokens=N, n_experts=E, top_k=k, ep_size=R, hidden=128, dtype=dtype)
     ids = synthetic_topk_ids(N, E, k, seed=N + E, device=DEV, skew=1.1)
     x = torch.randn((N, 128), device=DEV).to(torch.float32 if dtype == "f32" else torch.bfloat16)
