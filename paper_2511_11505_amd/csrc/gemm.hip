@@ -433,6 +433,14 @@ __device__ __forceinline__ void store_tile(floatx16 (&acc)[TM][TN], unsigned cha
 // The epilogue goes through LDS in passes of IPP 32-row accumulator rows per
 // wave, every wave converting in every pass (gate/up: SiLU(g) * u), then all
 // threads store whole 16-byte chunks of the staged rows.
+//
+// Waves: WGM rows of two, each wave BM / WGM x BN / 2.  Four waves (WGM = 2)
+// hold one per SIMD; eight (WGM = 4: 256 x 256 tiles, 64 x 128 per wave)
+// two per SIMD, with the 128 accumulators of a wave in ordinary VGPRs.  The
+// 256 x 256 tile takes eight: four waves of 128 x 128 need all 512
+// registers and spill (72 bytes per lane), for the same time (DeepSeek-V3-
+// shaped shared down pass, 4096 x 7168, K 2048: 134-140 against 133-137 us
+// alone on the GPU).
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
@@ -441,8 +449,9 @@ __device__ __forceinline__ void wait_lgkm0() {
 
 typedef int int32x8 __attribute__((ext_vector_type(8)));
 
-template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false, bool SPL = false>
-__global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
+template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false, bool SPL = false,
+          int WGM = 2>
+__global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ B, int K, int NOUT,
@@ -450,8 +459,8 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
     int splits, int kps, float* __restrict__ P) {
   using TE = typename std::conditional<F8, uint8_t, bf16_t>::type;
   using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
-  constexpr int NT = 256;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int NT = 128 * WGM;                    // WGM x 2 waves
+  constexpr int WTM = BM / WGM, WTN = BN / 2;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int ES = F8 ? 1 : 2;                   // element bytes
   constexpr int CE = 16 / ES;                      // elements per 16-byte chunk
@@ -460,7 +469,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   constexpr int RPB = 1024 / ROWB;
   constexpr int SWD = 16 / CPR;
   constexpr int STAGE = (BM + BN) * ROWB;
-  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;
+  constexpr int A_LD = BM / RPB / (2 * WGM), B_LD = BN / RPB / (2 * WGM);
   constexpr int NLD = A_LD + B_LD;
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
   constexpr int SST = NCOL + 8;                    // staged row, bf16 elements
@@ -482,17 +491,18 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_il_kernel(
   static_assert(KS >= 2, "at least two K steps per block");
   static_assert(DPQ <= 2, "two DMAs per MFMA at most");
   static_assert(!F8 || BK == 128, "FP8 rows are 128 elements");
-  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (2 * WGM * RPB) == 0 && BN % (2 * WGM * RPB) == 0,
+                "tile");
   // Cross-tile candidates: 128-row tiles without split K (256-row tiles
   // already use every register).  Their staging must fit one slot, the
   // others' the whole ring.  IPP: accumulator rows (of 32) per wave and
   // epilogue pass; SROWS: staged rows per pass.
-  constexpr bool XTC = !SPL && BM == 128;
+  constexpr bool XTC = !SPL && BM == 128 && WGM == 2;
   constexpr int SCAP = XTC ? STAGE : STAGES * STAGE;
-  constexpr int IPP = (TM % 4 == 0 && 256 * SST * 2 <= SCAP)   ? 4
-                      : (TM % 2 == 0 && 128 * SST * 2 <= SCAP) ? 2
-                                                               : 1;
-  constexpr int SROWS = 64 * IPP;
+  constexpr int IPP = (TM % 4 == 0 && WGM * 128 * SST * 2 <= SCAP)  ? 4
+                      : (TM % 2 == 0 && WGM * 64 * SST * 2 <= SCAP) ? 2
+                                                                    : 1;
+  constexpr int SROWS = WGM * 32 * IPP;
   constexpr bool XT = XTC && SROWS * SST * 2 <= STAGE;
   static_assert(SROWS * SST * 2 <= STAGES * STAGE, "epilogue pass must fit in the ring");
   static_assert((SROWS * NCOL / 8) % NT == 0, "whole store rounds");
@@ -1688,9 +1698,9 @@ constexpr int kBM = 128, kBN = 128, kBK = 64;
 // tiles fill the 256 compute units, and the interleaved 128 x 256 x 64 ring
 // (5) otherwise, where half-empty 256-row tail tiles would waste MFMA work
 // or too few tiles would leave CUs idle (narrow tensor-parallel slices);
-// down takes the interleaved 256 x 256 x 64 ring (7) when K < 2816, the
-// groups average at least 1024 rows and its tiles fill the 256 compute
-// units, and the 128-row interleaved ring (5) otherwise.  nout: output
+// down takes the interleaved 256 x 256 x 64 ring with eight waves (7) when
+// K < 2816, the groups average at least 2048 rows and its tiles fill the
+// 256 compute units, and the 128-row interleaved ring (5) otherwise.  nout: output
 // columns of the pass (F for gate/up, d for down).
 int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
   if (down) {
@@ -1743,32 +1753,35 @@ struct KSplit {
   float* P = nullptr;
 };
 
-template <int MODE, int BM, int BN, int BK, int ST, int OCC>
+template <int MODE, int BM, int BN, int BK, int ST, int OCC, int WGM = 2>
 void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s,
             const KSplit& sp = KSplit{}) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, OCC);
   if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true>, (unsigned)g, 256, 0, s,
-             A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, sp.splits, sp.kps,
-             sp.P);
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM>, (unsigned)g,
+             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
+             sp.splits, sp.kps, sp.P);
   else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC>, (unsigned)g, 256, 0, s, A, rows, goff,
-             G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1, K / BK, nullptr);
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM>, (unsigned)g,
+             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
+             K / BK, nullptr);
 }
-template <int MODE, int BM, int BN, int ST>
+template <int MODE, int BM, int BN, int ST, int WGM = 2>
 void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
                const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc, const float* sA,
                const float* sB, hipStream_t s, const KSplit& sp) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, 1);
   if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, true>, (unsigned)g, 256, 0, s, A,
-             rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, sp.splits, sp.kps, sp.P);
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, true, WGM>, (unsigned)g,
+             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, sp.splits,
+             sp.kps, sp.P);
   else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true>, (unsigned)g, 256, 0, s, A, rows,
-             goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128, nullptr);
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, false, WGM>, (unsigned)g,
+             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128,
+             nullptr);
 }
 template <int MODE, int BM, int BN, int BK>
 void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
@@ -1781,14 +1794,14 @@ void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
 // Variants 5, 7 and 8 have BN = 256 and BK = 64: they need NOUT % 128 == 0
 // for gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
 // only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to the
-// interleaved variants 5 and 7 only.)
+// interleaved variant 5 only.)
 template <int MODE>
 void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
                int64_t m_total, const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc,
                hipStream_t s, const KSplit& sp = KSplit{}) {
 #define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
   switch (v) {
-    case 7: run_il<MODE, 256, 256, 64, 2, 1>(FS_ARGS, sp); break;
+    case 7: run_il<MODE, 256, 256, 64, 2, 1, 4>(FS_ARGS); break;
     case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
     case 10:
       // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
@@ -2007,9 +2020,8 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
                                         ((size_t)max_rows * ffn * 2 + 255) / 256 * 256);
     const size_t pbytes = stream_partial_bytes(dtype, max_rows, ffn, d);
     auto split_of = [&](int v, bool gateup, int K, int NOUT) {
-      if (v != 5 && v != 7) return KSplit{};
-      return make_split(ring_splits(gateup, v == 7 ? 256 : 128, max_rows, G, K / 64, NOUT, pbytes),
-                        K / 64, P);
+      if (v != 5) return KSplit{};
+      return make_split(ring_splits(gateup, 128, max_rows, G, K / 64, NOUT, pbytes), K / 64, P);
     };
     if (profile) prof_begin(pg, s);
     {

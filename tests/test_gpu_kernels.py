@@ -261,6 +261,37 @@ def test_grouped_ffn_many_tiles(counts, d, F, gather):
     assert np.all(np.isnan(outn[np.setdiff1d(np.arange(n_src), rr)]))
 
 
+def test_grouped_ffn_wide_tiles():
+    """Two long groups (4100 and 2050 rows, both ragged at 256) with a short
+    K: the down pass takes the eight-wave 256 x 256 tiles ((17 + 9) x 16 =
+    416 tiles), gate/up the 128-row ring; sampled rows of each group (the first
+    64, 64 from the middle, the last 300: its ragged tiles) against the
+    oracle element by element."""
+    counts = np.array([4100, 2050])
+    d, F = 4096, 256
+    G, M = len(counts), int(counts.sum())
+    goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    gen = torch.Generator(device=DEV).manual_seed(4100)
+    n_src = M + 11
+    X = torch.randn((n_src, d), generator=gen, device=DEV).to(torch.bfloat16)
+    wgu = (0.05 * torch.randn((G, 2 * F, d), generator=gen, device=DEV)).to(torch.bfloat16)
+    wd = (0.05 * torch.randn((G, d, F), generator=gen, device=DEV)).to(torch.bfloat16)
+    rows = torch.randperm(n_src, generator=gen, device=DEV)[:M].to(torch.int32)
+    out = torch.full((n_src, d), float("nan"), device=DEV).to(torch.bfloat16)
+    desc = L.make_desc(CONFIGS["tiny"].scaled(hidden=d, ffn=F, dtype="bf16"))
+    L.fs_grouped_expert_ffn(desc, G, F, X, rows, torch.from_numpy(goff).to(DEV), M, wgu, wd, out,
+                            ws_for(desc, L.FS_OP_GROUPED_FFN, M, F))
+    torch.cuda.synchronize()
+    rr = rows.cpu().numpy()
+    for gi in range(G):
+        n = counts[gi]
+        pick = np.concatenate([np.arange(64), np.arange(n // 2 - 32, n // 2 + 32), np.arange(n - 300, n)])
+        sel = rr[goff[gi] + pick]
+        want = oracle.swiglu(f64(X[torch.from_numpy(sel).to(DEV).long()]), f64(wgu[gi]), f64(wd[gi]))
+        assert rel_err(f64(out[torch.from_numpy(sel).to(DEV).long()]), want) <= TOL["bf16"], f"group {gi}"
+    assert torch.isnan(out[torch.from_numpy(np.setdiff1d(np.arange(n_src), rr)).to(DEV).long()]).all()
+
+
 @pytest.mark.parametrize("counts,d,F,gather", [([100, 0, 170, 50], 1024, 1024, True),
                                                ([41, 300, 7], 2048, 512, False)])
 def test_grouped_ffn_split_k(counts, d, F, gather):
