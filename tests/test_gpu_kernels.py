@@ -323,12 +323,17 @@ def test_grouped_ffn_split_k(counts, d, F, gather):
 
 @pytest.mark.parametrize("counts,d,F,gather", [
     ([0, 1, 64, 65, 130], 768, 320, True),     # m-chunks of 64, split K 6 / 2 slices (3 + 2 blocks)
-    ([37], 512, 256, False),                   # one group (a decode shared expert)
+    ([37], 512, 256, False),                   # one group (a decode shared expert), K 256: streamed
+    ([50], 1024, 512, True),                   # one group, K 512: the skinny down pass
+    ([64], 512, 1024, False),                  # a full 64-row group, skinny down (K 1024)
+    ([1], 512, 512, True),                     # one row, skinny down
     ([3, 0, 5, 9, 1, 0, 2, 7], 384, 192, True),  # many small groups
 ])
 def test_grouped_ffn_streaming(counts, d, F, gather):
     """Groups averaging at most 64 rows take the weight-streaming kernel (with
-    split K when its tiles are few); element by element against the oracle."""
+    split K when its tiles are few); the down pass of one group of at most 64
+    rows takes the skinny kernel where K % 512 == 0; element by element
+    against the oracle."""
     counts = np.array(counts)
     G, M = len(counts), int(counts.sum())
     goff = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
