@@ -7,10 +7,10 @@
 //   down:     Y[row_i] = H[i] . Wd^T                        (rows scattered
 //             through group_rows)
 // bf16 runs on MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) with both
-// operand tiles staged through a ring of LDS slots: direct global->LDS copies
-// (DMA kernels) or loads a block ahead into registers (register-staged
-// kernel).  The launcher picks the tile variant per pass from the shape.
-// fp32 runs on the vector ALUs.
+// operand tiles staged through a ring of LDS slots by direct global->LDS
+// copies; few-row passes stream the weights straight into registers.  The
+// launcher picks the tile variant per pass from the shape.  fp32 runs on
+// the vector ALUs.
 //
 // Groups have ragged row counts known only on the device.  Every workgroup
 // rebuilds the per-group m-tile prefix from group_offsets in LDS, then walks
@@ -330,64 +330,6 @@ __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
-// Tile epilogue shared by the LDS-ring kernels.  Accumulator element v of
-// lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32 of its 32x32 tile.
-// Passes of 128 output columns are staged as bf16 in the ring (which must be
-// idle), then stored as 16-byte row chunks; gate/up tiles apply SwiGLU to
-// matching gate and up accumulators first.  Ends with a barrier, after which
-// the ring may be refilled.
-template <int MODE, int BM, int NCOL, int TM, int TN, int WTM, int WTN, int NT>
-__device__ __forceinline__ void store_tile(floatx16 (&acc)[TM][TN], unsigned char* ring, int wm,
-                                           int wn, int lane, int tid, int m0, int rows_g,
-                                           int row_base, const int32_t* __restrict__ rows,
-                                           bf16_t* __restrict__ C, int ldc, int n0) {
-  constexpr int ECOL = 128;
-  constexpr int CST = ECOL + 8;
-  constexpr int PASSES = NCOL / ECOL;
-  static_assert(NCOL % ECOL == 0, "epilogue passes");
-  static_assert(MODE != MODE_GATEUP || (TN % 2 == 0 && 2 * (WTN / 2) == ECOL), "gate/up pairing");
-  static_assert(MODE != MODE_DOWN || ECOL % WTN == 0, "a wave's columns stay in one pass");
-  bf16_t* Cs = reinterpret_cast<bf16_t*>(ring);
-#pragma unroll
-  for (int pass = 0; pass < PASSES; ++pass) {
-    __syncthreads();
-    if (MODE == MODE_GATEUP || (wn * WTN) / ECOL == pass) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          if (MODE == MODE_GATEUP) {
-#pragma unroll
-            for (int jn = 0; jn < TN / 2; ++jn) {
-              const float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
-              Cs[r * CST + wn * (WTN / 2) + jn * 32 + (lane & 31)] = f2bf(swiglu_bf16_epi(gt, up));
-            }
-          } else {
-#pragma unroll
-            for (int jn = 0; jn < TN; ++jn)
-              Cs[r * CST + (wn * WTN) % ECOL + jn * 32 + (lane & 31)] = f2bf(acc[i][jn][v]);
-          }
-        }
-      }
-    }
-    __syncthreads();
-    constexpr int CPRC = ECOL / 8;
-#pragma unroll 4
-    for (int c = tid; c < BM * CPRC; c += NT) {
-      const int r = c / CPRC, ch = c % CPRC;
-      const int m = m0 + r;
-      if (m < rows_g) {
-        const int grow = row_base + m;
-        const int64_t orow = (MODE == MODE_DOWN && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-        st16(C + orow * ldc + n0 + pass * ECOL + ch * 8,
-             *reinterpret_cast<const uint4*>(Cs + r * CST + ch * 8));
-      }
-    }
-  }
-  __syncthreads();
-}
-
 // ---------------------------------------------------------------- bf16 MFMA, interleaved
 // Same tiles, ring and swizzle as above, with the memory work hidden under
 // the MFMAs by a rolling pipeline over 16-wide K steps.  Each step first
@@ -434,13 +376,17 @@ __device__ __forceinline__ void store_tile(floatx16 (&acc)[TM][TN], unsigned cha
 // wave, every wave converting in every pass (gate/up: SiLU(g) * u), then all
 // threads store whole 16-byte chunks of the staged rows.
 //
-// Waves: WGM rows of two, each wave BM / WGM x BN / 2.  Four waves (WGM = 2)
-// hold one per SIMD; eight (WGM = 4: 256 x 256 tiles, 64 x 128 per wave)
-// two per SIMD, with the 128 accumulators of a wave in ordinary VGPRs.  The
-// 256 x 256 tile takes eight: four waves of 128 x 128 need all 512
-// registers and spill (72 bytes per lane), for the same time (DeepSeek-V3-
-// shaped shared down pass, 4096 x 7168, K 2048: 134-140 against 133-137 us
-// alone on the GPU).
+// Waves: a WGM x WGN grid, each wave BM / WGM x BN / WGN.  Four waves (2 x 2)
+// hold one per SIMD; eight hold two per SIMD, whose instruction streams
+// interleave: with one wave per SIMD the wave waits to issue 44% of its
+// cycles (SQ_WAIT_INST_ANY, Llama-4-Scout-shaped routed gate/up) while the
+// MFMA pipe is busy 55%.  The 128 x 256 tile runs 2 x 4 waves of 64 x 64
+// (routed gate/up 1493 -> 1432 us Scout-shaped, 377 -> 362 us
+// DeepSeek-V2-Lite-shaped; DeepSeek-V3-shaped down 1073 -> 997 us; alone
+// on the GPU), the 256 x 256 tile 4 x 2 waves of 64 x 128: four waves of
+// 128 x 128 need all 512 registers and spill (72 bytes per lane), for the
+// same time (DeepSeek-V3-shaped shared down pass, 4096 x 7168, K 2048:
+// 134-140 against 133-137 us).
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
@@ -450,8 +396,8 @@ __device__ __forceinline__ void wait_lgkm0() {
 typedef int int32x8 __attribute__((ext_vector_type(8)));
 
 template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false, bool SPL = false,
-          int WGM = 2>
-__global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
+          int WGM = 2, int WGN = 2>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ B, int K, int NOUT,
@@ -459,8 +405,8 @@ __global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
     int splits, int kps, float* __restrict__ P) {
   using TE = typename std::conditional<F8, uint8_t, bf16_t>::type;
   using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
-  constexpr int NT = 128 * WGM;                    // WGM x 2 waves
-  constexpr int WTM = BM / WGM, WTN = BN / 2;
+  constexpr int NT = 64 * WGM * WGN;               // WGM x WGN waves
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int ES = F8 ? 1 : 2;                   // element bytes
   constexpr int CE = 16 / ES;                      // elements per 16-byte chunk
@@ -469,7 +415,7 @@ __global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
   constexpr int RPB = 1024 / ROWB;
   constexpr int SWD = 16 / CPR;
   constexpr int STAGE = (BM + BN) * ROWB;
-  constexpr int A_LD = BM / RPB / (2 * WGM), B_LD = BN / RPB / (2 * WGM);
+  constexpr int A_LD = BM / RPB / (WGN * WGM), B_LD = BN / RPB / (WGN * WGM);
   constexpr int NLD = A_LD + B_LD;
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
   constexpr int SST = NCOL + 8;                    // staged row, bf16 elements
@@ -491,7 +437,7 @@ __global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
   static_assert(KS >= 2, "at least two K steps per block");
   static_assert(DPQ <= 2, "two DMAs per MFMA at most");
   static_assert(!F8 || BK == 128, "FP8 rows are 128 elements");
-  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (2 * WGM * RPB) == 0 && BN % (2 * WGM * RPB) == 0,
+  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (WGN * WGM * RPB) == 0 && BN % (WGN * WGM * RPB) == 0,
                 "tile");
   // Cross-tile candidates: 128-row tiles without split K (256-row tiles
   // already use every register).  Their staging must fit one slot, the
@@ -515,7 +461,7 @@ __global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
   __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
 
   const int nn = NOUT / NCOL;
@@ -879,205 +825,6 @@ __global__ __launch_bounds__(128 * WGM, OCC) void gemm_bf16_il_kernel(
       sb = (sb + KT) % STAGES;
       primed = has_next;
     }
-  }
-}
-
-// ---------------------------------------------------------------- bf16 MFMA, register-staged
-// 256 x 256 x 64 tiles: four waves of 128 x 128 (sixteen 32x32 accumulators
-// each, held in AGPRs), one wave per SIMD, two LDS slots of 64 KB.  A K block's
-// operand tiles are loaded into registers one whole block ahead (block kt+2
-// during block kt) and written to the free LDS slot at the start of the next
-// block, so a global load has a full block of MFMAs (64 per wave) to land,
-// where a direct-to-LDS copy into a two-slot ring would have three K steps.
-// Rows are 128 bytes (BK = 64 bf16), so every 8-lane group of a load reads
-// one whole cache line.
-//
-// Per block kt (four 16-wide K steps, rolling fragment reads as above):
-//   step 0: MFMAs, each followed by one LDS write of block kt+1
-//   step 1: MFMAs, each followed by one global load of block kt+2
-//   step 3: wait for this wave's LDS traffic, barrier, then read block kt+1.
-// The barrier of block kt-1 is what frees slot (kt+1) % 2 for the writes.
-template <int MODE, int BM, int BN, int BK>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_rs_kernel(
-    const bf16_t* __restrict__ A, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ goff, int G, int64_t m_total, const bf16_t* __restrict__ B, int K,
-    int NOUT, bf16_t* __restrict__ C, int ldc) {
-  constexpr int NT = 256, STAGES = 2;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int ROWB = BK * 2;
-  constexpr int CPR = BK / 8;
-  constexpr int RPB = 1024 / ROWB;
-  constexpr int SWD = 16 / CPR;
-  constexpr int STAGE = (BM + BN) * ROWB;
-  constexpr int A_LD = BM / RPB / 4, B_LD = BN / RPB / 4;
-  constexpr int NLD = A_LD + B_LD;
-  constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
-  constexpr int KS = BK / 16;
-  constexpr int NF = TM + TN;
-  constexpr int MPS = TM * TN;
-  auto read_slot = [](int r) { return ((r + 1) * MPS) / NF - 1; };
-  static_assert(KS >= 2 && KS % 2 == 0, "an even number of K steps per block");
-  static_assert(MPS >= NF, "one fragment read per MFMA at most");
-  static_assert(NLD <= MPS, "one LDS write and one global load per MFMA at most");
-  static_assert(A_LD >= 1 && B_LD >= 1 && BM % (4 * RPB) == 0 && BN % (4 * RPB) == 0, "tile");
-  static_assert(MODE != MODE_GATEUP || TN % 2 == 0, "gate/up tiles come in pairs");
-
-  __shared__ int s_goff[kMaxGroups + 1];
-  __shared__ int s_tpre[kMaxGroups + 1];
-  __shared__ int s_wtot[NT / 64];
-  __shared__ __align__(1024) unsigned char ring[STAGES * STAGE];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  sched_setup<NT, BM>(goff, G, m_total, s_goff, s_tpre, s_wtot);
-
-  const int nn = NOUT / NCOL;
-  const int64_t total = (int64_t)nn * s_tpre[G];
-  const int64_t per_xcd = (total + kXcd - 1) / kXcd;
-  const int64_t xcd_base = (int64_t)(blockIdx.x % kXcd) * per_xcd;
-  const int64_t stride = gridDim.x / kXcd;
-  const int KT = K / BK;
-  const size_t bstride = (size_t)((MODE == MODE_GATEUP) ? 2 * NOUT : NOUT) * K;
-  // lane l loads row l / CPR of a 1 KB block, the logical chunk that the
-  // swizzle stores at position l % CPR; it writes LDS linearly at l * 16
-  const int drow = lane / CPR, dpos = lane % CPR;
-  auto dchunk = [&](int block) { return dpos ^ (((block * RPB + drow) / SWD) % CPR); };
-
-  int aoff[TM], boff[TN], asw[TM], bsw[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = wm * WTM + i * 32 + (lane & 31);
-    aoff[i] = r * ROWB;
-    asw[i] = (r / SWD) % CPR;
-  }
-#pragma unroll
-  for (int jn = 0; jn < TN; ++jn) {
-    int r;
-    if (MODE == MODE_GATEUP)
-      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
-    else
-      r = wn * WTN + jn * 32;
-    r += lane & 31;
-    boff[jn] = BM * ROWB + r * ROWB;
-    bsw[jn] = (r / SWD) % CPR;
-  }
-
-  for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
-    const int64_t L = xcd_base + j;
-    if (L >= total) break;
-    const int g = find_group(s_tpre, G, nn, L);
-    const int Tg = s_tpre[g + 1] - s_tpre[g];
-    const int64_t local = L - (int64_t)nn * s_tpre[g];
-    const int nt = (int)(local / Tg), mt = (int)(local % Tg);
-    const int row_base = s_goff[g], rows_g = s_goff[g + 1] - row_base;
-    const int m0 = mt * BM, n0 = nt * NCOL;
-    const bf16_t* Bg = B + (size_t)g * bstride;
-
-    const bf16_t* src[NLD];
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int blk = wave * A_LD + i;
-      int m = m0 + blk * RPB + drow;
-      if (m >= rows_g) m = rows_g - 1;
-      const int grow = row_base + m;
-      const int64_t sr = (MODE == MODE_GATEUP && rows) ? (int64_t)rows[grow] : (int64_t)grow;
-      src[i] = A + sr * K + dchunk(blk) * 8;
-    }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int blk = wave * B_LD + i;
-      const int r = blk * RPB + drow;
-      int wrow;
-      if (MODE == MODE_GATEUP)
-        wrow = (r < BN / 2) ? n0 + r : NOUT + n0 + (r - BN / 2);
-      else
-        wrow = n0 + r;
-      src[A_LD + i] = Bg + (size_t)wrow * K + dchunk(blk) * 8;
-    }
-    auto dst_of = [&](int i) {
-      return (i < A_LD ? (wave * A_LD + i) * 1024 : BM * ROWB + (wave * B_LD + (i - A_LD)) * 1024) +
-             lane * 16;
-    };
-    uint4 stg[NLD];
-    auto gload = [&](int i, int kt) { stg[i] = ld16(src[i] + kt * BK); };
-    auto lwrite = [&](int i, int kt) { st16(ring + (kt % STAGES) * STAGE + dst_of(i), stg[i]); };
-
-    floatx16 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < TN; ++jn)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
-
-    bf16x8 Fa[NF], Fb[NF];
-    // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
-    // A1..A(TM-1); read r is issued after MFMA read_slot(r) of the step before
-    auto read_one = [&](bf16x8 (&F)[NF], int kt, int ks, int r) {
-      const unsigned char* slot = ring + (kt % STAGES) * STAGE;
-      const int c = ks * 2 + (lane >> 5);
-      const int f = r == 0 ? 0 : (r <= TN ? TM + r - 1 : r - TN);
-      const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
-      F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
-    };
-    auto read_step = [&](bf16x8 (&F)[NF], int kt, int ks) {
-#pragma unroll
-      for (int r = 0; r < NF; ++r) read_one(F, kt, ks, r);
-    };
-    // N1 / N2 (compile-time flags): blocks kt+1 / kt+2 exist.  Reads of the
-    // next step's fragments are spread between the MFMAs as in the DMA kernel.
-    auto step = [&](bf16x8 (&Fc)[NF], bf16x8 (&Fn)[NF], int kt, int ks, auto N1, auto N2) {
-      constexpr bool n1 = decltype(N1)::value, n2 = decltype(N2)::value;
-      const bool more = ks < KS - 1 || n1;
-      const int rkt = ks < KS - 1 ? kt : kt + 1, rks = ks < KS - 1 ? ks + 1 : 0;
-#pragma unroll
-      for (int q = 0; q < MPS; ++q) {
-        const int i = q / TN, jn = q % TN;
-        acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (n1 && q == 0 && ks == KS - 1) {
-          wait_lgkm0();
-          barrier_nofence();
-          __builtin_amdgcn_sched_barrier(0);
-        }
-#pragma unroll
-        for (int r = 0; r < NF; ++r)
-          if (q == read_slot(r) && more) read_one(Fn, rkt, rks, r);
-        if (q < NLD) {
-          if (n1 && ks == 0) lwrite(q, kt + 1);
-          if (n2 && ks == 1) gload(q, kt + 2);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    auto run_block = [&](int kt, auto N1, auto N2) {
-#pragma unroll
-      for (int ks = 0; ks < KS; ks += 2) {
-        step(Fa, Fb, kt, ks, N1, N2);
-        step(Fb, Fa, kt, ks + 1, N1, N2);
-      }
-    };
-
-    // prologue: block 0 in slot 0, block 1 in registers, block 0's first
-    // fragments read
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) gload(i, 0);
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) lwrite(i, 0);
-    if (KT > 1) {
-#pragma unroll
-      for (int i = 0; i < NLD; ++i) gload(i, 1);
-    }
-    wait_lgkm0();
-    barrier_nofence();
-    read_step(Fa, 0, 0);
-    for (int kt = 0; kt + 2 < KT; ++kt) run_block(kt, std::true_type{}, std::true_type{});
-    if (KT >= 2) run_block(KT - 2, std::true_type{}, std::false_type{});
-    run_block(KT - 1, std::false_type{}, std::false_type{});
-
-    store_tile<MODE, BM, NCOL, TM, TN, WTM, WTN, NT>(acc, ring, wm, wn, lane, tid, m0, rows_g,
-                                                     row_base, rows, C, ldc, n0);
   }
 }
 
@@ -1787,15 +1534,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 
 // Tile variant of the LDS-ring GEMMs, per pass, from the measured expert
-// shapes: gate/up takes the register-staged 256 x 256 x 64 kernel (8) when
-// the groups average at least 2048 rows (dense, shared-expert-like) and its
-// tiles fill the 256 compute units, and the interleaved 128 x 256 x 64 ring
-// (5) otherwise, where half-empty 256-row tail tiles would waste MFMA work
-// or too few tiles would leave CUs idle (narrow tensor-parallel slices);
-// down takes the interleaved 256 x 256 x 64 ring with eight waves (7) when
-// K < 2816, the groups average at least 2048 rows and its tiles fill the
-// 256 compute units, and the 128-row interleaved ring (5) otherwise.  nout: output
-// columns of the pass (F for gate/up, d for down).
+// shapes: gate/up always takes the interleaved 128 x 256 x 64 ring with
+// eight waves (5; on the dense Llama-4-Scout-shaped shared gate/up it beat
+// a register-staged 256 x 256 kernel, 1317 -> 1232 us, and 256-row tiles
+// would waste MFMA work on routed tail tiles); down takes the interleaved
+// 256 x 256 x 64 ring with eight waves (7) when K < 2816, the groups
+// average at least 2048 rows and its tiles fill the 256 compute units, and
+// the 128-row ring (5) otherwise.  nout: output columns of the pass (F for
+// gate/up, d for down).
 int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
   if (down) {
     if (nout % 256 != 0) return 10;   // the only down variant for such widths
@@ -1805,8 +1551,7 @@ int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
     // tile's first K blocks during the previous tile, is faster.
     return K < 2816 && max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
   }
-  const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 128);
-  return max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 8 : 5;
+  return 5;
 }
 
 int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
@@ -1847,45 +1592,37 @@ struct KSplit {
   float* P = nullptr;
 };
 
-template <int MODE, int BM, int BN, int BK, int ST, int OCC, int WGM = 2>
+template <int MODE, int BM, int BN, int BK, int ST, int OCC, int WGM = 2, int WGN = 2>
 void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s,
             const KSplit& sp = KSplit{}) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, OCC);
   if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM>, (unsigned)g,
-             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM, WGN>, (unsigned)g,
+             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
              sp.splits, sp.kps, sp.P);
   else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM>, (unsigned)g,
-             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM, WGN>, (unsigned)g,
+             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
              K / BK, nullptr);
 }
-template <int MODE, int BM, int BN, int ST, int WGM = 2>
+template <int MODE, int BM, int BN, int ST, int WGM = 2, int WGN = 2>
 void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
                const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc, const float* sA,
                const float* sB, hipStream_t s, const KSplit& sp) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, 1);
   if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, true, WGM>, (unsigned)g,
-             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, sp.splits,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, true, WGM, WGN>, (unsigned)g,
+             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, sp.splits,
              sp.kps, sp.P);
   else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, false, WGM>, (unsigned)g,
-             128 * WGM, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, 128, ST, 1, true, false, WGM, WGN>, (unsigned)g,
+             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128,
              nullptr);
 }
-template <int MODE, int BM, int BN, int BK>
-void run_rs(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
-            const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s) {
-  constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
-  const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL, 1);
-  launch_k(gemm_bf16_rs_kernel<MODE, BM, BN, BK>,
-      (unsigned)g, 256, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc);
-}
-// Variants 5, 7 and 8 have BN = 256 and BK = 64: they need NOUT % 128 == 0
+// Variants 5 and 7 have BN = 256 and BK = 64: they need NOUT % 128 == 0
 // for gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
 // only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to the
 // interleaved variant 5 only.)
@@ -1896,12 +1633,11 @@ void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff,
 #define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
   switch (v) {
     case 7: run_il<MODE, 256, 256, 64, 2, 1, 4>(FS_ARGS); break;
-    case 8: run_rs<MODE, 256, 256, 64>(FS_ARGS); break;
     case 10:
       // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
       if constexpr (MODE == MODE_DOWN) run_il<MODE, 128, 128, 64, 4, 1>(FS_ARGS);
       break;
-    default: run_il<MODE, 128, 256, 64, 3, 1>(FS_ARGS, sp); break;   // 5
+    default: run_il<MODE, 128, 256, 64, 3, 1, 2, 4>(FS_ARGS, sp); break;   // 5
   }
 #undef FS_ARGS
 }
@@ -1942,19 +1678,16 @@ bool use_stream(int dtype, int64_t max_rows, int G, int ffn, int d) {
   return ring_tiles < 256;
 }
 
-// One FP8 GEMM pass, 128 x 256 tiles except where the bf16 rule takes the
-// dense register-staged variant (8, gate/up over groups of at least 2048
-// rows that fill the CUs): there 256 x 256.  Measured on the routed and
-// dense expert shapes, 256-row FP8 tiles lose everywhere else (the routed
+// One FP8 GEMM pass on 128 x 256 tiles, eight waves of 64 x 64 (as bf16:
+// routed gate/up of the DeepSeek-V3-shaped prefill 1000 -> 955 us, down
+// 660 -> 616 us against four waves of 64 x 128).  Measured on the routed
+// and dense expert shapes, 256-row FP8 tiles lose everywhere (the routed
 // down pass of the 32-expert 7168-wide prefill: 817 against 760 us).
 template <int MODE>
-void gemm_pass_f8(int v, const uint8_t* A, const int32_t* rows, const int32_t* goff, int G,
+void gemm_pass_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G,
                   int64_t m_total, const uint8_t* B, int K, int NOUT, bf16_t* C, int ldc,
                   const float* sA, const float* sB, hipStream_t s, const KSplit& sp) {
-  if (v == 8)
-    run_il_f8<MODE, 256, 256, 2>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s, sp);
-  else
-    run_il_f8<MODE, 128, 256, 3>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s, sp);
+  run_il_f8<MODE, 128, 256, 3, 2, 4>(A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, s, sp);
 }
 
 // K slices for an interleaved-ring pass with fewer tiles (BM rows x 128
@@ -2028,10 +1761,9 @@ hipError_t launch_grouped_ffn_fp8(int G, int ffn, int d, const uint8_t* x, const
   bf16_t* Y = static_cast<bf16_t*>(out);
   if (profile) prof_begin(prof_gate_up, s);
   {
-    const int v = tile_choice(false, max_rows, G, d, ffn);
-    const KSplit sp = make_split(
-        ring_splits(true, v == 8 ? 256 : 128, max_rows, G, d / 128, ffn, pbytes), d / 128, P);
-    gemm_pass_f8<MODE_GATEUP>(v, x, rows_in, goff, G, max_rows, w_gate_up, d, ffn, H, ffn,
+    const KSplit sp =
+        make_split(ring_splits(true, 128, max_rows, G, d / 128, ffn, pbytes), d / 128, P);
+    gemm_pass_f8<MODE_GATEUP>(x, rows_in, goff, G, max_rows, w_gate_up, d, ffn, H, ffn,
                               x_scale, s_gate_up, s, sp);
     reduce_split<MODE_GATEUP>(sp, rows_in, goff, G, max_rows, ffn, H, ffn, s);
   }
@@ -2040,10 +1772,9 @@ hipError_t launch_grouped_ffn_fp8(int G, int ffn, int d, const uint8_t* x, const
   hipError_t e = launch_quantize_fp8(1, H, max_rows, ffn, goff ? goff + G : nullptr, Hq, Hs, s);
   if (e != hipSuccess) return e;
   {
-    const int v = tile_choice(true, max_rows, G, ffn, d);
     const KSplit sp = make_split(ring_splits(false, 128, max_rows, G, ffn / 128, d, pbytes),
                                  ffn / 128, P);
-    gemm_pass_f8<MODE_DOWN>(v, Hq, rows_out, goff, G, max_rows, w_down, ffn, d, Y, d, Hs, s_down,
+    gemm_pass_f8<MODE_DOWN>(Hq, rows_out, goff, G, max_rows, w_down, ffn, d, Y, d, Hs, s_down,
                             s, sp);
     reduce_split<MODE_DOWN>(sp, rows_out, goff, G, max_rows, d, Y, d, s);
   }

@@ -85,11 +85,10 @@ def ffn_case(G, F, d, counts, gather, seed):
     return x, wgu, wdn, goff, rows, M
 
 
-# [2304] is one dense group whose 256-row tiles fill the CUs: its gate/up
-# pass takes the 256 x 256 FP8 tiles, every other pass 128 x 256; the last
-# case but one has few tiles and long K, so both passes split K; the last
-# has more tiles than workgroups with two-block K rings (the ring runs on
-# from tile to tile)
+# Every pass runs on 128 x 256 FP8 tiles (eight waves); [2304] is one dense
+# group that fills the CUs; the last case but one has few tiles and long
+# K, so both passes split K; the last has more tiles than workgroups with
+# two-block K rings (the ring runs on from tile to tile)
 FFN_CASES = [([0, 1, 64, 65, 130], 256, 512, True),
              ([37], 128, 256, False),
              ([3, 0, 5, 300, 1, 0, 2, 7], 384, 768, True),
