@@ -6,11 +6,11 @@
 //             the SwiGLU runs in the epilogue; H is stored in the element type)
 //   down:     Y[row_i] = H[i] . Wd^T                        (rows scattered
 //             through group_rows)
-// bf16 runs on MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) with both
-// operand tiles staged through a ring of LDS slots by direct global->LDS
-// copies; few-row passes stream the weights straight into registers.  The
-// launcher picks the tile variant per pass from the shape.  fp32 runs on
-// the vector ALUs.
+// bf16 runs on MFMA (v_mfma_f32_16x16x32_bf16 or _32x32x16_bf16, fp32
+// accumulation) with both operand tiles staged through a ring of LDS slots
+// by direct global->LDS copies; few-row passes stream the weights straight
+// into registers.  The launcher picks the tile variant per pass from the
+// shape.  fp32 runs on the vector ALUs.
 //
 // Groups have ragged row counts known only on the device.  Every workgroup
 // rebuilds the per-group m-tile prefix from group_offsets in LDS, then walks
@@ -387,6 +387,17 @@ __device__ __forceinline__ void barrier_nofence() {
 // 128 x 128 need all 512 registers and spill (72 bytes per lane), for the
 // same time (DeepSeek-V3-shaped shared down pass, 4096 x 7168, K 2048:
 // 134-140 against 133-137 us).
+//
+// M16 (bf16): 16 x 16 fragments on v_mfma_f32_16x16x32_bf16 (lane l: row
+// l % 16, k 8 (l / 16) .. + 7 of a 32-wide step; accumulator element v of
+// lane l: row 4 (l / 16) + v, column l % 16), two K steps per 64-wide
+// block, the same bytes per MFMA cycle from LDS.  The smaller MFMA runs at
+// a higher clock under the part's power limit: with eight waves of 64 x 64
+// on the 128 x 256 tile, Llama-4-Scout-shaped block step 4.34 -> 4.16 ms
+// (routed gate/up 1458 -> 1415 us, dense shared gate/up 1266 -> 1210 us),
+// DeepSeek-V3-shaped prefill 3.92 -> 3.83 ms, DeepSeek-V2-Lite-shaped
+// 0.925 -> 0.893 ms (same-box A/B).  (With four waves of 64 x 128 it had
+// been slower on every pass.)
 
 __device__ __forceinline__ void wait_lgkm0() {
   // lgkmcnt(0), vmcnt and expcnt unconstrained
@@ -396,7 +407,7 @@ __device__ __forceinline__ void wait_lgkm0() {
 typedef int int32x8 __attribute__((ext_vector_type(8)));
 
 template <int MODE, int BM, int BN, int BK, int STAGES, int OCC, bool F8 = false, bool SPL = false,
-          int WGM = 2, int WGN = 2>
+          int WGM = 2, int WGN = 2, bool M16 = false>
 __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     const typename std::conditional<F8, uint8_t, bf16_t>::type* __restrict__ A,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ goff, int G, int64_t m_total,
@@ -407,7 +418,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   using FragT = typename std::conditional<F8, int32x8, bf16x8>::type;
   constexpr int NT = 64 * WGM * WGN;               // WGM x WGN waves
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
+  static_assert(!(F8 && M16), "16 x 16 fragments for bf16 only");
+  constexpr int FR = M16 ? 16 : 32;                // fragment rows
+  constexpr int TM = WTM / FR, TN = WTN / FR;      // fragments per wave tile
+  constexpr int TU = WTM / 32;                     // 32-row accumulator units
+  constexpr int BPU = 32 / FR;                     // fragments per unit
+  constexpr int AV = M16 ? 4 : 16;                 // accumulator elements
+  using AccT = typename std::conditional<M16, floatx4, floatx16>::type;
   constexpr int ES = F8 ? 1 : 2;                   // element bytes
   constexpr int CE = 16 / ES;                      // elements per 16-byte chunk
   constexpr int ROWB = BK * ES;
@@ -419,7 +436,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   constexpr int NLD = A_LD + B_LD;
   constexpr int NCOL = (MODE == MODE_GATEUP) ? BN / 2 : BN;
   constexpr int SST = NCOL + 8;                    // staged row, bf16 elements
-  constexpr int KS = ROWB / (F8 ? 64 : 32);        // K steps per block
+  constexpr int KS = ROWB / (F8 || M16 ? 64 : 32); // K steps per block
   constexpr int NF = TM + TN;                      // fragments per K step
   constexpr int MPS = TM * TN;                     // MFMAs per K step
   // read r of the next step goes out after MFMA read_slot(r) of this one
@@ -445,8 +462,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   // epilogue pass; SROWS: staged rows per pass.
   constexpr bool XTC = !SPL && BM == 128 && WGM == 2;
   constexpr int SCAP = XTC ? STAGE : STAGES * STAGE;
-  constexpr int IPP = (TM % 4 == 0 && WGM * 128 * SST * 2 <= SCAP)  ? 4
-                      : (TM % 2 == 0 && WGM * 64 * SST * 2 <= SCAP) ? 2
+  constexpr int IPP = (TU % 4 == 0 && WGM * 128 * SST * 2 <= SCAP)  ? 4
+                      : (TU % 2 == 0 && WGM * 64 * SST * 2 <= SCAP) ? 2
                                                                     : 1;
   constexpr int SROWS = WGM * 32 * IPP;
   constexpr bool XT = XTC && SROWS * SST * 2 <= STAGE;
@@ -480,7 +497,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   int aoff[TM], boff[TN], asw[TM], bsw[TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int r = wm * WTM + i * 32 + (lane & 31);
+    const int r = wm * WTM + i * FR + (lane & (FR - 1));
     aoff[i] = r * ROWB;
     asw[i] = (r / SWD) % CPR;
   }
@@ -488,10 +505,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   for (int jn = 0; jn < TN; ++jn) {
     int r;
     if (MODE == MODE_GATEUP)
-      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * 32 : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+      r = (jn < TN / 2) ? wn * (WTN / 2) + jn * FR : BN / 2 + wn * (WTN / 2) + (jn - TN / 2) * FR;
     else
-      r = wn * WTN + jn * 32;
-    r += lane & 31;
+      r = wn * WTN + jn * FR;
+    r += lane & (FR - 1);
     boff[jn] = BM * ROWB + r * ROWB;
     bsw[jn] = (r / SWD) % CPR;
   }
@@ -595,13 +612,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
       dma16_at(srcN[i] + (b - KT) * BK, ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i));
     };
 
-    floatx16 acc[TM][TN];
+    AccT acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int jn = 0; jn < TN; ++jn)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][jn][v] = 0.f;
+        for (int v = 0; v < AV; ++v) acc[i][jn][v] = 0.f;
 
     FragT Fa[NF], Fb[NF];
     // fragment r of a step in the order its MFMAs use them: A0, B0..B(TN-1),
@@ -617,7 +634,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
         const int4 hi = *reinterpret_cast<const int4*>(slot + base + (((c + 1) ^ sw) << 4));
         F[f] = int32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
       } else {
-        const int c = ks * 2 + (lane >> 5);
+        const int c = M16 ? ks * 4 + (lane >> 4) : ks * 2 + (lane >> 5);
         const int off = f < TM ? aoff[f] + ((c ^ asw[f]) << 4) : boff[f - TM] + ((c ^ bsw[f - TM]) << 4);
         F[f] = *reinterpret_cast<const bf16x8*>(slot + off);
       }
@@ -644,6 +661,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
         if constexpr (F8)
           acc[i][jn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Fc[i], Fc[TM + jn], acc[i][jn],
                                                                        0, 0, 0, 127, 0, 127);
+        else if constexpr (M16)
+          acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
         else
           acc[i][jn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Fc[i], Fc[TM + jn], acc[i][jn], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
@@ -746,8 +765,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        for (int v = 0; v < AV; ++v) {
+          const int r = wm * WTM + i * FR +
+                        (M16 ? 4 * (lane >> 4) + v : 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3));
           if (m0 + r >= rows_g) continue;
           const float sa = F8 ? s_sa[r] : 1.f;
           float* prow = Ps + (size_t)(row_base + m0 + r) * W;
@@ -755,13 +775,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
           for (int jn = 0; jn < TN; ++jn) {
             int col;
             if (MODE == MODE_GATEUP)
-              col = (jn < TN / 2) ? n0 + wn * (WTN / 2) + jn * 32
-                                  : NOUT + n0 + wn * (WTN / 2) + (jn - TN / 2) * 32;
+              col = (jn < TN / 2) ? n0 + wn * (WTN / 2) + jn * FR
+                                  : NOUT + n0 + wn * (WTN / 2) + (jn - TN / 2) * FR;
             else
-              col = n0 + wn * WTN + jn * 32;
+              col = n0 + wn * WTN + jn * FR;
             float y = acc[i][jn][v];
             if constexpr (F8) y = y * sa * sbg[jn];
-            prow[col + (lane & 31)] = y;
+            prow[col + (lane & (FR - 1))] = y;
           }
         }
       // the next tile's prologue refills ring slots that slower waves may
@@ -773,35 +793,39 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     // staged rows [wm IPP 32, (wm + 1) IPP 32)
     bf16_t* Cs = reinterpret_cast<bf16_t*>(ring + (XT ? slot_of(KT - 1) * STAGE : 0));
 #pragma unroll
-    for (int p = 0; p < TM / IPP; ++p) {
+    for (int p = 0; p < TU / IPP; ++p) {
       __syncthreads();
 #pragma unroll
       for (int ii = 0; ii < IPP; ++ii) {
-        const int i = p * IPP + ii;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int rr = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          const int r = wm * WTM + i * 32 + rr;               // tile row
-          const int sr = wm * (IPP * 32) + ii * 32 + rr;      // staged row
-          const float sa = F8 ? s_sa[r] : 1.f;
-          if (MODE == MODE_GATEUP) {
+        for (int sb = 0; sb < BPU; ++sb) {
+          const int i = (p * IPP + ii) * BPU + sb;
 #pragma unroll
-            for (int jn = 0; jn < TN / 2; ++jn) {
-              float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
-              if constexpr (F8) {
-                gt = gt * sa * sbg[jn];
-                up = up * sa * sbg[jn + TN / 2];
+          for (int v = 0; v < AV; ++v) {
+            const int rr = M16 ? sb * 16 + 4 * (lane >> 4) + v
+                               : 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const int r = wm * WTM + (p * IPP + ii) * 32 + rr;   // tile row
+            const int sr = wm * (IPP * 32) + ii * 32 + rr;      // staged row
+            const float sa = F8 ? s_sa[r] : 1.f;
+            if (MODE == MODE_GATEUP) {
+#pragma unroll
+              for (int jn = 0; jn < TN / 2; ++jn) {
+                float gt = acc[i][jn][v], up = acc[i][jn + TN / 2][v];
+                if constexpr (F8) {
+                  gt = gt * sa * sbg[jn];
+                  up = up * sa * sbg[jn + TN / 2];
+                }
+                const int col = wn * (WTN / 2) + jn * FR + (lane & (FR - 1));
+                Cs[sr * SST + col] = f2bf(swiglu_bf16_epi(gt, up));
               }
-              const int col = wn * (WTN / 2) + jn * 32 + (lane & 31);
-              Cs[sr * SST + col] = f2bf(swiglu_bf16_epi(gt, up));
-            }
-          } else {
+            } else {
 #pragma unroll
-            for (int jn = 0; jn < TN; ++jn) {
-              const int col = wn * WTN + jn * 32 + (lane & 31);
-              float y = acc[i][jn][v];
-              if constexpr (F8) y = y * sa * sbg[jn];
-              Cs[sr * SST + col] = f2bf(y);
+              for (int jn = 0; jn < TN; ++jn) {
+                const int col = wn * WTN + jn * FR + (lane & (FR - 1));
+                float y = acc[i][jn][v];
+                if constexpr (F8) y = y * sa * sbg[jn];
+                Cs[sr * SST + col] = f2bf(y);
+              }
             }
           }
         }
@@ -1592,18 +1616,19 @@ struct KSplit {
   float* P = nullptr;
 };
 
-template <int MODE, int BM, int BN, int BK, int ST, int OCC, int WGM = 2, int WGN = 2>
+template <int MODE, int BM, int BN, int BK, int ST, int OCC, int WGM = 2, int WGN = 2,
+          bool M16 = false>
 void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
             const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc, hipStream_t s,
             const KSplit& sp = KSplit{}) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, OCC);
   if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM, WGN>, (unsigned)g,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM, WGN, M16>, (unsigned)g,
              64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
              sp.splits, sp.kps, sp.P);
   else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM, WGN>, (unsigned)g,
+    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM, WGN, M16>, (unsigned)g,
              64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
              K / BK, nullptr);
 }
@@ -1637,7 +1662,7 @@ void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff,
       // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
       if constexpr (MODE == MODE_DOWN) run_il<MODE, 128, 128, 64, 4, 1>(FS_ARGS);
       break;
-    default: run_il<MODE, 128, 256, 64, 3, 1, 2, 4>(FS_ARGS, sp); break;   // 5
+    default: run_il<MODE, 128, 256, 64, 3, 1, 2, 4, true>(FS_ARGS, sp); break;   // 5
   }
 #undef FS_ARGS
 }
