@@ -383,10 +383,7 @@ __device__ __forceinline__ void barrier_nofence() {
 // MFMA pipe is busy 55%.  The 128 x 256 tile runs 2 x 4 waves of 64 x 64
 // (routed gate/up 1493 -> 1432 us Scout-shaped, 377 -> 362 us
 // DeepSeek-V2-Lite-shaped; DeepSeek-V3-shaped down 1073 -> 997 us; alone
-// on the GPU), the 256 x 256 tile 4 x 2 waves of 64 x 128: four waves of
-// 128 x 128 need all 512 registers and spill (72 bytes per lane), for the
-// same time (DeepSeek-V3-shaped shared down pass, 4096 x 7168, K 2048:
-// 134-140 against 133-137 us).
+// on the GPU).
 //
 // M16 (bf16): 16 x 16 fragments on v_mfma_f32_16x16x32_bf16 (lane l: row
 // l % 16, k 8 (l / 16) .. + 7 of a 32-wide step; accumulator element v of
@@ -1557,24 +1554,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 
-// Tile variant of the LDS-ring GEMMs, per pass, from the measured expert
-// shapes: gate/up always takes the interleaved 128 x 256 x 64 ring with
-// eight waves (5; on the dense Llama-4-Scout-shaped shared gate/up it beat
-// a register-staged 256 x 256 kernel, 1317 -> 1232 us, and 256-row tiles
-// would waste MFMA work on routed tail tiles); down takes the interleaved
-// 256 x 256 x 64 ring with eight waves (7) when K < 2816, the groups
-// average at least 2048 rows and its tiles fill the 256 compute units, and
-// the 128-row ring (5) otherwise.  nout: output columns of the pass (F for
-// gate/up, d for down).
-int tile_choice(bool down, int64_t max_rows, int G, int K, int nout) {
-  if (down) {
-    if (nout % 256 != 0) return 10;   // the only down variant for such widths
-    const int64_t tiles256 = cdiv64(max_rows, 256) * (nout / 256);
-    // 256-row tiles only for long groups (a dense shared expert): on routed
-    // groups of about a thousand rows the 128-row kernel, which primes each
-    // tile's first K blocks during the previous tile, is faster.
-    return K < 2816 && max_rows >= 2048 * (int64_t)G && tiles256 >= 256 ? 7 : 5;
-  }
+// Tile variant of the LDS-ring GEMMs, per pass: the interleaved 128 x 256
+// x 64 ring with eight waves (5) for every shape, except down passes whose
+// output width is a multiple of 128 but not of 256 (10: 128 x 128 tiles).
+// Measured against it and dropped: a register-staged 256 x 256 kernel on
+// dense gate/up (Llama-4-Scout-shaped shared expert 1317 -> 1232 us for the
+// ring), 256 x 256 tiles of eight waves on dense short-K down passes
+// (DeepSeek-V3-shaped shared down, 133 us either way), and 256-row tiles on
+// routed passes, whose half-empty tail tiles waste MFMA work.  nout: output
+// columns of the pass (F for gate/up, d for down).
+int tile_choice(bool down, int nout) {
+  if (down && nout % 256 != 0) return 10;   // the only down variant for such widths
   return 5;
 }
 
@@ -1647,8 +1637,8 @@ void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G
              64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, sA, sB, 1, K / 128,
              nullptr);
 }
-// Variants 5 and 7 have BN = 256 and BK = 64: they need NOUT % 128 == 0
-// for gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
+// Variant 5 has BN = 256 and BK = 64: it needs NOUT % 128 == 0 for
+// gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
 // only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to the
 // interleaved variant 5 only.)
 template <int MODE>
@@ -1657,7 +1647,6 @@ void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff,
                hipStream_t s, const KSplit& sp = KSplit{}) {
 #define FS_ARGS A, rows, goff, G, m_total, B, K, NOUT, C, ldc, s
   switch (v) {
-    case 7: run_il<MODE, 256, 256, 64, 2, 1, 4>(FS_ARGS); break;
     case 10:
       // 128 x 128 tiles, four waves of 64 x 64, four 32 KB slots
       if constexpr (MODE == MODE_DOWN) run_il<MODE, 128, 128, 64, 4, 1>(FS_ARGS);
@@ -1881,7 +1870,7 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
     };
     if (profile) prof_begin(pg, s);
     {
-      const int v = tile_choice(false, max_rows, G, d, ffn);
+      const int v = tile_choice(false, ffn);
       const KSplit sp = split_of(v, true, d, ffn);
       gemm_pass<MODE_GATEUP>(v, (const bf16_t*)in, rows_in, goff, G, max_rows,
                              (const bf16_t*)w_gate_up, d, ffn, H, ffn, s, sp);
@@ -1890,7 +1879,7 @@ hipError_t launch_grouped_ffn(int dtype, int G, int ffn, int d, const void* in,
     if (profile) prof_end(pg, s);
     if (profile) prof_begin(pd, s);
     {
-      const int v = tile_choice(true, max_rows, G, ffn, d);
+      const int v = tile_choice(true, d);
       const KSplit sp = split_of(v, false, ffn, d);
       gemm_pass<MODE_DOWN>(v, H, rows_out, goff, G, max_rows, (const bf16_t*)w_down, ffn, d,
                            (bf16_t*)out, d, s, sp);
@@ -2009,7 +1998,7 @@ hipError_t launch_dense_linear(int dtype, int m, int n, int kdim, const void* a,
   if (dtype == 1 && n % 128 == 0) {
     // the LDS-ring kernels as one group of m rows (128 x 128 tiles when n is
     // not a multiple of 256)
-    gemm_pass<MODE_DOWN>(tile_choice(true, m, 1, kdim, n), (const bf16_t*)a, nullptr, nullptr, 1,
+    gemm_pass<MODE_DOWN>(tile_choice(true, n), (const bf16_t*)a, nullptr, nullptr, 1,
                          m, (const bf16_t*)w, kdim, n, (bf16_t*)out, n, s);
   } else if (dtype == 1) {
     const int64_t g = grid_for(m, 1, kBM, n / kBN);

@@ -262,11 +262,11 @@ def test_grouped_ffn_many_tiles(counts, d, F, gather):
 
 
 def test_grouped_ffn_wide_tiles():
-    """Two long groups (4100 and 2050 rows, both ragged at 256) with a short
-    K: the down pass takes the eight-wave 256 x 256 tiles ((17 + 9) x 16 =
-    416 tiles), gate/up the 128-row ring; sampled rows of each group (the first
-    64, 64 from the middle, the last 300: its ragged tiles) against the
-    oracle element by element."""
+    """Two long groups (4100 and 2050 rows, both ragged) of a dense-shaped
+    pass with a short down K and a 4096-wide output (the shape of a
+    prefill's shared expert); sampled rows of each group (the first 64, 64
+    from the middle, the last 300: its ragged tiles) against the oracle
+    element by element."""
     counts = np.array([4100, 2050])
     d, F = 4096, 256
     G, M = len(counts), int(counts.sum())
