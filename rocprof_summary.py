@@ -38,6 +38,11 @@ whose short name contains SUBSTRING: bench.py runs warm-up steps, the timed
 steps and then an untimed pass with every kernel's events on, so the timed
 steps' launches are a window of the trace.
 
+With --split SUBSTRING N, the launches of a kernel whose short name
+contains SUBSTRING are told apart by their launch index modulo N (shown as
+"name #i"): one step may launch the same kernel for two passes, e.g. the
+shared and then the routed gate/up.
+
 With --traffic-json, the calibrated HBM bytes per launch (FETCH + WRITE) of
 the one kernel whose short name contains --kernel are written to OUT, with
 the sha256 of the kernel's source file, so that a reader of OUT can tell
@@ -57,7 +62,28 @@ import re
 def short(name):
     name = name.replace("(anonymous namespace)::", "").replace("void ", "")
     name = re.sub(r"\(.*", "", name)
-    return name.replace("fs::", "").replace("at::native::", "torch:")[:60]
+    return name.replace("fs::", "").replace("at::native::", "torch:")[:90]
+
+
+# --split SUBSTRING N: launches of a kernel whose short name contains
+# SUBSTRING are told apart by their index in launch order modulo N (a pass
+# that two calls of one step make with the same kernel, e.g. the shared and
+# the routed gate/up), shown as "name #i".
+SPLIT = None
+
+
+def named(rows, order_field):
+    """(short name with the --split class, row) in the rows' launch order."""
+    out, seen = [], collections.Counter()
+    # (files without the field keep their own order: the sort is stable)
+    for r in sorted(rows, key=lambda r: int(r.get(order_field) or 0)):
+        k = short(r["Kernel_Name"])
+        if SPLIT and SPLIT[0] in k:
+            i = seen[k]
+            seen[k] += 1
+            k = f"{k} #{i % SPLIT[1]}"
+        out.append((k, r))
+    return out
 
 
 def one(pattern):
@@ -70,20 +96,20 @@ def one(pattern):
 def trace_table(trace_dir):
     rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
     agg = collections.defaultdict(list)
-    for r in rows:
-        key = (short(r["Kernel_Name"]), int(r["Grid_Size_X"]))
+    for k, r in named(rows, "Start_Timestamp"):
+        key = (k, int(r["Grid_Size_X"]))
         agg[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     return agg
 
 
 def window_report(trace_dir, substring, start, count):
-    rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
-    names = {short(r["Kernel_Name"]) for r in rows if substring in short(r["Kernel_Name"])}
+    rows = named(list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv"))))),
+                 "Start_Timestamp")
+    names = {k for k, _ in rows if substring in k}
     if len(names) != 1:
         raise SystemExit(f"--window: {substring!r} matches {sorted(names)}")
     name, = names
-    sel = sorted((r for r in rows if short(r["Kernel_Name"]) == name),
-                 key=lambda r: int(r["Start_Timestamp"]))[start:start + count]
+    sel = [r for k, r in rows if k == name][start:start + count]
     if len(sel) != count:
         raise SystemExit(f"--window: {name} has {len(sel)} launches in [{start}, {start + count})")
     d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel]
@@ -183,9 +209,8 @@ def memory_report(trace_dir, pmc_dirs, min_us):
 def counter_table(pmc_dir, counter):
     rows = list(csv.DictReader(open(one(os.path.join(pmc_dir, "*_counter_collection.csv")))))
     agg = collections.defaultdict(list)
-    for r in rows:
-        if r["Counter_Name"] == counter:
-            agg[(short(r["Kernel_Name"]), int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+    for k, r in named([r for r in rows if r["Counter_Name"] == counter], "Dispatch_Id"):
+        agg[(k, int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
     return agg
 
 
@@ -211,9 +236,14 @@ def main():
     ap.add_argument("--tile", default="")
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--window", nargs=3, metavar=("SUBSTRING", "START", "COUNT"))
+    ap.add_argument("--split", nargs=2, metavar=("SUBSTRING", "N"),
+                    help="tell a kernel's launches apart by launch index modulo N")
     ap.add_argument("--all-kernels", action="store_true",
                     help="also list torch's kernels (input generation during setup)")
     a = ap.parse_args()
+    global SPLIT
+    if a.split:
+        SPLIT = (a.split[0], int(a.split[1]))
     keep = (lambda k: True) if a.all_kernels else (lambda k: not k.startswith("torch:"))
     scales, kib = {}, {}
     if a.overlap:

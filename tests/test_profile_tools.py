@@ -90,3 +90,32 @@ def test_launch_window(tmp_path):
     r = subprocess.run([sys.executable, TOOL, str(tmp_path), "--window", "gemm<0>", "3", "5"],
                        capture_output=True, text=True)
     assert r.returncode != 0 and "has 2 launches" in r.stderr
+
+
+def test_split_launch_classes(tmp_path):
+    # one kernel launched twice per step, a short pass (10 us) then a long
+    # one (40 us), written out of order; --split tells them apart by launch
+    # index modulo 2 in the trace, and in a counter run by dispatch order
+    us = 1000
+    rows = []
+    for step in range(3):
+        t = step * 1000 * us
+        rows.append((0, "void fs::gemm<0>(int)", t + 500 * us, t + 540 * us, 65536))
+        rows.append((0, "void fs::gemm<0>(int)", t, t + 10 * us, 65536))
+    write_trace(str(tmp_path / "trace"), rows)
+    out = run(str(tmp_path / "trace"), "--split", "gemm<0>", "2", "--window", "gemm<0> #1", "0", "3")
+    assert "| gemm<0> #0 | 65536 | 3 | 10.00 | 10.00 | 10.00 |" in out
+    assert "| gemm<0> #1 | 65536 | 3 | 40.00 | 40.00 | 40.00 |" in out
+    assert "gemm<0> #1: launches 0..2 (start order) average 40.00 us" in out
+    d = str(tmp_path / "fetch")
+    os.makedirs(d)
+    with open(os.path.join(d, "x_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name",
+                                          "Counter_Value"])
+        w.writeheader()
+        for i, kib in ((4, 700), (1, 100), (3, 100), (2, 700)):
+            w.writerow({"Dispatch_Id": i, "Kernel_Name": "void fs::gemm<0>(int)", "Grid_Size": 65536,
+                        "Counter_Name": "FETCH_SIZE", "Counter_Value": kib})
+    out = run(str(tmp_path / "trace"), "--split", "gemm<0>", "2", "--fetch", d)
+    assert "| gemm<0> #0 | 65536 | 2 | 100 | - |" in out
+    assert "| gemm<0> #1 | 65536 | 2 | 700 | - |" in out
