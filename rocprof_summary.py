@@ -118,12 +118,14 @@ def window_report(trace_dir, substring, start, count):
           f"{sum(d) / len(d):.2f} us (min {min(d):.2f}, max {max(d):.2f})")
 
 
-def overlap_report(trace_dir, min_us, skip, copy_kernel="copyBuffer"):
+def overlap_report(trace_dir, min_us, skip, copy_kernel="copyBuffer", copy_stream=None):
     rows = list(csv.DictReader(open(one(os.path.join(trace_dir, "*_kernel_trace.csv")))))
     span = lambda r: (int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
     copies = [r for r in rows if copy_kernel in r["Kernel_Name"]]
     longest = max(span(r)[1] - span(r)[0] for r in copies)
     streams = {r["Stream_Id"] for r in copies if span(r)[1] - span(r)[0] >= 0.5 * longest}
+    if copy_stream is not None:
+        streams = {copy_stream}
     if len(streams) != 1:
         raise SystemExit(f"the largest copies run on several streams: {sorted(streams)}")
     cs = streams.pop()
@@ -226,6 +228,10 @@ def main():
     ap.add_argument("--copy-kernel", default="copyBuffer",
                     help="--overlap: kernel-name substring of the copies (paced_copy: the "
                          "link-paced stand-in copies)")
+    ap.add_argument("--copy-stream", default=None,
+                    help="--overlap: the stream of the copies to report (when copies of both "
+                         "schedules are long, e.g. link-paced copies of the regular schedule "
+                         "on the compute stream)")
     ap.add_argument("--mfma")
     ap.add_argument("--memory", action="append", default=[],
                     help="counter-run directories for the GEMM memory-pipeline table")
@@ -247,7 +253,7 @@ def main():
     keep = (lambda k: True) if a.all_kernels else (lambda k: not k.startswith("torch:"))
     scales, kib = {}, {}
     if a.overlap:
-        overlap_report(a.trace_dir, a.min_us, a.skip, a.copy_kernel)
+        overlap_report(a.trace_dir, a.min_us, a.skip, a.copy_kernel, a.copy_stream)
         return
     if a.mfma:
         mfma_report(a.trace_dir, a.mfma, a.min_us)

@@ -119,3 +119,21 @@ def test_split_launch_classes(tmp_path):
     out = run(str(tmp_path / "trace"), "--split", "gemm<0>", "2", "--fetch", d)
     assert "| gemm<0> #0 | 65536 | 2 | 100 | - |" in out
     assert "| gemm<0> #1 | 65536 | 2 | 700 | - |" in out
+
+
+def test_overlap_copy_stream(tmp_path):
+    # long copies on both streams (the regular schedule's on the compute
+    # stream 0, later in time): without --copy-stream the tool refuses;
+    # with it, only stream 1's copy is reported and stream 0's is compute
+    us = 1000
+    write_trace(str(tmp_path), [
+        (1, "paced_copy_kernel<uint4>", 0, 80 * us, 32768),
+        (0, "void fs::gemm<0>(int)", 0, 60 * us, 65536),
+        (0, "paced_copy_kernel<uint4>", 1000 * us, 1080 * us, 32768),
+    ])
+    r = subprocess.run([sys.executable, TOOL, str(tmp_path), "--overlap", "--copy-kernel", "paced_copy"],
+                       capture_output=True, text=True)
+    assert r.returncode != 0 and "several streams" in r.stderr
+    out = run(str(tmp_path), "--overlap", "--copy-kernel", "paced_copy", "--copy-stream", "1")
+    assert "copy stream 1: 1 copies" in out
+    assert "| 1 | 80.0 | 75.0% | 75.0% | 75.0% | 20.0 |" in out
