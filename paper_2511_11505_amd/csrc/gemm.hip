@@ -312,6 +312,26 @@ __device__ __forceinline__ void dma16_at(const void* g, unsigned lds) {
                : "memory");
 }
 
+// The same with the global address split into a wave-uniform 64-bit base
+// (SGPRs) and a 32-bit per-lane byte offset: the weight rows of a wave's DMAs
+// share one base, so they hold two VGPRs of offsets instead of a 64-bit
+// pointer per DMA.
+__device__ __forceinline__ void dma16_sb(const void* base, unsigned off, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds), "v"(off), "s"(base)
+               : "memory");
+}
+
+// A pointer made wave-uniform (held in SGPRs): lane 0's value.
+template <typename T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (T*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
 // LDS address of a __shared__ location as a wave-uniform 32-bit value.
 __device__ __forceinline__ unsigned lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(const lds_void_t*)p);
@@ -516,7 +536,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   };
   const int wave_s = XT ? __builtin_amdgcn_readfirstlane(wave) : wave;
   int ghint = 0;   // group of the previous item: a lower bound for the next
-  auto decode = [&](int64_t L, Item& it, const TE* (&sp)[NLD]) {
+  // B DMA i of a wave (block wave * B_LD + i of the tile's B rows) reads
+  // base + i RPB K + the lane's offset; the chunk swizzle repeats every two
+  // blocks, so two lane offsets serve all of them
+  static_assert((2 * (RPB / SWD)) % CPR == 0, "B swizzle period of two blocks");
+  unsigned bdl[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    bdl[j] = (unsigned)((drow * K + dchunk(wave * B_LD + j) * CE) * ES);
+  auto decode = [&](int64_t L, Item& it, const TE* (&sp)[A_LD], const TE*& bsp) {
     const int64_t Lt = SPL ? L / nspl : L;
     it.ksl = SPL ? (int)(L - Lt * nspl) : 0;
     it.kbase = it.ksl * kpsv;
@@ -557,17 +585,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
       }
       sp[i] = A + sr * K + (size_t)it.kbase * BK + dchunk(blk) * CE;
     }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int blk = wave_s * B_LD + i;
-      const int r = blk * RPB + drow;
-      int wrow;
-      if (MODE == MODE_GATEUP)
-        wrow = (r < BN / 2) ? it.n0 + r : NOUT + it.n0 + (r - BN / 2);
-      else
-        wrow = it.n0 + r;
-      sp[A_LD + i] = Bg + (size_t)wrow * K + (size_t)it.kbase * BK + dchunk(blk) * CE;
-    }
+    // the wave's B rows lie in one half (gate or up) of the tile's B rows
+    const int r0 = wave * B_LD * RPB;
+    const int wrow0 = (MODE == MODE_GATEUP && r0 >= BN / 2) ? NOUT + it.n0 + (r0 - BN / 2) : it.n0 + r0;
+    bsp = uniform_ptr(Bg + (size_t)wrow0 * K + (size_t)it.kbase * BK);
   };
 
   // wave-uniform LDS destinations: ring base + slot + this wave's blocks
@@ -580,8 +601,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
   const bool xt_ok = XT && KT_all >= STAGES - 1;
   int sb = 0;            // ring slot of the current item's block 0
   bool primed = false;   // its first STAGES - 1 blocks are already in flight
-  const TE* src[NLD];
-  const TE* srcN[NLD];
+  static_assert(MODE != MODE_GATEUP || (BN / 2) % (B_LD * RPB) == 0, "a wave's B rows in one half");
+  const TE* src[A_LD];
+  const TE* srcN[A_LD];
+  const TE* bsrc = nullptr;    // wave-uniform B row base of the current item
+  const TE* bsrcN = nullptr;   // and of the next
   Item itN;              // the next item, decoded during this one's last blocks
 
   for (int64_t j = blockIdx.x / kXcd; j < per_xcd; j += stride) {
@@ -591,9 +615,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     if (XT && primed) {
       it = itN;
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) src[i] = srcN[i];
+      for (int i = 0; i < A_LD; ++i) src[i] = srcN[i];
+      bsrc = bsrcN;
     } else {
-      decode(L, it, src);
+      decode(L, it, src, bsrc);
     }
     const int KT = it.KT, m0 = it.m0, n0 = it.n0, row_base = it.row_base, rows_g = it.rows_g;
     const int g = it.g, ksl = it.ksl;
@@ -603,10 +628,18 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     auto slot_of = [&](int b) { return (unsigned)((sb + b) % STAGES); };
     // DMA i of block b: b < KT from this item, b >= KT block b - KT of the next
     auto dma_cur = [&](int i, int b) {
-      dma16_at(src[i] + b * BK, ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i));
+      const unsigned lds = ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i);
+      if (i < A_LD)
+        dma16_at(src[i] + b * BK, lds);
+      else
+        dma16_sb(bsrc + (size_t)b * BK + (size_t)(i - A_LD) * RPB * K, bdl[(i - A_LD) & 1], lds);
     };
     auto dma_nxt = [&](int i, int b) {
-      dma16_at(srcN[i] + (b - KT) * BK, ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i));
+      const unsigned lds = ring_lds + slot_of(b) * (unsigned)STAGE + dst_of(i);
+      if (i < A_LD)
+        dma16_at(srcN[i] + (b - KT) * BK, lds);
+      else
+        dma16_sb(bsrcN + (size_t)(b - KT) * BK + (size_t)(i - A_LD) * RPB * K, bdl[(i - A_LD) & 1], lds);
     };
 
     AccT acc[TM][TN];
@@ -727,7 +760,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_il_kernel(
     };
     const int kt_pf = KT - (STAGES - 1);   // blocks that prefetch from this item
     for (int kt = 0; kt < kt_pf; ++kt) run_block(kt, std::integral_constant<int, 1>{});
-    if (has_next) decode(xcd_base + jnext, itN, srcN);
+    if (has_next) decode(xcd_base + jnext, itN, srcN, bsrcN);
     for (int kt = kt_pf < 0 ? 0 : kt_pf; kt < KT; ++kt)
       run_block(kt, std::integral_constant<int, 2>{});
 
@@ -1554,20 +1587,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 
-// Tile variant of the LDS-ring GEMMs, per pass: the interleaved 128 x 256
-// x 64 ring with eight waves (5) for every shape, except down passes whose
-// output width is a multiple of 128 but not of 256 (10: 128 x 128 tiles).
-// Measured against it and dropped: a register-staged 256 x 256 kernel on
-// dense gate/up (Llama-4-Scout-shaped shared expert 1317 -> 1232 us for the
-// ring), 256 x 256 tiles of eight waves on dense short-K down passes
-// (DeepSeek-V3-shaped shared down, 133 us either way), and 256-row tiles on
-// routed passes, whose half-empty tail tiles waste MFMA work.  nout: output
-// columns of the pass (F for gate/up, d for down).
-int tile_choice(bool down, int nout) {
-  if (down && nout % 256 != 0) return 10;   // the only down variant for such widths
-  return 5;
-}
-
 int64_t grid_for(int64_t max_rows, int G, int BM, int nn) {
   int64_t upper = (cdiv64(max_rows, BM) + G) * nn;
   upper = ((upper + kXcd - 1) / kXcd) * kXcd;
@@ -1585,6 +1604,32 @@ int num_cus() {
     return n;
   }();
   return cus;
+}
+
+// Tile variant of the LDS-ring GEMMs, per pass: the interleaved 128 x 256
+// x 64 ring with eight waves (5) for every shape, except down passes whose
+// output width is a multiple of 128 but not of 256 (10: 128 x 128 tiles).
+// Measured against it and dropped (block steps, same box):
+// - a register-staged 256 x 256 kernel on dense gate/up (Llama-4-Scout-shaped
+//   shared expert 1317 -> 1232 us for the ring);
+// - 256-row tiles on routed passes, whose half-empty tail tiles waste MFMA
+//   work;
+// - 256 x 256 tiles (eight waves of 128 x 64, two 64 KB slots, 16 x 16 x 32
+//   MFMAs) on dense passes.  Alone they are faster on the DeepSeek-V3-shaped
+//   shared expert (gate/up 195 -> 184 us, down 119 -> 111 us), but their
+//   workgroups hold a whole CU's registers, and in the block, where the
+//   shared passes run beside the Dispatch stand-in copy, the copy's cost
+//   moves to whichever pass it overlaps: gate/up alone on them, 380 -> 230
+//   us, shared down 133 -> 399 us, step 3.78 -> 3.93 ms.  Llama-4-Scout-shaped
+//   shared gate/up (eight rounds of tiles) 1215 -> 1402 us;
+// - two K groups of four waves on the 128 x 256 tile (each wave 64 x 128
+//   over every other 32-wide K step, partial sums added in LDS): a quarter
+//   fewer LDS fragment reads, yet Llama-4-Scout-shaped routed gate/up 1390
+//   -> 1408 us, DeepSeek-V3-shaped down 977 -> 1050 us.
+// nout: output columns of the pass (F for gate/up, d for down).
+int tile_choice(bool down, int nout) {
+  if (down && nout % 256 != 0) return 10;   // the only down variant for such widths
+  return 5;
 }
 
 // occ workgroups per compute unit (capped by the tile count, a multiple of 8).
@@ -1613,14 +1658,18 @@ void run_il(const bf16_t* A, const int32_t* rows, const int32_t* goff, int G, in
             const KSplit& sp = KSplit{}) {
   constexpr int NCOL = MODE == MODE_GATEUP ? BN / 2 : BN;
   const int64_t g = persistent_grid(m_total, G, BM, NOUT / NCOL * sp.splits, OCC);
-  if (sp.splits > 1)
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM, WGN, M16>, (unsigned)g,
-             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
-             sp.splits, sp.kps, sp.P);
-  else
-    launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM, WGN, M16>, (unsigned)g,
-             64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
-             K / BK, nullptr);
+  // (split K: the 128 x 256 ring only)
+  if constexpr (BM == 128 && BN == 256) {
+    if (sp.splits > 1) {
+      launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, true, WGM, WGN, M16>, (unsigned)g,
+               64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr,
+               sp.splits, sp.kps, sp.P);
+      return;
+    }
+  }
+  launch_k(gemm_bf16_il_kernel<MODE, BM, BN, BK, ST, OCC, false, false, WGM, WGN, M16>, (unsigned)g,
+           64 * WGM * WGN, 0, s, A, rows, goff, G, m_total, B, K, NOUT, C, ldc, nullptr, nullptr, 1,
+           K / BK, nullptr);
 }
 template <int MODE, int BM, int BN, int ST, int WGM = 2, int WGN = 2>
 void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G, int64_t m_total,
@@ -1639,8 +1688,8 @@ void run_il_f8(const uint8_t* A, const int32_t* rows, const int32_t* goff, int G
 }
 // Variant 5 has BN = 256 and BK = 64: it needs NOUT % 128 == 0 for
 // gate/up, NOUT % 256 == 0 for down and K % 64 == 0.  Variant 10 (down
-// only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to the
-// interleaved variant 5 only.)
+// only) has 128 x 128 tiles for NOUT % 128 == 0.  (A K split applies to
+// variant 5 only.)
 template <int MODE>
 void gemm_pass(int v, const bf16_t* A, const int32_t* rows, const int32_t* goff, int G,
                int64_t m_total, const bf16_t* B, int K, int NOUT, bf16_t* C, int ldc,

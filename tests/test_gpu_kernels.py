@@ -88,6 +88,10 @@ ROUTER_EXTRA = {
     # slices (the last 128 wide), workgroup 28 taking slices 56 and 57
     "e16_two_slices": CONFIGS["scout"].scaled(n_tokens=2148, hidden=14720, ffn=256,
                                               ffn_shared=256, name="e16_two_slices"),
+    # decode-sized: 36 slices summed by the top-k kernel (four batches of
+    # eight loads and a ragged tail of four)
+    "decode_36_slices": CONFIGS["dsv3_decode"].scaled(n_tokens=20, hidden=9216, ffn=128,
+                                                      ffn_shared=128, name="decode_36_slices"),
 }
 
 
@@ -110,11 +114,13 @@ def test_router_logits_bitexact_and_topk(name):
         assert rel_err(w.cpu().numpy()[far], w_ref[far]) <= 2e-6
 
 
-# groups of 16, 24, 32 and 64 experts
+# groups of 16, 24, 32 and 64 experts, over 64 to 512 experts (one to
+# eight per lane)
 @pytest.mark.parametrize("score,G,TG,k,E", [("softmax", 1, 1, 4, 40), ("sigmoid", 4, 2, 3, 96),
                                             ("sigmoid", 8, 4, 8, 256), ("softmax", 16, 3, 5, 512),
                                             ("sigmoid", 1, 1, 32, 200), ("sigmoid", 16, 5, 6, 256),
-                                            ("softmax", 4, 2, 4, 256)])
+                                            ("softmax", 4, 2, 4, 256), ("sigmoid", 4, 2, 3, 64),
+                                            ("sigmoid", 4, 3, 4, 128), ("softmax", 8, 2, 6, 192)])
 def test_topk_from_given_logits(score, G, TG, k, E):
     # Quantised logits create exact ties: selection must break them toward
     # the lower expert (softmax compares the logits themselves).
