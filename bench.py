@@ -527,7 +527,8 @@ def main():
             r2 = bench_block(args, CONFIGS[name], torch, L, with_cpu=False)
             res["workloads"][name] = {key: r2[key] for key in (
                 "value", "unit", "ms_per_step", "config", "roofline", "ffn", "permute_frac_hbm",
-                "step_roofline_frac", "block_roofline_frac", "kernels_us", "vendor_reference")
+                "step_roofline_frac", "block_roofline_frac", "kernels_us", "vendor_reference",
+                "shared_beside")
                 if key in r2}
             torch.cuda.empty_cache()
     print(json.dumps(res), flush=True)
@@ -652,8 +653,23 @@ def bench_block(args, cfg, torch, L, with_cpu):
     nxts = [torch.empty_like(wl.x) for _ in xs] if args.overlap else None
     outs = [torch.empty_like(wl.x) for _ in xs] if args.overlap else None
 
-    def step(i, comm_stream):
+    side = torch.cuda.Stream(device=dev)
+
+    def step(i, comm_stream, beside=False):
         j = i % len(xs)
+        if beside:
+            # the shared experts on a side stream beside the routed experts:
+            # GATE, then SHARED on `side` while EXPERTS runs on `compute`;
+            # COMBINE adds into the partial input SHARED wrote, so it waits
+            blk.phase(L.FS_PHASE_GATE, xs[j], compute=compute, comm=comm_stream)
+            side.wait_stream(compute)
+            blk.phase(L.FS_PHASE_SHARED, xs[j], partial_out=partials[j], compute=side,
+                      comm=comm_stream)
+            blk.phase(L.FS_PHASE_EXPERTS, xs[j], compute=compute, comm=comm_stream)
+            compute.wait_stream(side)
+            blk.phase(L.FS_PHASE_COMBINE, xs[j], residual_io=partials[j], compute=compute,
+                      comm=comm_stream)
+            return
         blk.begin(xs[j], partials[j], compute=compute, comm=comm_stream)
         if args.overlap:
             # the far-skipped next layer reads the partial input while the
@@ -666,15 +682,25 @@ def bench_block(args, cfg, torch, L, with_cpu):
         else:
             blk.finish(xs[j], partials[j], compute=compute, comm=comm_stream)
 
-    def timed(comm_stream):
+    def timed(comm_stream, beside=False):
         n = [0]
 
         def run():
-            step(n[0], comm_stream)
+            step(n[0], comm_stream, beside)
             n[0] += 1
         return time_steps(L, run, args.steps, args.warmup, compute)
 
     ms, kernels = timed(comm)
+    shared_beside = None
+    if comm is not None and not args.overlap:
+        # the same step with the shared experts beside the routed experts;
+        # the two passes then share the GPU, so the per-kernel table and the
+        # roofline stay the default schedule's
+        ms_sb, _ = timed(comm, beside=True)
+        shared_beside = {"ms_per_step": ms_sb, "tokens_per_s": cfg.n_tokens / (ms_sb * 1e-3),
+                         "note": "shared experts on a side stream beside the routed experts "
+                                 "(GATE; SHARED on the side stream while EXPERTS runs; COMBINE "
+                                 "after both), same kernels and results"}
     serial = timed(None) if (args.overlap and comm is not None) else None
     graph = None
     if args.graph:
@@ -824,6 +850,8 @@ def bench_block(args, cfg, torch, L, with_cpu):
         res["overlap"] = overlap
     if graph is not None:
         res["graph"] = graph
+    if shared_beside is not None:
+        res["shared_beside"] = shared_beside
     if fp8_routed:
         res["grouped_gemm_frac_bf16_peak"] = None
         res["grouped_gemm_frac_fp8_peak"] = None if roof is None else roof["mfma_frac"]

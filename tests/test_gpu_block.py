@@ -130,6 +130,38 @@ def test_two_stream_run_is_race_free(name):
     blk.close()
 
 
+@pytest.mark.parametrize("name", ["tiny", "dsv2lite_s", "dsv3_prefill_s", "dsv3_decode_s"])
+def test_shared_experts_beside_routed_equal_default(name):
+    # The shared experts may run on a side stream while the routed experts
+    # run (GATE; SHARED on the side stream; EXPERTS; COMBINE once SHARED is
+    # done): the same kernels, disjoint workspace regions, so the block's
+    # output equals the default order bit for bit.  The partial input is
+    # NaN-poisoned first, so COMBINE reading it before SHARED wrote it shows.
+    cfg = SMALL[name]
+    wl = make_workload(cfg, DEV)
+    blk = build_block(cfg, wl)
+    x = wl.x
+    compute = torch.cuda.current_stream()
+    comm, side = torch.cuda.Stream(), torch.cuda.Stream()
+    want = torch.empty_like(x)
+    blk.begin(x, want, compute=compute, comm=comm)
+    blk.finish(x, want, compute=compute, comm=comm)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        got = torch.full_like(x, float("nan"))
+        torch.cuda.synchronize()
+        blk.phase(L.FS_PHASE_GATE, x, compute=compute, comm=comm)
+        side.wait_stream(compute)
+        blk.phase(L.FS_PHASE_SHARED, x, partial_out=got, compute=side, comm=comm)
+        blk.phase(L.FS_PHASE_EXPERTS, x, compute=compute, comm=comm)
+        compute.wait_stream(side)
+        blk.phase(L.FS_PHASE_COMBINE, x, residual_io=got, compute=compute, comm=comm)
+        torch.cuda.synchronize()
+        assert not torch.isnan(got).any()
+        assert torch.equal(got, want)
+    blk.close()
+
+
 @pytest.mark.parametrize("name", ["tiny", "scout_s", "dsv3_decode_s"])
 def test_zero_moe_output_farskip_equals_regular(name):
     # Eq. 6 vs Eq. 7 with a zero routed output: the two connectivities are
