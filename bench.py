@@ -495,6 +495,9 @@ def main():
                     help="workgroups of each link-paced stand-in copy")
     ap.add_argument("--vendor-reference", action="store_true",
                     help="also time the block's GEMM passes as plain hipBLASLt GEMMs (context)")
+    ap.add_argument("--no-shared-beside", action="store_true",
+                    help="skip the extra timing of the side-stream phase order (kernel traces "
+                         "then hold the default order's launches only)")
     ap.add_argument("--overlap", action="store_true",
                     help="run the next-layer stand-in (d x d linear) between BEGIN and FINISH and "
                          "compare with a serial run")
@@ -692,7 +695,7 @@ def bench_block(args, cfg, torch, L, with_cpu):
 
     ms, kernels = timed(comm)
     shared_beside = None
-    if comm is not None and not args.overlap:
+    if comm is not None and not args.overlap and not getattr(args, "no_shared_beside", False):
         # the same step with the shared experts beside the routed experts;
         # the two passes then share the GPU, so the per-kernel table and the
         # roofline stay the default schedule's
